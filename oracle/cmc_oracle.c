@@ -1,0 +1,307 @@
+/*
+ * CPU oracle for the CMC two-tier decode path.  TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously correct statement of what the path computes,
+ * in fp64, written from the paper (Sec. 2.5, "Inference with Two-Tier KV
+ * Cache Policy").  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load this library; the product path never does.  It
+ * shares no code, header, table or constant with the HIP library.
+ *
+ * Inputs arrive as the exact bits both sides receive (fp32, or bf16 as raw
+ * 16-bit patterns); every value is widened losslessly to double and all
+ * arithmetic is double.  Readings of points the paper leaves open:
+ *   - cosine denominator: max(||m_j||, 1e-8) * max(||q||, 1e-8), so a zero
+ *     row or question scores 0;
+ *   - exact score ties at the top-k boundary go to the lower index (earlier
+ *     document position);
+ *   - the Tier-2 window is a ring of capacity W holding the most recent W
+ *     tokens; slot (count + t) mod W receives the t-th appended row;
+ *   - decode attention is ordinary softmax attention with z = scale * <q,k>
+ *     over the explicit key list [pool rows idx[0..k-1]] ++ [ring slots
+ *     0..min(count,W)-1]; query head h reads kv head h / (Hq/Hkv); an empty
+ *     key list yields a zero output row.
+ *
+ * Parity pins: tests check this file against exact-rational ranking,
+ * list-history attention written without ring arithmetic, a library SDPA
+ * special case, closed forms and invariants.
+ *
+ * Every entry point returns 0 on success and a positive code on an invalid
+ * argument (nothing is written then).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_BAD_ARG 1
+#define ORACLE_BAD_INDEX 2
+#define ORACLE_NO_MEMORY 3
+
+/* bf16 -> double: the bf16 pattern is the top half of an fp32 pattern. */
+static double widen_bf16(uint16_t h)
+{
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static double load_elem(const void *base, int is_bf16, size_t i)
+{
+    if (is_bf16)
+        return widen_bf16(((const uint16_t *)base)[i]);
+    return (double)((const float *)base)[i];
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* ------------------------------------------------------------------ */
+/* Tier-1 scoring and top-K selection (Sec. 2.5, Tier-1 paragraph and  */
+/* its cosine score equation; M is the row-wise concatenation of the   */
+/* segments' memory vectors in document order, Sec. 2.3 eq. for M).    */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    double s;
+    int j;
+} ranked;
+
+/* Descending score; equal scores: ascending index (earlier position). */
+static int by_rank(const void *a, const void *b)
+{
+    const ranked *x = (const ranked *)a, *y = (const ranked *)b;
+    if (x->s > y->s) return -1;
+    if (x->s < y->s) return 1;
+    return (x->j > y->j) - (x->j < y->j);
+}
+
+static int by_value(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+/*
+ * sel_keys [B][N][D] fp32, q_vec [B][D] fp32.
+ * idx_out  [B][k] int32: the K best-scoring rows, written in ascending order
+ *          ("re-ordered by original document position").
+ * scores_out [B][N] double cosine scores, or NULL.
+ * gap_out  [B] double, or NULL: (s_(k) - s_(k+1)) / |s_(k)| for the k-th and
+ *          (k+1)-th largest scores; +inf when k == 0 or k == N.
+ */
+int oracle_select(const float *sel_keys, const float *q_vec, int B, int N, int D, int k,
+                  int32_t *idx_out, double *scores_out, double *gap_out)
+{
+    if (B < 0 || N < 0 || D <= 0 || k < 0 || k > N || (B > 0 && (!sel_keys || !q_vec)))
+        return ORACLE_BAD_ARG;
+    if (B > 0 && k > 0 && !idx_out)
+        return ORACLE_BAD_ARG;
+    ranked *all = (ranked *)malloc(sizeof(ranked) * (size_t)(N > 0 ? N : 1) * (size_t)(B > 0 ? B : 1));
+    if (!all)
+        return ORACLE_NO_MEMORY;
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+        const float *q = q_vec + (size_t)b * D;
+        double qq = 0.0;
+        for (int d = 0; d < D; ++d)
+            qq += (double)q[d] * (double)q[d];
+        double qn = sqrt(qq);
+        ranked *r = all + (size_t)b * N;
+        for (int j = 0; j < N; ++j) {
+            const float *m = sel_keys + ((size_t)b * N + j) * D;
+            double dot = 0.0, mm = 0.0;
+            for (int d = 0; d < D; ++d) {
+                dot += (double)m[d] * (double)q[d];
+                mm += (double)m[d] * (double)m[d];
+            }
+            double mn = sqrt(mm);
+            double s = dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));
+            r[j].s = s;
+            r[j].j = j;
+            if (scores_out)
+                scores_out[(size_t)b * N + j] = s;
+        }
+        qsort(r, (size_t)N, sizeof(ranked), by_rank);
+        int32_t *out = idx_out ? idx_out + (size_t)b * k : NULL;
+        for (int i = 0; i < k; ++i)
+            out[i] = r[i].j;
+        if (k > 0)
+            qsort(out, (size_t)k, sizeof(int32_t), by_value);
+        if (gap_out) {
+            double g;
+            if (k == 0 || k == N) {
+                g = INFINITY;
+            } else {
+                double hi = r[k - 1].s, lo = r[k].s;
+                double den = fabs(hi);
+                g = den > 0.0 ? (hi - lo) / den : (hi > lo ? INFINITY : 0.0);
+            }
+            gap_out[b] = g;
+        }
+    }
+    free(all);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Tier-2 window (Sec. 2.5, Tier-2 paragraph and its window equation;  */
+/* the cache bound K + W + |q| in the KV cache assembly paragraph).    */
+/* ------------------------------------------------------------------ */
+
+/* start = max(0, min(|C| - W, alpha - W/2)), W/2 taken as floor(W/2). */
+long long oracle_window_start(long long ctx_len, long long W, long long alpha)
+{
+    long long s = alpha - W / 2;
+    long long hi = ctx_len - W;
+    if (s > hi) s = hi;
+    if (s < 0) s = 0;
+    return s;
+}
+
+/*
+ * Ring append.  win_k/win_v [B][Hkv][W][Dh], new_k/new_v [B][Hkv][T_new][Dh],
+ * elements of elem_bytes (2 or 4) bytes, copied verbatim.  For each sequence,
+ * row t goes to slot (count + t) mod W, then count += T_new.  W == 0 means
+ * there is no Tier-2: nothing is touched.
+ */
+int oracle_window_append(void *win_k, void *win_v, int elem_bytes, int32_t *win_count,
+                         const void *new_k, const void *new_v,
+                         int B, int Hkv, int W, int Dh, int T_new)
+{
+    if (B < 0 || Hkv <= 0 || W < 0 || Dh <= 0 || (elem_bytes != 2 && elem_bytes != 4))
+        return ORACLE_BAD_ARG;
+    if (W == 0)
+        return ORACLE_OK;
+    if (T_new < 1 || T_new > W)
+        return ORACLE_BAD_ARG;
+    size_t row = (size_t)Dh * (size_t)elem_bytes;
+    for (int b = 0; b < B; ++b)
+        if (win_count[b] < 0)
+            return ORACLE_BAD_ARG;
+    for (int b = 0; b < B; ++b) {
+        int32_t c = win_count[b];
+        for (int t = 0; t < T_new; ++t) {
+            int slot = (int)(((long long)c + t) % W);
+            for (int h = 0; h < Hkv; ++h) {
+                size_t dst = (((size_t)b * Hkv + h) * W + slot) * row;
+                size_t src = (((size_t)b * Hkv + h) * T_new + t) * row;
+                memcpy((char *)win_k + dst, (const char *)new_k + src, row);
+                memcpy((char *)win_v + dst, (const char *)new_v + src, row);
+            }
+        }
+        win_count[b] = c + T_new;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Two-tier decode attention (Sec. 2.5, KV cache assembly: the frozen  */
+/* decoder attends over [M* || C_local] (+ question rows, which a      */
+/* caller passes as extra pool rows), a cache bounded by K + W + |q|). */
+/* ------------------------------------------------------------------ */
+
+/*
+ * q       [B][Hq][Dh] fp32
+ * cme_k/v [B][Hkv][N][Dh] (bf16 bits or fp32)
+ * idx     [B][k] int32 rows of the pool, or NULL for rows 0..k-1
+ * win_k/v [B][Hkv][W][Dh] ring, valid slots 0..min(count, W)-1
+ * out     [B][Hq][Dh] double
+ */
+int oracle_two_tier_decode(const float *q, const void *cme_k, const void *cme_v, int kv_is_bf16,
+                           const int32_t *idx, int k,
+                           const void *win_k, const void *win_v, const int32_t *win_count, int W,
+                           int B, int Hq, int Hkv, int Dh, int N, double scale, double *out)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Dh <= 0 || N < 0 || k < 0 || W < 0)
+        return ORACLE_BAD_ARG;
+    if (k > N && idx == NULL)
+        return ORACLE_BAD_ARG;
+    for (int b = 0; b < B; ++b) {
+        if (W > 0 && win_count[b] < 0)
+            return ORACLE_BAD_ARG;
+        for (int i = 0; idx && i < k; ++i)
+            if (idx[(size_t)b * k + i] < 0 || idx[(size_t)b * k + i] >= N)
+                return ORACLE_BAD_INDEX;
+    }
+    const int G = Hq / Hkv;
+    int status = ORACLE_OK;
+
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < Hq; ++h) {
+            const int kv = h / G;
+            const int valid = W > 0 ? (win_count[b] < W ? win_count[b] : W) : 0;
+            const int n = k + valid;
+            const float *qh = q + ((size_t)b * Hq + h) * Dh;
+            double *o = out + ((size_t)b * Hq + h) * Dh;
+            double *z = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+            size_t *row = (size_t *)malloc(sizeof(size_t) * (size_t)(n > 0 ? n : 1));
+            const void **kb = (const void **)malloc(sizeof(void *) * (size_t)(n > 0 ? n : 1));
+            const void **vb = (const void **)malloc(sizeof(void *) * (size_t)(n > 0 ? n : 1));
+            if (!z || !row || !kb || !vb) {
+#pragma omp atomic write
+                status = ORACLE_NO_MEMORY;
+                free(z); free(row); free(kb); free(vb);
+                continue;
+            }
+            /* The explicit two-tier key list. */
+            for (int i = 0; i < k; ++i) {
+                int r = idx ? idx[(size_t)b * k + i] : i;
+                row[i] = (((size_t)b * Hkv + kv) * N + (size_t)r) * Dh;
+                kb[i] = cme_k;
+                vb[i] = cme_v;
+            }
+            for (int s = 0; s < valid; ++s) {
+                row[k + s] = (((size_t)b * Hkv + kv) * W + (size_t)s) * Dh;
+                kb[k + s] = win_k;
+                vb[k + s] = win_v;
+            }
+            /* Logits and their maximum. */
+            double m = -INFINITY;
+            for (int i = 0; i < n; ++i) {
+                double acc = 0.0;
+                for (int d = 0; d < Dh; ++d)
+                    acc += (double)qh[d] * load_elem(kb[i], kv_is_bf16, row[i] + d);
+                z[i] = scale * acc;
+                if (z[i] > m) m = z[i];
+            }
+            /* Softmax-weighted sum of the values. */
+            double den = 0.0;
+            for (int i = 0; i < n; ++i) {
+                z[i] = exp(z[i] - m);
+                den += z[i];
+            }
+            for (int d = 0; d < Dh; ++d) {
+                double acc = 0.0;
+                for (int i = 0; i < n; ++i)
+                    acc += z[i] * load_elem(vb[i], kv_is_bf16, row[i] + d);
+                o[d] = n > 0 ? acc / den : 0.0;
+            }
+            free(z); free(row); free(kb); free(vb);
+        }
+    }
+    return status;
+}

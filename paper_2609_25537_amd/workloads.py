@@ -1,0 +1,256 @@
+"""Seeded synthetic workloads for the two-tier decode path.
+
+This module draws random numbers and nothing else: it holds none of the
+method's arithmetic (no scoring, no selection, no attention). Both the HIP
+path and the CPU oracle are fed from it, so it imports neither.
+
+Every tensor comes from its own counter-keyed stream,
+``numpy.random.default_rng([seed, role, layer, ...])``, so any slice
+(a sequence, a head, a decode step) can be regenerated on its own without
+drawing the rest.  bf16 tensors are produced by drawing fp32 values and
+rounding them to bf16 with round-to-nearest-even; they are returned as the
+raw 16-bit patterns (``numpy.uint16``).
+
+The shapes follow the Llama/Mistral-class decoders the paper evaluates
+(Sec. 3, efficiency study; App. A.5 geometry n_h, d_h, n_l), with Tier-1
+size k and window W as in Sec. 2.5.  The paper's own efficiency runs use
+SQuAD, which is not available here; these synthetic inputs stand in for it.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+# Stream roles: part of the seed key of every draw.
+ROLE = {
+    "sel_keys": 1,   # decoder-ready memory rows M (selection keys)
+    "q_vec": 2,      # mean-pooled question vector
+    "cme_k": 3,      # Tier-1 pool keys, one row per CME
+    "cme_v": 4,      # Tier-1 pool values
+    "win_k": 5,      # initial Tier-2 window keys (prefilled C_local)
+    "win_v": 6,      # initial Tier-2 window values
+    "q": 7,          # per-step decoder queries
+    "new_k": 8,      # per-step appended key row
+    "new_v": 9,      # per-step appended value row
+    "chan": 10,      # log-normal per-channel scale
+    "full_k": 11,    # uncompressed-cache baseline keys
+    "full_v": 12,    # uncompressed-cache baseline values
+}
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One synthetic decode workload.
+
+    B batch, Hq/Hkv query/key-value heads, Dh head dim, N CMEs per
+    sequence, D selection-key dim, k Tier-1 size, W window capacity,
+    steps decode steps, layers decoder layers sharing one index list.
+    ``kv_dtype`` is "f32" or "bf16"; selection keys, q_vec and decoder
+    queries are always fp32.  ``kv_std`` is the standard deviation of the
+    K/V/query draws before any channel scale; ``chan_sigma`` > 0 multiplies
+    K and V by exp(N(0, chan_sigma^2)) per (kv head, channel).
+    ``full_ctx`` > 0 describes an uncompressed-cache baseline of that many
+    prefilled tokens.
+    """
+
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    Dh: int
+    N: int
+    D: int
+    k: int
+    W: int
+    steps: int
+    kv_dtype: str
+    kv_std: float
+    seed: int
+    layers: int = 1
+    chan_sigma: float = 0.0
+    full_ctx: int = 0
+    gap_min: float = 1e-3
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.Dh)
+
+    @property
+    def kv_bytes(self) -> int:
+        return 2 if self.kv_dtype == "bf16" else 4
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    # Tiny fp32 single layer: the correctness case.
+    "tiny_fp32": Workload("tiny_fp32", B=1, Hq=4, Hkv=4, Dh=64, N=64, D=256, k=16,
+                          W=128, steps=16, kv_dtype="f32", kv_std=1.0, seed=101),
+    # One Llama-3-8B-shaped layer: 8192-token context at ratio 4 -> 2048 CMEs.
+    "llama3_8b_layer": Workload("llama3_8b_layer", B=1, Hq=32, Hkv=8, Dh=128, N=2048,
+                                D=4096, k=256, W=512, steps=3000, kv_dtype="bf16",
+                                kv_std=1.0 / math.sqrt(128.0), seed=202),
+    # Mistral-7B-shaped batched decode, per-sequence pools and index lists.
+    "mistral7b_batch64": Workload("mistral7b_batch64", B=64, Hq=32, Hkv=8, Dh=128,
+                                  N=4096, D=4096, k=512, W=1024, steps=3000,
+                                  kv_dtype="bf16", kv_std=1.0 / math.sqrt(128.0),
+                                  seed=303),
+    # Long-context wide-head layer: 131072 tokens at ratio 8 -> 16384 CMEs.
+    "long_wide_d256": Workload("long_wide_d256", B=16, Hq=16, Hkv=16, Dh=256, N=16384,
+                               D=3072, k=1024, W=2048, steps=3000, kv_dtype="bf16",
+                               kv_std=1.0, seed=404, chan_sigma=1.0),
+    # 32-layer Llama-shaped decode stack; baseline is a 32768-token full cache.
+    "llama_stack32": Workload("llama_stack32", B=32, Hq=32, Hkv=8, Dh=128, N=8192,
+                              D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",
+                              kv_std=1.0 / math.sqrt(128.0), seed=505, layers=32,
+                              full_ctx=32768),
+}
+
+
+def get(name: str) -> Workload:
+    return WORKLOADS[name]
+
+
+# ---------------------------------------------------------------- streams
+
+def _rng(seed: int, role: str, *ids: int) -> np.random.Generator:
+    return np.random.default_rng([int(seed), ROLE[role], *[int(i) for i in ids]])
+
+
+def normal_f32(seed: int, role: str, ids: Sequence[int], shape, std: float = 1.0) -> np.ndarray:
+    """fp32 N(0, std^2) draws from the stream keyed by (seed, role, *ids)."""
+    x = _rng(seed, role, *ids).standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        x *= np.float32(std)
+    return x
+
+
+# ------------------------------------------------------------------ bf16
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (round to nearest, ties to even); return the bits.
+
+    Inputs are finite draws, so NaN handling is not needed here.
+    """
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(h: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to fp32."""
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _kv_cast(w: Workload, x: np.ndarray) -> np.ndarray:
+    return f32_to_bf16_bits(x) if w.kv_dtype == "bf16" else x
+
+
+# ------------------------------------------------------------- selection
+
+def sel_keys(w: Workload, b: Optional[int] = None) -> np.ndarray:
+    """Selection keys M, fp32 N(0,1): [B][N][D], or [N][D] for one sequence."""
+    if b is not None:
+        return normal_f32(w.seed, "sel_keys", (b,), (w.N, w.D))
+    return np.stack([sel_keys(w, i) for i in range(w.B)])
+
+
+def q_vec(w: Workload, b: int, attempt: int = 0) -> np.ndarray:
+    """Question vector for sequence b, fp32 N(0,1) [D]; ``attempt`` picks a
+    fresh draw (used by tests that reject draws with a narrow score gap)."""
+    return normal_f32(w.seed, "q_vec", (b, attempt), (w.D,))
+
+
+def q_vecs(w: Workload, attempts: Optional[Sequence[int]] = None) -> np.ndarray:
+    att = attempts if attempts is not None else [0] * w.B
+    return np.stack([q_vec(w, b, att[b]) for b in range(w.B)])
+
+
+# ------------------------------------------------------------- KV caches
+
+def chan_scale(w: Workload, layer: int = 0) -> Optional[np.ndarray]:
+    """Per (kv head, channel) log-normal scale [Hkv][Dh], or None."""
+    if w.chan_sigma <= 0:
+        return None
+    z = normal_f32(w.seed, "chan", (layer,), (w.Hkv, w.Dh))
+    return np.exp(np.float32(w.chan_sigma) * z).astype(np.float32)
+
+
+def _kv_rows(w: Workload, role: str, layer: int, b: int, h: int, rows: int,
+             scale: Optional[np.ndarray], extra: Sequence[int] = ()) -> np.ndarray:
+    x = normal_f32(w.seed, role, (layer, b, h, *extra), (rows, w.Dh), w.kv_std)
+    if scale is not None:
+        x *= scale[h][None, :]
+    return x
+
+
+def pool_kv(w: Workload, layer: int = 0, b: Optional[int] = None,
+            h: Optional[int] = None, rows: Optional[int] = None):
+    """Tier-1 pool K and V, [B][Hkv][N][Dh] (or one sequence / one head).
+
+    ``rows`` overrides N (the uncompressed baseline uses the same layout
+    with ``full_ctx`` rows and its own roles).
+    """
+    n = w.N if rows is None else rows
+    rk, rv = ("cme_k", "cme_v") if rows is None else ("full_k", "full_v")
+    s = chan_scale(w, layer)
+    bs = range(w.B) if b is None else [b]
+    hs = range(w.Hkv) if h is None else [h]
+    K = np.stack([np.stack([_kv_rows(w, rk, layer, bb, hh, n, s) for hh in hs]) for bb in bs])
+    V = np.stack([np.stack([_kv_rows(w, rv, layer, bb, hh, n, s) for hh in hs]) for bb in bs])
+    if h is not None:
+        K, V = K[:, 0], V[:, 0]
+    if b is not None:
+        K, V = K[0], V[0]
+    return _kv_cast(w, K), _kv_cast(w, V)
+
+
+def window_kv(w: Workload, layer: int = 0, fill: Optional[int] = None):
+    """Initial Tier-2 ring [B][Hkv][W][Dh] and its count [B] (int32).
+
+    The ring starts holding ``fill`` prefilled tokens (default: full, W) in
+    slots 0..fill-1; unused slots are zero.
+    """
+    f = w.W if fill is None else fill
+    s = chan_scale(w, layer)
+    K = np.zeros((w.B, w.Hkv, w.W, w.Dh), np.float32)
+    V = np.zeros((w.B, w.Hkv, w.W, w.Dh), np.float32)
+    for b in range(w.B):
+        for h in range(w.Hkv):
+            if f:
+                K[b, h, :f] = _kv_rows(w, "win_k", layer, b, h, f, s)
+                V[b, h, :f] = _kv_rows(w, "win_v", layer, b, h, f, s)
+    count = np.full((w.B,), f, np.int32)
+    return _kv_cast(w, K), _kv_cast(w, V), count
+
+
+# ------------------------------------------------------------ decode steps
+
+def step_q(w: Workload, step: int, layer: int = 0) -> np.ndarray:
+    """Decoder queries for one step: fp32 [B][Hq][Dh], N(0, kv_std^2)."""
+    return normal_f32(w.seed, "q", (layer, step), (w.B, w.Hq, w.Dh), w.kv_std)
+
+
+def step_new_kv(w: Workload, step: int, layer: int = 0, t_new: int = 1):
+    """Rows appended at one step: [B][Hkv][t_new][Dh] each (K, V)."""
+    s = chan_scale(w, layer)
+    K = normal_f32(w.seed, "new_k", (layer, step), (w.B, w.Hkv, t_new, w.Dh), w.kv_std)
+    V = normal_f32(w.seed, "new_v", (layer, step), (w.B, w.Hkv, t_new, w.Dh), w.kv_std)
+    if s is not None:
+        K *= s[None, :, None, :]
+        V *= s[None, :, None, :]
+    return _kv_cast(w, K), _kv_cast(w, V)
+
+
+def kv_to_f32(w: Workload, x: np.ndarray) -> np.ndarray:
+    """K/V tensor as exact fp32 values (bf16 widened)."""
+    return bf16_bits_to_f32(x) if w.kv_dtype == "bf16" else np.asarray(x, np.float32)

@@ -1,0 +1,57 @@
+"""Mutation check of the pins: each plausible mistake planted in a copy of
+the oracle's source (built on the CPU into a temporary library) must make at
+least one pin fail.  The real oracle is never modified."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# (name, original text, planted mistake)
+MUTANTS = [
+    ("row_norm_dropped", "double s = dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));",
+     "double s = dot / fmax(qn, 1e-8);"),
+    ("question_norm_dropped", "double s = dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));",
+     "double s = dot / fmax(mn, 1e-8);"),
+    ("score_sign", "double s = dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));",
+     "double s = -dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));"),
+    ("tie_break_reversed", "return (x->j > y->j) - (x->j < y->j);",
+     "return (x->j < y->j) - (x->j > y->j);"),
+    ("no_document_order", "qsort(out, (size_t)k, sizeof(int32_t), by_value);",
+     "(void)by_value;"),
+    ("norm_of_query_in_row", "mm += (double)m[d] * (double)m[d];",
+     "mm += (double)q[d] * (double)q[d];"),
+    ("window_start_full_W", "long long s = alpha - W / 2;", "long long s = alpha - W;"),
+    ("window_start_no_clamp_hi", "if (s > hi) s = hi;", "(void)hi;"),
+    ("ring_slot_off_by_one", "int slot = (int)(((long long)c + t) % W);",
+     "int slot = (int)(((long long)c + t + 1) % W);"),
+    ("ring_count_not_advanced", "win_count[b] = c + T_new;", "win_count[b] = c;"),
+    ("gqa_modulo_mapping", "const int kv = h / G;", "const int kv = h % Hkv;"),
+    ("window_always_full", "(win_count[b] < W ? win_count[b] : W)", "W"),
+    ("index_list_ignored", "int r = idx ? idx[(size_t)b * k + i] : i;", "int r = i;"),
+    ("keys_from_values", "kb[i] = cme_k;", "kb[i] = cme_v;"),
+    ("scale_dropped", "z[i] = scale * acc;", "z[i] = acc;"),
+    ("no_max_subtraction", "z[i] = exp(z[i] - m);", "z[i] = exp(z[i]);"),
+    ("no_normaliser", "o[d] = n > 0 ? acc / den : 0.0;", "o[d] = n > 0 ? acc : 0.0;"),
+    ("value_element_index", "acc += z[i] * load_elem(vb[i], kv_is_bf16, row[i] + d);",
+     "acc += z[i] * load_elem(vb[i], kv_is_bf16, row[i] + (Dh - 1 - d));"),
+    ("window_row_stride", "row[k + s] = (((size_t)b * Hkv + kv) * W + (size_t)s) * Dh;",
+     "row[k + s] = (((size_t)b * Hkv + kv) * W + (size_t)(valid - 1 - s) / 2) * Dh;"),
+    ("bf16_widening", "uint32_t u = ((uint32_t)h) << 16;", "uint32_t u = ((uint32_t)h) << 15;"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_kill_mutant(tmp_path, name, old, new):
+    src = open(oracle.SOURCE).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(src.replace(old, new))
+    lib = oracle.compile_source(str(mutated), str(tmp_path / "libmutant.so"))
+    r = subprocess.run([sys.executable, "-m", "tests.pins", lib], cwd=ROOT,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"mutant {name} survived every pin:\n{r.stdout}{r.stderr}"
