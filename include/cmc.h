@@ -1,0 +1,181 @@
+/*
+ * cmc.h -- C ABI of the MI355X (gfx950) two-tier KV-cache decode path of CMC
+ * ("Compressing Long Context into Answer-Aligned Memory Embeddings for LLM
+ * Inference").
+ *
+ * The paper compresses a long context C into decoder-ready memory rows M
+ * (Sec. 2.3, eq. for M) and, at inference, lets the frozen decoder attend to
+ * a two-tier cache (Sec. 2.5):
+ *   Tier-1  the top-K memory rows by cosine similarity to a mean-pooled
+ *           question vector, re-ordered by document position;
+ *   Tier-2  a W-token local window of the context at full resolution;
+ * with the cache bounded by K + W + |q| at every generation step.  This
+ * library implements the per-step hot path of that policy:
+ *   cmc_select_cmes      Tier-1 scoring and top-K selection (once per question)
+ *   cmc_window_append    Tier-2 ring-buffer append (every step)
+ *   cmc_two_tier_decode  decode attention over [selected rows || window]
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
+ *     all memory, including workspaces.  The library never allocates, frees,
+ *     copies to the host or synchronizes.
+ *   - Arrays are dense, row-major, with the shapes given below; every base
+ *     pointer must be 16-byte aligned (else CMC_ERR_UNSUPPORTED).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  CMC_OK means
+ *     the work was enqueued on that stream; device faults surface at the
+ *     caller's next synchronization.
+ *   - Arguments are validated on the host before anything is enqueued.  On
+ *     any non-OK status nothing is enqueued and no output is touched;
+ *     cmc_last_error() then returns a description (thread-local).
+ *   - Values must be finite.  bf16 tensors are passed as their raw 16-bit
+ *     patterns (uint16_t storage).
+ *   - Concurrent calls on different streams must not share output buffers,
+ *     windows or workspaces.
+ */
+#ifndef CMC_H
+#define CMC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cmc_status {
+    CMC_OK = 0,
+    CMC_ERR_INVALID_ARGUMENT = 1,   /* shape/value out of the documented range   */
+    CMC_ERR_UNSUPPORTED = 2,        /* valid but not implemented (dtype, Dh, G, alignment) */
+    CMC_ERR_WORKSPACE_TOO_SMALL = 3,
+    CMC_ERR_HIP = 4                 /* a HIP runtime call or launch failed        */
+} cmc_status;
+
+typedef enum cmc_dtype {
+    CMC_F32 = 0,
+    CMC_BF16 = 1
+} cmc_dtype;
+
+/* ------------------------------------------------------------------------ */
+/* Tier-1 selection.                                                        */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of workspace cmc_select_cmes needs for these sizes (0 is a valid
+ * answer only when B*N == 0).  Returns 0 for invalid sizes. */
+size_t cmc_select_workspace_bytes(int B, int N);
+
+/*
+ * Question-guided top-K selection (Sec. 2.5, Tier-1 paragraph and its score
+ * equation; Eq. 2 of the problem statement, M* = TopK(M, q, K)).
+ *
+ *   sel_keys   [B][N][D] fp32  decoder-ready memory rows m_j of each sequence,
+ *                              row j = document position j (Sec. 2.3, eq. M)
+ *   q_vec      [B][D]    fp32  mean-pooled question embedding q_vec
+ *   idx_out    [B][k]    int32 the k rows with the largest
+ *                              score_j = m_j.q / (max(|m_j|,1e-8) max(|q|,1e-8)),
+ *                              written in ASCENDING order (document order).
+ *                              Equal scores at the boundary: lower index wins.
+ *   scores_out [B][N]    fp32  the cosine scores, or NULL
+ *   workspace  >= cmc_select_workspace_bytes(B, N) bytes, any content
+ *
+ * Limits: B >= 0, 0 <= k <= N <= 32768, D >= 4 and D % 4 == 0.
+ * Arithmetic: fp32 with a fixed reduction order (run-to-run bit-identical).
+ */
+cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec,
+                           int B, int N, int D, int k,
+                           int32_t *idx_out, float *scores_out,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Tier-2 window.                                                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Ring-buffer append keeping the window at its W most recent tokens, which
+ * bounds the cache by K + W + |q| during generation (Sec. 2.5, KV cache
+ * assembly).
+ *
+ *   win_k, win_v   [B][Hkv][W][Dh]     ring storage, updated in place
+ *   win_count      [B] int32           tokens ever appended (read and advanced);
+ *                                      slots 0..min(count,W)-1 are valid
+ *   new_k, new_v   [B][Hkv][T_new][Dh] rows to append; row t of sequence b goes
+ *                                      to slot (count_b + t) mod W, then
+ *                                      count_b += T_new
+ *   kv_dtype       element type of the four K/V arrays
+ *
+ * Limits: Hkv >= 1, Dh in {64, 128, 256}, W >= 0, 1 <= T_new <= W, count_b
+ * >= 0 and count_b + T_new < 2^31.  W == 0 (no Tier-2) is a no-op that
+ * returns CMC_OK and touches nothing.
+ */
+cmc_status cmc_window_append(void *win_k, void *win_v, cmc_dtype kv_dtype, int32_t *win_count,
+                             const void *new_k, const void *new_v,
+                             int B, int Hkv, int W, int Dh, int T_new, void *stream);
+
+/*
+ * Host helper (no device work): the Tier-2 window start of Sec. 2.5,
+ * start = max(0, min(ctx_len - W, alpha - floor(W/2))), for a caller filling
+ * the ring with C[start : start + W] at prefill.
+ */
+long long cmc_window_start(long long ctx_len, long long W, long long alpha);
+
+/* ------------------------------------------------------------------------ */
+/* Two-tier decode attention.                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of workspace cmc_two_tier_decode needs for these sizes; 0 for
+ * invalid sizes. */
+size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W);
+
+/*
+ * One decode step of attention over the two-tier cache (Sec. 2.5, KV cache
+ * assembly: the decoder attends over [M* || C_local] (+ question rows), the
+ * key set being bounded by K + W + |q|).
+ *
+ *   q          [B][Hq][Dh] fp32   this step's queries (positional encoding
+ *                                 already applied by the caller)
+ *   cme_k/v    [B][Hkv][N][Dh]    Tier-1 pool: one K/V row per memory row
+ *   idx        [B][k] int32       pool rows to attend to (any order, values in
+ *                                 [0, N)), or NULL for rows 0..k-1.  Question
+ *                                 rows, when pinned, are extra pool rows here.
+ *   win_k/v    [B][Hkv][W][Dh]    Tier-2 ring; slots 0..min(count_b, W)-1 are used
+ *   win_count  [B] int32          as maintained by cmc_window_append
+ *   scale      logit scale (1/sqrt(Dh) for standard attention)
+ *   out        [B][Hq][Dh] fp32   softmax(scale q K^T) V over the key list
+ *                                 [pool rows idx] ++ [valid ring slots]; query
+ *                                 head h reads kv head h / (Hq/Hkv).  A sequence
+ *                                 whose key list is empty gets a zero row.
+ *   workspace  >= cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W) bytes
+ *
+ * Limits: Hq % Hkv == 0 with Hq/Hkv in {1, 2, 4, 8}; Dh in {64, 128, 256};
+ * 0 <= k <= N when idx == NULL; k + W >= 1; W >= 0.  Index values are not
+ * checked on the device: out-of-range values are undefined behaviour.
+ * Arithmetic: fp32 accumulation, fixed reduction order (run-to-run
+ * bit-identical).
+ */
+cmc_status cmc_two_tier_decode(const float *q,
+                               const void *cme_k, const void *cme_v,
+                               const int32_t *idx, int k,
+                               const void *win_k, const void *win_v,
+                               const int32_t *win_count, int W,
+                               cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                               float scale, float *out,
+                               void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics.                                                             */
+/* ------------------------------------------------------------------------ */
+
+/* Static name of a status code. */
+const char *cmc_status_string(cmc_status s);
+
+/* Thread-local description of the last non-OK return on this thread ("" if
+ * none).  Valid until the next call into the library on the same thread. */
+const char *cmc_last_error(void);
+
+/* Library version string. */
+const char *cmc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CMC_H */

@@ -1,0 +1,222 @@
+"""Thin Python binding of libcmc.so (the C ABI in include/cmc.h).
+
+Argument marshalling only: tensors become device pointers, the current
+torch stream becomes the HIP stream, status codes become exceptions.  Every
+step of the computation runs in the library's HIP kernels; there is no
+fallback path, and a missing library raises.
+
+Names match the C entry points: ``cmc_select_cmes``, ``cmc_window_append``,
+``cmc_two_tier_decode``, the two workspace queries and ``cmc_window_start``.
+bf16 K/V tensors (torch.bfloat16) are passed through as their raw bits.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(_PKG, "libcmc.so")
+
+CMC_OK = 0
+CMC_ERR_INVALID_ARGUMENT = 1
+CMC_ERR_UNSUPPORTED = 2
+CMC_ERR_WORKSPACE_TOO_SMALL = 3
+CMC_ERR_HIP = 4
+CMC_F32 = 0
+CMC_BF16 = 1
+
+EXPORTED = [
+    "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_window_append", "cmc_window_start",
+    "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_status_string", "cmc_last_error",
+    "cmc_version",
+]
+
+
+class CmcError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBRARY):
+            raise RuntimeError(f"{LIBRARY} is missing: build it with __graft_entry__.build() "
+                               "(python -m paper_2609_25537_amd.build)")
+        L = ctypes.CDLL(LIBRARY)
+        P, I, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        L.cmc_select_workspace_bytes.argtypes = [I, I]
+        L.cmc_select_workspace_bytes.restype = SZ
+        L.cmc_select_cmes.argtypes = [P, P, I, I, I, I, P, P, P, SZ, P]
+        L.cmc_select_cmes.restype = I
+        L.cmc_window_append.argtypes = [P, P, I, P, P, P, I, I, I, I, I, P]
+        L.cmc_window_append.restype = I
+        L.cmc_window_start.argtypes = [ctypes.c_longlong] * 3
+        L.cmc_window_start.restype = ctypes.c_longlong
+        L.cmc_decode_workspace_bytes.argtypes = [I, I, I, I, I, I]
+        L.cmc_decode_workspace_bytes.restype = SZ
+        L.cmc_two_tier_decode.argtypes = [P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
+                                          ctypes.c_float, P, P, SZ, P]
+        L.cmc_two_tier_decode.restype = I
+        L.cmc_status_string.argtypes = [I]
+        L.cmc_status_string.restype = ctypes.c_char_p
+        L.cmc_last_error.argtypes = []
+        L.cmc_last_error.restype = ctypes.c_char_p
+        L.cmc_version.argtypes = []
+        L.cmc_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().cmc_status_string(int(s)).decode()
+
+
+def last_error() -> str:
+    return lib().cmc_last_error().decode()
+
+
+def version() -> str:
+    return lib().cmc_version().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != CMC_OK:
+        raise CmcError(rc, last_error())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _kv_dtype(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return CMC_BF16
+    if t.dtype == torch.float32:
+        return CMC_F32
+    raise TypeError(f"K/V tensors must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+# ------------------------------------------------------------- selection
+
+def cmc_select_workspace_bytes(B: int, N: int) -> int:
+    return int(lib().cmc_select_workspace_bytes(int(B), int(N)))
+
+
+def cmc_select_cmes(sel_keys, q_vec, k: int, idx_out=None, scores_out=None, workspace=None,
+                    stream=None):
+    """Tier-1 selection.  sel_keys [B][N][D] fp32, q_vec [B][D] fp32 (device).
+    Returns idx_out [B][k] int32 (ascending)."""
+    import torch
+    _need(sel_keys.dim() == 3 and sel_keys.is_contiguous(), "sel_keys must be contiguous [B][N][D]")
+    B, N, D = sel_keys.shape
+    _need(q_vec.shape == (B, D) and q_vec.is_contiguous(), "q_vec must be contiguous [B][D]")
+    _need(sel_keys.dtype == torch.float32 and q_vec.dtype == torch.float32, "fp32 inputs expected")
+    if idx_out is None:
+        idx_out = torch.empty((B, k), dtype=torch.int32, device=sel_keys.device)
+    _need(idx_out.shape == (B, k) and idx_out.dtype == torch.int32 and idx_out.is_contiguous(),
+          "idx_out must be contiguous int32 [B][k]")
+    if scores_out is not None:
+        _need(scores_out.shape == (B, N) and scores_out.dtype == torch.float32, "scores_out [B][N] fp32")
+    ws_bytes = 0
+    if scores_out is None and workspace is None:
+        workspace = torch.empty(max(1, cmc_select_workspace_bytes(B, N)), dtype=torch.uint8,
+                                device=sel_keys.device)
+    if workspace is not None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_select_cmes(_ptr(sel_keys), _ptr(q_vec), B, N, D, int(k), _ptr(idx_out),
+                               _ptr(scores_out), _ptr(workspace), ws_bytes, _stream(stream))
+    _check(rc)
+    return idx_out
+
+
+# ---------------------------------------------------------------- window
+
+def cmc_window_start(ctx_len: int, W: int, alpha: int) -> int:
+    return int(lib().cmc_window_start(int(ctx_len), int(W), int(alpha)))
+
+
+def cmc_window_append(win_k, win_v, win_count, new_k, new_v, stream=None) -> None:
+    """Ring append in place.  win_* [B][Hkv][W][Dh], new_* [B][Hkv][T][Dh],
+    win_count [B] int32 (all on the device)."""
+    import torch
+    _need(win_k.dim() == 4 and win_k.is_contiguous() and win_v.is_contiguous(), "win_k/v [B][Hkv][W][Dh]")
+    B, Hkv, W, Dh = win_k.shape
+    _need(win_v.shape == win_k.shape and win_v.dtype == win_k.dtype, "win_v must match win_k")
+    _need(new_k.dim() == 4 and new_k.shape[:2] == (B, Hkv) and new_k.shape[3] == Dh, "new_k [B][Hkv][T][Dh]")
+    _need(new_v.shape == new_k.shape and new_k.dtype == win_k.dtype == new_v.dtype, "new_k/v must match")
+    _need(new_k.is_contiguous() and new_v.is_contiguous(), "new_k/v must be contiguous")
+    _need(win_count.shape == (B,) and win_count.dtype == torch.int32, "win_count [B] int32")
+    rc = lib().cmc_window_append(_ptr(win_k), _ptr(win_v), _kv_dtype(win_k), _ptr(win_count),
+                                 _ptr(new_k), _ptr(new_v), B, Hkv, W, Dh, int(new_k.shape[2]),
+                                 _stream(stream))
+    _check(rc)
+
+
+# ---------------------------------------------------------------- decode
+
+def cmc_decode_workspace_bytes(B: int, Hq: int, Hkv: int, Dh: int, k: int, W: int) -> int:
+    return int(lib().cmc_decode_workspace_bytes(int(B), int(Hq), int(Hkv), int(Dh), int(k), int(W)))
+
+
+def cmc_two_tier_decode(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, scale: float,
+                        out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """One decode step over [pool rows idx || ring slots].  q [B][Hq][Dh] fp32,
+    cme_* [B][Hkv][N][Dh], idx [B][k] int32 or None, win_* [B][Hkv][W][Dh] or
+    None (W = 0), win_count [B] int32.  Returns out [B][Hq][Dh] fp32."""
+    import torch
+    _need(q.dim() == 3 and q.is_contiguous() and q.dtype == torch.float32, "q must be contiguous fp32 [B][Hq][Dh]")
+    B, Hq, Dh = q.shape
+    _need(cme_k.dim() == 4 and cme_k.is_contiguous() and cme_v.is_contiguous(), "cme_k/v [B][Hkv][N][Dh]")
+    _need(cme_k.shape[0] == B and cme_k.shape[3] == Dh and cme_v.shape == cme_k.shape, "pool shape")
+    Hkv, N = cme_k.shape[1], cme_k.shape[2]
+    _need(cme_v.dtype == cme_k.dtype, "cme_v dtype must match cme_k")
+    if W is None:
+        W = 0 if win_k is None else win_k.shape[2]
+    if W > 0:
+        _need(win_k.shape == (B, Hkv, W, Dh) and win_v.shape == win_k.shape, "window shape")
+        _need(win_k.dtype == cme_k.dtype == win_v.dtype, "window dtype must match pool")
+        _need(win_k.is_contiguous() and win_v.is_contiguous(), "window must be contiguous")
+        _need(win_count is not None and win_count.shape == (B,) and win_count.dtype == torch.int32,
+              "win_count [B] int32")
+    if idx is not None:
+        _need(idx.shape == (B, k) and idx.dtype == torch.int32 and idx.is_contiguous(), "idx [B][k] int32")
+    if out is None:
+        out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
+    _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
+    if workspace is None:
+        workspace = torch.empty(max(1, cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W)),
+                                dtype=torch.uint8, device=q.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_two_tier_decode(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k),
+                                   _ptr(win_k) if W > 0 else None, _ptr(win_v) if W > 0 else None,
+                                   _ptr(win_count) if W > 0 else None, int(W), _kv_dtype(cme_k),
+                                   B, Hq, Hkv, Dh, N, float(scale), _ptr(out), _ptr(workspace),
+                                   ws_bytes, _stream(stream))
+    _check(rc)
+    return out

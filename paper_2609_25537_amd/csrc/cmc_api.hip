@@ -1,0 +1,218 @@
+// Host side of the C ABI declared in include/cmc.h: argument validation,
+// launch planning and error reporting.  Everything here runs on the host;
+// every computation runs in the kernels of decode.hip, select.hip and
+// window.hip, enqueued on the caller's stream.
+#include <math.h>
+#include <algorithm>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "cmc.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local char g_error[512] = "";
+
+cmc_status fail(cmc_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+cmc_status ok() {
+    g_error[0] = '\0';
+    return CMC_OK;
+}
+
+cmc_status hip_fail(hipError_t e, const char *what) {
+    return fail(CMC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool misaligned(const void *p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u); }
+
+bool supported_dh(int dh) { return dh == 64 || dh == 128 || dh == 256; }
+
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+}  // namespace
+
+namespace cmc {
+
+// Key-axis split plan.  Aim for about kTargetWG workgroups in flight (a few
+// per CU on 256 CUs) without cutting a split below kGranule keys; the plan
+// depends only on sizes, so the workspace query and the launch always agree.
+DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
+    constexpr long long kTargetWG = 1024;
+    constexpr long long kGranule = 32;
+    DecodePlan pl;
+    const long long L = (long long)k + W;
+    const long long pairs = (long long)B * Hkv;
+    if (L <= 0 || pairs <= 0) return pl;
+    const long long s_target = std::max(1LL, (kTargetWG + pairs - 1) / pairs);
+    long long chunk = (L + s_target - 1) / s_target;
+    chunk = ((chunk + kGranule - 1) / kGranule) * kGranule;
+    const long long S = (L + chunk - 1) / chunk;
+    const int G = Hq / Hkv;
+    pl.S = (int)S;
+    pl.chunk = (int)chunk;
+    pl.ml_bytes = align256((size_t)(pairs * S * G * 2) * sizeof(float));
+    pl.acc_bytes = align256((size_t)(pairs * S * G * Dh) * sizeof(float));
+    pl.total = pl.ml_bytes + pl.acc_bytes;
+    return pl;
+}
+
+}  // namespace cmc
+
+extern "C" {
+
+const char *cmc_version(void) { return "cmc-mi355x 0.1 (gfx950)"; }
+
+const char *cmc_status_string(cmc_status s) {
+    switch (s) {
+        case CMC_OK: return "CMC_OK";
+        case CMC_ERR_INVALID_ARGUMENT: return "CMC_ERR_INVALID_ARGUMENT";
+        case CMC_ERR_UNSUPPORTED: return "CMC_ERR_UNSUPPORTED";
+        case CMC_ERR_WORKSPACE_TOO_SMALL: return "CMC_ERR_WORKSPACE_TOO_SMALL";
+        case CMC_ERR_HIP: return "CMC_ERR_HIP";
+    }
+    return "CMC_ERR_UNKNOWN";
+}
+
+const char *cmc_last_error(void) { return g_error; }
+
+long long cmc_window_start(long long ctx_len, long long W, long long alpha) {
+    long long start = alpha - W / 2;
+    if (start > ctx_len - W) start = ctx_len - W;
+    if (start < 0) start = 0;
+    return start;
+}
+
+// ------------------------------------------------------------- selection
+
+size_t cmc_select_workspace_bytes(int B, int N) {
+    if (B < 0 || N < 0) return 0;
+    return align256((size_t)B * (size_t)N * sizeof(float));
+}
+
+cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int N, int D, int k,
+                           int32_t *idx_out, float *scores_out, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    if (B < 0 || N < 0 || k < 0 || D < 4)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "select: need B >= 0, N >= 0, k >= 0, D >= 4 (got B=%d N=%d k=%d D=%d)", B, N, k, D);
+    if (k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "select: k=%d exceeds N=%d", k, N);
+    if (D % 4 != 0) return fail(CMC_ERR_UNSUPPORTED, "select: D=%d must be a multiple of 4", D);
+    if (N > cmc::kSelectMaxN) return fail(CMC_ERR_UNSUPPORTED, "select: N=%d exceeds %d", N, cmc::kSelectMaxN);
+    if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "select: B=%d exceeds 65535", B);
+    if ((long long)B * N == 0) return ok();
+    if (!sel_keys || !q_vec) return fail(CMC_ERR_INVALID_ARGUMENT, "select: sel_keys and q_vec must be non-null");
+    if (k > 0 && !idx_out) return fail(CMC_ERR_INVALID_ARGUMENT, "select: idx_out must be non-null when k > 0");
+    if (misaligned(sel_keys) || misaligned(q_vec) || misaligned(idx_out) || misaligned(scores_out) ||
+        misaligned(workspace))
+        return fail(CMC_ERR_UNSUPPORTED, "select: every pointer must be 16-byte aligned");
+    float *scores = scores_out;
+    if (!scores) {
+        const size_t need = cmc_select_workspace_bytes(B, N);
+        if (!workspace || workspace_bytes < need)
+            return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "select: workspace of %zu bytes needed, %zu given", need,
+                        workspace ? workspace_bytes : (size_t)0);
+        scores = static_cast<float *>(workspace);
+    }
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k};
+    hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "select launch");
+    return ok();
+}
+
+// ---------------------------------------------------------------- window
+
+cmc_status cmc_window_append(void *win_k, void *win_v, cmc_dtype kv_dtype, int32_t *win_count,
+                             const void *new_k, const void *new_v, int B, int Hkv, int W, int Dh,
+                             int T_new, void *stream) {
+    if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
+        return fail(CMC_ERR_UNSUPPORTED, "append: unknown kv_dtype %d", (int)kv_dtype);
+    if (B < 0 || Hkv < 1 || W < 0)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "append: need B >= 0, Hkv >= 1, W >= 0 (got B=%d Hkv=%d W=%d)", B, Hkv, W);
+    if (!supported_dh(Dh)) return fail(CMC_ERR_UNSUPPORTED, "append: Dh=%d not in {64,128,256}", Dh);
+    if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "append: B=%d exceeds 65535", B);
+    if (W == 0 || B == 0) return ok();
+    if (T_new < 1 || T_new > W)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "append: need 1 <= T_new <= W (got T_new=%d W=%d)", T_new, W);
+    if (!win_k || !win_v || !win_count || !new_k || !new_v)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "append: null pointer");
+    if (misaligned(win_k) || misaligned(win_v) || misaligned(win_count) || misaligned(new_k) || misaligned(new_v))
+        return fail(CMC_ERR_UNSUPPORTED, "append: every pointer must be 16-byte aligned");
+    const int elem = kv_dtype == CMC_BF16 ? 2 : 4;
+    cmc::AppendParams p{win_k, win_v, win_count, new_k, new_v, B, Hkv, W, T_new, Dh * elem / 16};
+    hipError_t e = cmc::launch_window_append(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "append launch");
+    return ok();
+}
+
+// ---------------------------------------------------------------- decode
+
+size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W) {
+    if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || k < 0 || W < 0 || !supported_dh(Dh)) return 0;
+    return cmc::plan_decode(B, Hq, Hkv, Dh, k, W).total;
+}
+
+cmc_status cmc_two_tier_decode(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                               int k, const void *win_k, const void *win_v, const int32_t *win_count,
+                               int W, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                               float scale, float *out, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
+        return fail(CMC_ERR_UNSUPPORTED, "decode: unknown kv_dtype %d", (int)kv_dtype);
+    if (B < 0 || Hq < 1 || Hkv < 1 || k < 0 || W < 0 || N < 0)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "decode: need B >= 0, Hq, Hkv >= 1, k, W, N >= 0");
+    if (Hq % Hkv != 0) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
+    const int G = Hq / Hkv;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+        return fail(CMC_ERR_UNSUPPORTED, "decode: Hq/Hkv=%d not in {1,2,4,8}", G);
+    if (!supported_dh(Dh)) return fail(CMC_ERR_UNSUPPORTED, "decode: Dh=%d not in {64,128,256}", Dh);
+    if ((long long)k + W < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: empty cache (k + W = 0)");
+    if (!idx && k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: k=%d exceeds N=%d with idx == NULL", k, N);
+    if (k > 0 && N < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: k=%d rows requested from an empty pool", k);
+    if (!(scale == scale) || isinf(scale)) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: scale must be finite");
+    if (B > 65535 || Hkv > 65535) return fail(CMC_ERR_UNSUPPORTED, "decode: B and Hkv must be <= 65535");
+    if (B == 0) return ok();
+    if (!q || !out) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: q and out must be non-null");
+    if (k > 0 && (!cme_k || !cme_v)) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: null Tier-1 pool");
+    if (W > 0 && (!win_k || !win_v || !win_count))
+        return fail(CMC_ERR_INVALID_ARGUMENT, "decode: null Tier-2 window");
+    if (misaligned(q) || misaligned(cme_k) || misaligned(cme_v) || misaligned(idx) || misaligned(win_k) ||
+        misaligned(win_v) || misaligned(win_count) || misaligned(out) || misaligned(workspace))
+        return fail(CMC_ERR_UNSUPPORTED, "decode: every pointer must be 16-byte aligned");
+    const cmc::DecodePlan pl = cmc::plan_decode(B, Hq, Hkv, Dh, k, W);
+    if (!workspace || workspace_bytes < pl.total)
+        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "decode: workspace of %zu bytes needed, %zu given", pl.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    cmc::DecodeParams p{};
+    p.q = q;
+    p.cme_k = cme_k;
+    p.cme_v = cme_v;
+    p.idx = idx;
+    p.win_k = W > 0 ? win_k : nullptr;
+    p.win_v = W > 0 ? win_v : nullptr;
+    p.win_count = W > 0 ? win_count : nullptr;
+    p.out = out;
+    p.part_ml = static_cast<float *>(workspace);
+    p.part_acc = reinterpret_cast<float *>(static_cast<char *>(workspace) + pl.ml_bytes);
+    p.k = k;
+    p.W = W;
+    p.B = B;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.N = N;
+    p.S = pl.S;
+    p.chunk = pl.chunk;
+    p.qscale = cmc::decode_qscale(scale);
+    hipError_t e = cmc::launch_two_tier_decode(p, kv_dtype == CMC_BF16, G, Dh, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,56 @@
+// Internal launch interface between the C ABI (cmc_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cmc {
+
+struct DecodeParams {
+    const float *q;           // [B][Hq][Dh]
+    const void *cme_k;        // [B][Hkv][N][Dh]
+    const void *cme_v;
+    const int32_t *idx;       // [B][k] or nullptr
+    const void *win_k;        // [B][Hkv][W][Dh]
+    const void *win_v;
+    const int32_t *win_count; // [B]
+    float *out;               // [B][Hq][Dh]
+    float *part_ml;           // [B][Hkv][S][G][2]   (running max in log2 units, denominator)
+    float *part_acc;          // [B][Hkv][S][G][Dh]  (unnormalised numerator)
+    int k, W, B, Hq, Hkv, N;
+    int S, chunk;             // key-axis splits and keys per split
+    float qscale;             // scale * log2(e)
+};
+
+// Key-axis split plan; depends only on sizes, so the workspace query and the
+// launch agree.
+struct DecodePlan {
+    int S = 0, chunk = 0;
+    size_t ml_bytes = 0, acc_bytes = 0, total = 0;
+};
+DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W);
+
+hipError_t launch_two_tier_decode(const DecodeParams &p, bool bf16, int G, int Dh, hipStream_t stream);
+float decode_qscale(float scale);
+
+struct AppendParams {
+    void *win_k, *win_v;
+    int32_t *win_count;
+    const void *new_k, *new_v;
+    int B, Hkv, W, T_new;
+    int row_vecs;             // 16-byte vectors per row (Dh * elem / 16)
+};
+hipError_t launch_window_append(const AppendParams &p, hipStream_t stream);
+
+struct SelectParams {
+    const float *sel_keys;    // [B][N][D]
+    const float *q_vec;       // [B][D]
+    float *scores;            // [B][N]
+    int32_t *idx_out;         // [B][k]
+    int B, N, D, k;
+};
+constexpr int kSelectMaxN = 32768;
+hipError_t launch_select(const SelectParams &p, hipStream_t stream);
+
+}  // namespace cmc

@@ -1,0 +1,196 @@
+// Tier-1 question-guided selection (Sec. 2.5, Tier-1 paragraph and its score
+// equation): score_j = m_j.q / (|m_j| |q|), keep the K best, emit them in
+// document order.
+//
+// score_kernel: one wave per memory row (R rows per wave).  The dot product
+// and |m_j|^2 come out of ONE pass over the row (16-byte loads, fp32 FMA in
+// a fixed per-lane order, then a DPP/permlane butterfly), |q|^2 from the same
+// loop over q.  Zero norms are clamped to 1e-8, so a zero row scores 0.
+//
+// topk_kernel: one 1024-thread workgroup per sequence.  Scores become
+// order-preserving uint32 keys (kept in registers, 32 per thread, so N <=
+// 32768).  The k-th largest key T is found bit by bit from the top: T is the
+// largest value with count(key >= T) >= k, one block-wide count per bit.
+// Then every key > T is taken, plus the first (k - count(key > T)) keys equal
+// to T in index order (ties go to the earlier document position).  Two
+// block-wide exclusive scans over the threads' contiguous index ranges give
+// each selected row its output slot, so idx comes out ascending.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace cmc {
+
+namespace {
+
+template <int R>
+__global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
+    const int b = blockIdx.y;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int j0 = (blockIdx.x * 4 + wave) * R;
+    if (j0 >= p.N) return;  // wave-uniform; no barriers below
+
+    const int D4 = p.D / 4;
+    const float4 *q4 = reinterpret_cast<const float4 *>(p.q_vec + (size_t)b * p.D);
+    const float4 *rows[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = min(j0 + r, p.N - 1);
+        rows[r] = reinterpret_cast<const float4 *>(p.sel_keys + ((size_t)b * p.N + j) * p.D);
+    }
+    float dot[R], nn[R], qq = 0.f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) dot[r] = nn[r] = 0.f;
+
+#pragma unroll 2
+    for (int c = lane; c < D4; c += kWave) {
+        const float4 qv = q4[c];
+        qq = fmaf(qv.x, qv.x, qq);
+        qq = fmaf(qv.y, qv.y, qq);
+        qq = fmaf(qv.z, qv.z, qq);
+        qq = fmaf(qv.w, qv.w, qq);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float4 mv = rows[r][c];
+            dot[r] = fmaf(mv.x, qv.x, dot[r]);
+            dot[r] = fmaf(mv.y, qv.y, dot[r]);
+            dot[r] = fmaf(mv.z, qv.z, dot[r]);
+            dot[r] = fmaf(mv.w, qv.w, dot[r]);
+            nn[r] = fmaf(mv.x, mv.x, nn[r]);
+            nn[r] = fmaf(mv.y, mv.y, nn[r]);
+            nn[r] = fmaf(mv.z, mv.z, nn[r]);
+            nn[r] = fmaf(mv.w, mv.w, nn[r]);
+        }
+    }
+    qq = lane_reduce<OpSum, 1, kWave>(qq);
+    const float qn = fmaxf(sqrtf(qq), 1e-8f);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float d = lane_reduce<OpSum, 1, kWave>(dot[r]);
+        const float n2 = lane_reduce<OpSum, 1, kWave>(nn[r]);
+        const int j = j0 + r;
+        if (lane == 0 && j < p.N) p.scores[(size_t)b * p.N + j] = d / (fmaxf(sqrtf(n2), 1e-8f) * qn);
+    }
+}
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    if (u == 0x80000000u) u = 0u;  // -0 ranks as +0
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkWaves = kTopkThreads / kWave;
+constexpr int kPerThread = kSelectMaxN / kTopkThreads;  // 32
+
+// Block-wide sum of an integer count (< 2^24, exact in fp32); every thread
+// gets the same total.  `slot` alternates between two LDS rows so one barrier
+// per call suffices.
+__device__ __forceinline__ int block_count(int v, float (*s_part)[kTopkWaves], int &slot) {
+    const float w = lane_reduce<OpSum, 1, kWave>((float)v);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) s_part[slot][wave] = w;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < kTopkWaves; ++i) t += s_part[slot][i];
+    slot ^= 1;
+    return (int)t;
+}
+
+// Block-wide exclusive prefix sum of v over thread order.
+__device__ __forceinline__ int block_exclusive_scan(int v, int *s_wave) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+    }
+    if (lane == kWave - 1) s_wave[wave] = x;
+    __syncthreads();
+    int base = 0;
+    for (int i = 0; i < wave; ++i) base += s_wave[i];
+    __syncthreads();  // s_wave may be reused by the next scan
+    return base + x - v;
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int N = p.N, k = p.k;
+    const int per = (N + kTopkThreads - 1) / kTopkThreads;  // <= kPerThread
+    const int j0 = tid * per;
+    const int cnt = max(0, min(per, N - j0));
+
+    __shared__ float s_part[2][kTopkWaves];
+    __shared__ int s_wave[kTopkWaves];
+    int slot = 0;
+
+    uint32_t key[kPerThread];
+    const float *sc = p.scores + (size_t)b * N;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) key[i] = i < cnt ? order_key(sc[j0 + i]) : 0u;
+
+    // T = largest value with count(key >= T) >= k.
+    uint32_t T = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = T | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) c += (i < cnt && key[i] >= cand) ? 1 : 0;
+        if (block_count(c, s_part, slot) >= k) T = cand;
+    }
+
+    int gt = 0, eq = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        gt += (i < cnt && key[i] > T) ? 1 : 0;
+        eq += (i < cnt && key[i] == T) ? 1 : 0;
+    }
+    const int need_eq = k - block_count(gt, s_part, slot);
+    int eq_seen = block_exclusive_scan(eq, s_wave);
+
+    int take = 0;
+    uint32_t mask = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        bool sel = false;
+        if (i < cnt) {
+            if (key[i] > T) {
+                sel = true;
+            } else if (key[i] == T) {
+                sel = eq_seen < need_eq;
+                ++eq_seen;
+            }
+        }
+        if (sel) {
+            mask |= 1u << i;
+            ++take;
+        }
+    }
+    int pos = block_exclusive_scan(take, s_wave);
+    int32_t *out = p.idx_out + (size_t)b * k;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i)
+        if (mask & (1u << i)) out[pos++] = j0 + i;
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectParams &p, hipStream_t stream) {
+    if (p.B == 0 || p.N == 0) return hipSuccess;
+    const long long rows = (long long)p.B * p.N;
+    if (rows >= 65536) {
+        dim3 grid((p.N + 15) / 16, p.B);
+        score_kernel<4><<<grid, 256, 0, stream>>>(p);
+    } else {
+        dim3 grid((p.N + 3) / 4, p.B);
+        score_kernel<1><<<grid, 256, 0, stream>>>(p);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.k == 0) return e;
+    topk_kernel<<<p.B, kTopkThreads, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace cmc

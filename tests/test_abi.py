@@ -1,0 +1,126 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header
+declares, and its host-side validation returns the documented codes before
+touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_25537_amd import cmc
+from tests import pins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(cmc_[a-z0-9_]+)\s*\(", src))
+    return names
+
+
+def test_exports_every_declared_symbol():
+    declared = _declared()
+    assert {"cmc_select_cmes", "cmc_window_append", "cmc_two_tier_decode"} <= declared
+    L = cmc.lib()
+    for name in sorted(declared):
+        assert hasattr(L, name), name
+    assert set(cmc.EXPORTED) == declared
+
+
+def test_status_strings():
+    assert cmc.status_string(cmc.CMC_OK) == "CMC_OK"
+    assert cmc.status_string(cmc.CMC_ERR_WORKSPACE_TOO_SMALL) == "CMC_ERR_WORKSPACE_TOO_SMALL"
+    assert "gfx950" in cmc.version()
+
+
+def test_window_start_matches_golden():
+    for c in pins._golden()["window_start"]["cases"]:
+        assert cmc.cmc_window_start(c["ctx_len"], c["W"], c["alpha"]) == c["start"]
+
+
+FAKE = 1 << 20  # 16-byte aligned non-null address, never dereferenced: calls below fail validation first
+
+
+@pytest.mark.parametrize("args,code", [
+    ((FAKE, FAKE, 1, 4, 8, 5, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),   # k > N
+    ((FAKE, FAKE, 1, 4, 6, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),        # D % 4
+    ((FAKE, FAKE, 1, 40000, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),    # N too big
+    ((FAKE, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 16, None), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    ((None, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    ((FAKE + 4, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),   # alignment
+    ((FAKE, FAKE, 2, 64, 8, -1, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),
+])
+def test_select_validation(args, code):
+    assert cmc.lib().cmc_select_cmes(*args) == code
+    assert cmc.last_error()
+
+
+def test_select_empty_is_ok():
+    assert cmc.lib().cmc_select_cmes(None, None, 0, 10, 8, 3, None, None, None, 0, None) == cmc.CMC_OK
+    assert cmc.last_error() == ""
+
+
+def _dec(**kw):
+    a = dict(q=FAKE, ck=FAKE, cv=FAKE, idx=FAKE, k=4, wk=FAKE, wv=FAKE, wc=FAKE, W=8, dt=cmc.CMC_BF16,
+             B=1, Hq=8, Hkv=2, Dh=128, N=16, scale=0.1, out=FAKE, ws=FAKE, wsb=1 << 30, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_two_tier_decode(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hq=6, Hkv=4), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(Hq=12, Hkv=4), cmc.CMC_ERR_UNSUPPORTED),       # G = 3
+    (dict(Dh=96), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(k=0, W=0), cmc.CMC_ERR_INVALID_ARGUMENT),       # empty cache
+    (dict(idx=None, k=17), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(k=3, N=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(dt=7), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(wsb=64), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    (dict(ws=None), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    (dict(out=FAKE + 8), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(wc=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(q=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(scale=float("nan")), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(B=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
+])
+def test_decode_validation(kw, code):
+    assert _dec(**kw) == code
+
+
+def test_decode_empty_batch_ok():
+    assert _dec(B=0) == cmc.CMC_OK
+
+
+def test_decode_workspace_query():
+    assert cmc.cmc_decode_workspace_bytes(1, 32, 8, 128, 256, 512) > 0
+    assert cmc.cmc_decode_workspace_bytes(1, 32, 7, 128, 256, 512) == 0
+    assert cmc.cmc_decode_workspace_bytes(1, 32, 8, 100, 256, 512) == 0
+    assert cmc.cmc_decode_workspace_bytes(1, 32, 8, 128, 0, 0) == 0
+
+
+def _app(**kw):
+    a = dict(wk=FAKE, wv=FAKE, dt=cmc.CMC_BF16, wc=FAKE, nk=FAKE, nv=FAKE, B=2, Hkv=2, W=8, Dh=128, T=1, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_window_append(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(T=9), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(Dh=80), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(Hkv=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(nk=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(wc=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(dt=3), cmc.CMC_ERR_UNSUPPORTED),
+])
+def test_append_validation(kw, code):
+    assert _app(**kw) == code
+
+
+def test_append_without_window_is_noop():
+    assert _app(W=0, wk=None, wv=None, wc=None, T=5) == cmc.CMC_OK

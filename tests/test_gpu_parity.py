@@ -1,0 +1,244 @@
+"""HIP path vs the CPU oracle, through the C ABI, on identical input bits.
+
+Selection: index sets bit-exact.  Attention: max-abs 1e-5 (fp32 K/V) or
+2e-3 (bf16 K/V) against the fp64 oracle.  Ring state: bit-exact."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_25537_amd import cmc
+from paper_2609_25537_amd import workloads as wl
+from tests.gpu_util import DEV, max_abs, say, to_dev, to_host, tol_for
+from tests.inputs import accepted_attempts
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16(x):
+    return wl.f32_to_bf16_bits(x)
+
+
+# ------------------------------------------------------------------ select
+
+def _check_select(orc, keys, qv, k, what):
+    say(f"select {what}: B={keys.shape[0]} N={keys.shape[1]} D={keys.shape[2]} k={k}")
+    ref_idx, ref_s, _ = orc.select(keys, qv, k)
+    scores = torch.empty(keys.shape[:2], dtype=torch.float32, device=DEV)
+    idx = cmc.cmc_select_cmes(to_dev(keys), to_dev(qv), k, scores_out=scores)
+    torch.cuda.synchronize()
+    got = to_host(idx)
+    assert (got == ref_idx).all(), f"{what}: index sets differ"
+    assert max_abs(to_host(scores), ref_s) < 1e-6
+    # the workspace variant (scores not returned) gives the same indices
+    idx2 = cmc.cmc_select_cmes(to_dev(keys), to_dev(qv), k)
+    torch.cuda.synchronize()
+    assert (to_host(idx2) == got).all()
+
+
+def test_select_tiny(orc):
+    w = wl.get("tiny_fp32")
+    att = accepted_attempts(w, orc)
+    _check_select(orc, wl.sel_keys(w), wl.q_vecs(w, att), w.k, "tiny")
+
+
+def _separated(B, N, D, seed, dup_every=0):
+    """Keys whose cosine scores are distinct and well separated (in fp32),
+    with optional exact duplicates that tie exactly."""
+    rng = np.random.default_rng(seed)
+    keys = rng.standard_normal((B, N, D)).astype(np.float32) * np.float32(1e-3)
+    qv = np.zeros((B, D), np.float32)
+    qv[:, 0] = 1.0
+    for b in range(B):
+        a = (rng.permutation(N).astype(np.float64) / max(N, 1) * 10.0 - 5.0).astype(np.float32)
+        keys[b, :, 0] = a
+        keys[b, :, 1] = 1.0
+        keys[b, :, 2:] = 0.0
+        if dup_every:
+            for j in range(dup_every, N, dup_every):
+                keys[b, j] = keys[b, j - dup_every // 2]
+    return keys, qv
+
+
+@pytest.mark.parametrize("B,N,D,k", [
+    (1, 1, 4, 1), (1, 7, 8, 0), (1, 7, 8, 7), (3, 33, 12, 5), (2, 1000, 64, 999),
+    (4, 4096, 16, 512), (1, 32768, 8, 1024), (2, 32768, 8, 32768), (5, 2047, 260, 1),
+])
+def test_select_sizes(orc, B, N, D, k):
+    keys, qv = _separated(B, N, D, seed=N + k)
+    _check_select(orc, keys, qv, k, f"sizes")
+
+
+@pytest.mark.parametrize("N,k", [(64, 16), (1000, 100), (20000, 700)])
+def test_select_exact_ties(orc, N, k):
+    keys, qv = _separated(2, N, 8, seed=7, dup_every=4)
+    _check_select(orc, keys, qv, k, "ties")
+
+
+def test_select_zero_rows_and_question(orc):
+    keys, qv = _separated(2, 100, 8, seed=3)
+    keys[0, 10] = 0.0
+    keys[0, 50] = 0.0
+    qv[1] = 0.0               # every score 0: the first k rows win
+    _check_select(orc, keys, qv, 30, "zeros")
+
+
+def test_select_llama_layer_full_size(orc):
+    w = wl.get("llama3_8b_layer")
+    att = accepted_attempts(w, orc)
+    _check_select(orc, wl.sel_keys(w), wl.q_vecs(w, att), w.k, "llama3_8b_layer")
+
+
+# ------------------------------------------------------------------ append
+
+@pytest.mark.parametrize("dtype,Dh,W,T", [("f32", 64, 8, 1), ("bf16", 128, 5, 2), ("bf16", 256, 3, 3),
+                                          ("f32", 128, 1, 1)])
+def test_window_append_ring(orc, dtype, Dh, W, T):
+    rng = np.random.default_rng(W * 10 + T)
+    B, Hkv = 3, 2
+    mk = (lambda *s: _bf16(rng.standard_normal(s).astype(np.float32))) if dtype == "bf16" else \
+        (lambda *s: rng.standard_normal(s).astype(np.float32))
+    wk, wv = mk(B, Hkv, W, Dh), mk(B, Hkv, W, Dh)
+    cnt = np.array([0, min(2, W - 1), W + 3], np.int32)
+    dk, dv, dc = to_dev(wk), to_dev(wv), to_dev(cnt)
+    for step in range(2 * W + 1):
+        say(f"append {dtype} Dh={Dh} W={W} T={T} step {step}")
+        nk, nv = mk(B, Hkv, T, Dh), mk(B, Hkv, T, Dh)
+        orc.window_append(wk, wv, cnt, nk, nv)
+        cmc.cmc_window_append(dk, dv, dc, to_dev(nk), to_dev(nv))
+    torch.cuda.synchronize()
+    assert (to_host(dk) == wk).all() and (to_host(dv) == wv).all()
+    assert (to_host(dc) == cnt).all()
+
+
+# ------------------------------------------------------------------ decode
+
+def _logit_bound_tol(q, keys_f64, scale, vmax, Dh):
+    """Bound on the fp32 output error when the logits are large: each fp32
+    logit is off by at most gamma_Dh * scale * sum_d |q_d k_d| (gamma_n =
+    n u / (1 - n u), u = 2^-24), which moves the softmax weights by at most
+    that amount relatively, so |out error| <= 2 * max dz * max |v| (+ the
+    fp32 rounding of the weighted sum itself)."""
+    u = 2.0 ** -24
+    gamma = Dh * u / (1 - Dh * u)
+    dz = gamma * abs(scale) * float(np.max(np.abs(q.astype(np.float64)) @ np.abs(keys_f64).T))
+    return 2.0 * dz * vmax + 1e-5
+
+
+def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_none=False, scale=None,
+                 kv_std=1.0, derived_tol=False):
+    rng = np.random.default_rng(seed)
+    f = lambda *s: (rng.standard_normal(s) * kv_std).astype(np.float32)
+    cv = _bf16 if dtype == "bf16" else (lambda x: x)
+    pk, pv = cv(f(B, Hkv, N, Dh)), cv(f(B, Hkv, N, Dh))
+    if idx_none:
+        idx = None
+    else:
+        idx = np.stack([np.sort(rng.choice(N, size=k, replace=False)) for _ in range(B)]).astype(np.int32)
+    wk = np.zeros((B, Hkv, W, Dh), np.float32)
+    wv = np.zeros((B, Hkv, W, Dh), np.float32)
+    if fill:
+        wk[:, :, :fill] = f(B, Hkv, fill, Dh)
+        wv[:, :, :fill] = f(B, Hkv, fill, Dh)
+    wk, wv = cv(wk), cv(wv)
+    cnt = np.full((B,), fill, np.int32)
+    scale = 1.0 / math.sqrt(Dh) if scale is None else scale
+    d = dict(pk=to_dev(pk), pv=to_dev(pv), idx=None if idx is None else to_dev(idx),
+             wk=to_dev(wk) if W else None, wv=to_dev(wv) if W else None, wc=to_dev(cnt) if W else None)
+    worst = 0.0
+    for step in range(steps):
+        say(f"decode {dtype} B={B} Hq={Hq} Hkv={Hkv} Dh={Dh} N={N} k={k} W={W} fill={fill} step={step}")
+        if W:
+            nk, nv = cv(f(B, Hkv, 1, Dh)), cv(f(B, Hkv, 1, Dh))
+            orc.window_append(wk, wv, cnt, nk, nv)
+            cmc.cmc_window_append(d["wk"], d["wv"], d["wc"], to_dev(nk), to_dev(nv))
+        q = f(B, Hq, Dh)
+        ref = orc.two_tier_decode(q, pk, pv, idx, k, wk, wv, cnt, W, scale)
+        out = cmc.cmc_two_tier_decode(to_dev(q), d["pk"], d["pv"], d["idx"], k, d["wk"], d["wv"], d["wc"],
+                                      scale, W=W)
+        torch.cuda.synchronize()
+        err = max_abs(to_host(out), ref)
+        worst = max(worst, err)
+        tol = tol_for(dtype)
+        if derived_tol:
+            allk = np.concatenate([pk.reshape(-1, Dh), wk.reshape(-1, Dh)]).astype(np.float64)
+            vmax = float(max(np.abs(pv).max(), np.abs(wv).max()))
+            tol = max(tol, _logit_bound_tol(q.reshape(-1, Dh), allk, scale, vmax, Dh))
+        assert np.isfinite(to_host(out)).all()
+        assert err <= tol, f"step {step}: max abs err {err:.3e} > {tol:.3e}"
+    return worst
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Dh", [64, 128, 256])
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_decode_head_shapes(orc, dtype, Dh, G):
+    _decode_case(orc, B=2, Hq=2 * G, Hkv=2, Dh=Dh, N=97, k=37, W=19, fill=11, dtype=dtype, seed=Dh + G)
+
+
+@pytest.mark.parametrize("k,W,fill", [(1, 0, 0), (0, 5, 2), (0, 64, 64), (300, 0, 0), (5, 1, 0),
+                                      (2000, 3000, 2999), (513, 700, 0)])
+def test_decode_key_counts(orc, k, W, fill):
+    _decode_case(orc, B=2, Hq=8, Hkv=2, Dh=128, N=max(k, 1) + 50, k=k, W=W, fill=fill, dtype="bf16",
+                 seed=k * 7 + W)
+
+
+def test_decode_empty_window_zero_output(orc):
+    """k = 0 and an empty ring: zeros, like the oracle."""
+    _decode_case(orc, B=1, Hq=4, Hkv=4, Dh=64, N=10, k=0, W=4, fill=0, dtype="f32", seed=1, steps=1)
+
+
+def test_decode_identity_index(orc):
+    _decode_case(orc, B=3, Hq=8, Hkv=8, Dh=64, N=40, k=40, W=0, fill=0, dtype="f32", seed=5, idx_none=True)
+
+
+def test_decode_large_logits(orc):
+    """Logits around +-3e2: online max subtraction must keep it finite; the
+    tolerance is the fp32 logit-error bound, since 1e-5 absolute is below
+    what any fp32 evaluation of logits this large can guarantee."""
+    _decode_case(orc, B=2, Hq=4, Hkv=2, Dh=128, N=60, k=30, W=16, fill=16, dtype="f32", seed=9,
+                 scale=1.0, kv_std=3.0, derived_tol=True)
+
+
+def test_decode_bit_identical_runs():
+    rng = np.random.default_rng(0)
+    B, Hq, Hkv, Dh, N, k, W = 4, 32, 8, 128, 512, 128, 256
+    q = to_dev(rng.standard_normal((B, Hq, Dh)).astype(np.float32))
+    pk = to_dev(_bf16(rng.standard_normal((B, Hkv, N, Dh)).astype(np.float32)))
+    pv = to_dev(_bf16(rng.standard_normal((B, Hkv, N, Dh)).astype(np.float32)))
+    wk = to_dev(_bf16(rng.standard_normal((B, Hkv, W, Dh)).astype(np.float32)))
+    wv = to_dev(_bf16(rng.standard_normal((B, Hkv, W, Dh)).astype(np.float32)))
+    wc = to_dev(np.array([W, 7, 0, 1000], np.int32))
+    idx = to_dev(np.sort(rng.choice(N, size=(B, k)), axis=1).astype(np.int32))
+    say("decode bit-identical runs")
+    a = cmc.cmc_two_tier_decode(q, pk, pv, idx, k, wk, wv, wc, 0.088)
+    b = cmc.cmc_two_tier_decode(q, pk, pv, idx, k, wk, wv, wc, 0.088)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_tiny_workload_end_to_end(orc):
+    """The tiny fp32 workload: select, then 16 steps of append + decode."""
+    w = wl.get("tiny_fp32")
+    att = accepted_attempts(w, orc)
+    keys, qv = wl.sel_keys(w), wl.q_vecs(w, att)
+    ref_idx, _, _ = orc.select(keys, qv, w.k)
+    say("tiny e2e: select")
+    idx = cmc.cmc_select_cmes(to_dev(keys), to_dev(qv), w.k)
+    pk, pv = wl.pool_kv(w)
+    wk, wv, cnt = wl.window_kv(w)
+    d_pk, d_pv, d_wk, d_wv, d_wc = map(to_dev, (pk, pv, wk, wv, cnt))
+    torch.cuda.synchronize()
+    assert (to_host(idx) == ref_idx).all()
+    for t in range(w.steps):
+        say(f"tiny e2e: step {t}")
+        nk, nv = wl.step_new_kv(w, t)
+        q = wl.step_q(w, t)
+        orc.window_append(wk, wv, cnt, nk, nv)
+        ref = orc.two_tier_decode(q, pk, pv, ref_idx, w.k, wk, wv, cnt, w.W, w.scale)
+        cmc.cmc_window_append(d_wk, d_wv, d_wc, to_dev(nk), to_dev(nv))
+        out = cmc.cmc_two_tier_decode(to_dev(q), d_pk, d_pv, idx, w.k, d_wk, d_wv, d_wc, w.scale)
+        torch.cuda.synchronize()
+        assert max_abs(to_host(out), ref) <= 1e-5, t
+    assert (to_host(d_wk) == wk).all() and (to_host(d_wc) == cnt).all()
