@@ -60,7 +60,8 @@ def parse():
                     help="distinct per-step input sets (rotated); default all steps up to 4096 rows of q")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
-    ap.add_argument("--graph", action="store_true", help="replay each pass as a captured HIP graph")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every kernel from Python instead of replaying a captured HIP graph")
     ap.add_argument("--out", default=None, help="also append the JSON line to this file")
     return ap.parse_args()
 
@@ -96,8 +97,7 @@ class Inputs:
         self.out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=dev)
         from paper_2609_25537_amd import cmc
         self.sel_ws = torch.empty(max(1, cmc.cmc_select_workspace_bytes(w.B, w.N)), dtype=torch.uint8, device=dev)
-        self.dec_ws = torch.empty(max(1, cmc.cmc_decode_workspace_bytes(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W)),
-                                  dtype=torch.uint8, device=dev)
+        self.dec_ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, dev)
 
 
 def run_pass(inp: Inputs, steps: int):
@@ -107,34 +107,55 @@ def run_pass(inp: Inputs, steps: int):
     cmc.cmc_select_cmes(inp.keys, inp.qv, w.k, idx_out=inp.idx, workspace=inp.sel_ws)
     for t in range(steps):
         j = t % inp.P
-        cmc.cmc_window_append(inp.wk, inp.wv, inp.wc, inp.nk[j], inp.nv[j])
-        cmc.cmc_two_tier_decode(inp.q[j], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, w.scale,
-                                out=inp.out, workspace=inp.dec_ws)
+        cmc.cmc_decode_step(inp.q[j], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, inp.nk[j], inp.nv[j],
+                            w.scale, out=inp.out, workspace=inp.dec_ws)
 
 
 def decode_bytes(w) -> int:
-    """Algorithmic bytes of one decode launch: K and V of the k + W keys
-    (ring full), q, out and the index list."""
+    """Algorithmic bytes of one decode-step launch: K and V of the k + W
+    keys (ring full, the newest row read from the appended input), the
+    appended row written into the ring, q, out and the index list."""
     kv = w.B * w.Hkv * (w.k + w.W) * w.Dh * w.kv_bytes * 2
-    return kv + w.B * w.Hq * w.Dh * 4 * 2 + w.B * w.k * 4
+    ring_write = w.B * w.Hkv * w.Dh * w.kv_bytes * 2
+    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2 + w.B * w.k * 4
 
 
-def time_decode_launch(inp: Inputs, reps: int = 200):
-    """Average duration of one decode launch, HIP events on its stream."""
+def capture(fn):
+    """Capture fn's launches into a HIP graph (after one warm-up run)."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_decode_launch(inp: Inputs, reps: int = 500):
+    """Average duration of one decode launch: `reps` back-to-back launches
+    replayed from a graph, bracketed by HIP events on the replay stream."""
     import torch
     from paper_2609_25537_amd import cmc
     w = inp.w
+
+    def launches():
+        for r in range(reps):
+            j = r % inp.P
+            cmc.cmc_decode_step(inp.q[j], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, inp.nk[j],
+                                inp.nv[j], w.scale, out=inp.out, workspace=inp.dec_ws)
+
+    g = capture(launches)
     s = torch.cuda.current_stream()
-    for _ in range(10):
-        cmc.cmc_two_tier_decode(inp.q[0], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, w.scale,
-                                out=inp.out, workspace=inp.dec_ws)
+    g.replay()
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
     s.synchronize()
     a.record(s)
-    for _ in range(reps):
-        cmc.cmc_two_tier_decode(inp.q[0], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, w.scale,
-                                out=inp.out, workspace=inp.dec_ws)
+    g.replay()
     b.record(s)
     b.synchronize()
     return a.elapsed_time(b) / reps * 1e-3  # seconds
@@ -189,17 +210,7 @@ def main():
     inp = Inputs(w, steps, pool, dev)
     torch.cuda.synchronize()
 
-    graph = None
-    if args.graph:
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            run_pass(inp, steps)          # warm-up outside capture
-        torch.cuda.current_stream().wait_stream(s)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            run_pass(inp, steps)
-        torch.cuda.synchronize()
+    graph = None if args.eager else capture(lambda: run_pass(inp, steps))
 
     def one():
         if graph is not None:
@@ -236,7 +247,7 @@ def main():
             traffic = entry.get("bytes_per_launch")
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "cmc_two_tier_decode", "bytes_per_launch": nbytes,
+                "kernel": "decode_kernel (cmc_decode_step)", "bytes_per_launch": nbytes,
                 "launch_us": round(t_launch * 1e6, 3)}
 
     cpu = None

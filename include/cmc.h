@@ -14,6 +14,7 @@
  *   cmc_select_cmes      Tier-1 scoring and top-K selection (once per question)
  *   cmc_window_append    Tier-2 ring-buffer append (every step)
  *   cmc_two_tier_decode  decode attention over [selected rows || window]
+ *   cmc_decode_step      append + decode fused into one launch (every step)
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -121,8 +122,15 @@ long long cmc_window_start(long long ctx_len, long long W, long long alpha);
 /* Two-tier decode attention.                                               */
 /* ------------------------------------------------------------------------ */
 
-/* Bytes of workspace cmc_two_tier_decode needs for these sizes; 0 for
- * invalid sizes. */
+/* Bytes of workspace cmc_two_tier_decode and cmc_decode_step need for these
+ * sizes; 0 for invalid sizes.
+ *
+ * The decode workspace holds arrival counters (its first 4*(B + B*Hkv)
+ * bytes) followed by split-K partials.  It must be ZERO-FILLED before its
+ * first use (e.g. allocated zeroed); every call returns the counters to zero,
+ * so it can be reused by later calls (also from a captured HIP graph)
+ * without clearing.  Do not share one workspace between calls that may run
+ * concurrently. */
 size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W);
 
 /*
@@ -143,11 +151,13 @@ size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W);
  *                                 [pool rows idx] ++ [valid ring slots]; query
  *                                 head h reads kv head h / (Hq/Hkv).  A sequence
  *                                 whose key list is empty gets a zero row.
- *   workspace  >= cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W) bytes
+ *   workspace  >= cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W) bytes,
+ *              zero-filled before first use (see cmc_decode_workspace_bytes)
  *
  * Limits: Hq % Hkv == 0 with Hq/Hkv in {1, 2, 4, 8}; Dh in {64, 128, 256};
  * 0 <= k <= N when idx == NULL; k + W >= 1; W >= 0.  Index values are not
- * checked on the device: out-of-range values are undefined behaviour.
+ * checked on the host; the device clamps them into [0, N-1], which keeps
+ * memory access in bounds but makes the result meaningless.
  * Arithmetic: fp32 accumulation, fixed reduction order (run-to-run
  * bit-identical).
  */
@@ -159,6 +169,23 @@ cmc_status cmc_two_tier_decode(const float *q,
                                cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
                                float scale, float *out,
                                void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * One whole decode step in a single launch: the ring append of
+ * cmc_window_append (new_k/new_v [B][Hkv][T_new][Dh], 1 <= T_new <= W)
+ * followed by cmc_two_tier_decode over the updated cache.  Results (out, the
+ * ring contents and win_count) are identical to calling the two in that
+ * order.  With W == 0 there is no Tier-2 and new_k/new_v are ignored.
+ * Same arguments, limits and workspace as cmc_two_tier_decode otherwise.
+ */
+cmc_status cmc_decode_step(const float *q,
+                           const void *cme_k, const void *cme_v,
+                           const int32_t *idx, int k,
+                           void *win_k, void *win_v, int32_t *win_count, int W,
+                           const void *new_k, const void *new_v, int T_new,
+                           cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                           float scale, float *out,
+                           void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                             */

@@ -28,8 +28,8 @@ CMC_BF16 = 1
 
 EXPORTED = [
     "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_window_append", "cmc_window_start",
-    "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_status_string", "cmc_last_error",
-    "cmc_version",
+    "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step", "cmc_status_string",
+    "cmc_last_error", "cmc_version",
 ]
 
 
@@ -64,6 +64,9 @@ def lib() -> ctypes.CDLL:
         L.cmc_two_tier_decode.argtypes = [P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
                                           ctypes.c_float, P, P, SZ, P]
         L.cmc_two_tier_decode.restype = I
+        L.cmc_decode_step.argtypes = [P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
+                                      ctypes.c_float, P, P, SZ, P]
+        L.cmc_decode_step.restype = I
         L.cmc_status_string.argtypes = [I]
         L.cmc_status_string.restype = ctypes.c_char_p
         L.cmc_last_error.argtypes = []
@@ -184,6 +187,13 @@ def cmc_decode_workspace_bytes(B: int, Hq: int, Hkv: int, Dh: int, k: int, W: in
     return int(lib().cmc_decode_workspace_bytes(int(B), int(Hq), int(Hkv), int(Dh), int(k), int(W)))
 
 
+def decode_workspace(B: int, Hq: int, Hkv: int, Dh: int, k: int, W: int, device):
+    """A zero-filled decode workspace (the library keeps it zeroed)."""
+    import torch
+    return torch.zeros(max(1, cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W)), dtype=torch.uint8,
+                       device=device)
+
+
 def cmc_two_tier_decode(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, scale: float,
                         out=None, workspace=None, W: Optional[int] = None, stream=None):
     """One decode step over [pool rows idx || ring slots].  q [B][Hq][Dh] fp32,
@@ -210,13 +220,54 @@ def cmc_two_tier_decode(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, s
         out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
     _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
     if workspace is None:
-        workspace = torch.empty(max(1, cmc_decode_workspace_bytes(B, Hq, Hkv, Dh, k, W)),
-                                dtype=torch.uint8, device=q.device)
+        workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
     ws_bytes = workspace.numel() * workspace.element_size()
     rc = lib().cmc_two_tier_decode(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k),
                                    _ptr(win_k) if W > 0 else None, _ptr(win_v) if W > 0 else None,
                                    _ptr(win_count) if W > 0 else None, int(W), _kv_dtype(cme_k),
                                    B, Hq, Hkv, Dh, N, float(scale), _ptr(out), _ptr(workspace),
                                    ws_bytes, _stream(stream))
+    _check(rc)
+    return out
+
+
+def cmc_decode_step(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, new_k, new_v, scale: float,
+                    out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """Ring append of new_k/new_v [B][Hkv][T][Dh] followed by the two-tier
+    decode, in one launch.  Same arguments as cmc_two_tier_decode plus the
+    new rows.  Returns out [B][Hq][Dh] fp32."""
+    import torch
+    _need(q.dim() == 3 and q.is_contiguous() and q.dtype == torch.float32, "q must be contiguous fp32 [B][Hq][Dh]")
+    B, Hq, Dh = q.shape
+    _need(cme_k.dim() == 4 and cme_k.is_contiguous() and cme_v.is_contiguous(), "cme_k/v [B][Hkv][N][Dh]")
+    _need(cme_k.shape[0] == B and cme_k.shape[3] == Dh and cme_v.shape == cme_k.shape, "pool shape")
+    Hkv, N = cme_k.shape[1], cme_k.shape[2]
+    if W is None:
+        W = 0 if win_k is None else win_k.shape[2]
+    T = 0
+    if W > 0:
+        _need(win_k.shape == (B, Hkv, W, Dh) and win_v.shape == win_k.shape, "window shape")
+        _need(win_k.dtype == cme_k.dtype == win_v.dtype, "window dtype must match pool")
+        _need(win_k.is_contiguous() and win_v.is_contiguous(), "window must be contiguous")
+        _need(win_count is not None and win_count.shape == (B,) and win_count.dtype == torch.int32,
+              "win_count [B] int32")
+        _need(new_k.dim() == 4 and new_k.shape[:2] == (B, Hkv) and new_k.shape[3] == Dh, "new_k [B][Hkv][T][Dh]")
+        _need(new_v.shape == new_k.shape and new_k.dtype == new_v.dtype == cme_k.dtype, "new_k/v must match")
+        _need(new_k.is_contiguous() and new_v.is_contiguous(), "new_k/v must be contiguous")
+        T = int(new_k.shape[2])
+    if idx is not None:
+        _need(idx.shape == (B, k) and idx.dtype == torch.int32 and idx.is_contiguous(), "idx [B][k] int32")
+    if out is None:
+        out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
+    _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
+    if workspace is None:
+        workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_decode_step(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k),
+                               _ptr(win_k) if W > 0 else None, _ptr(win_v) if W > 0 else None,
+                               _ptr(win_count) if W > 0 else None, int(W),
+                               _ptr(new_k) if W > 0 else None, _ptr(new_v) if W > 0 else None, T,
+                               _kv_dtype(cme_k), B, Hq, Hkv, Dh, N, float(scale), _ptr(out), _ptr(workspace),
+                               ws_bytes, _stream(stream))
     _check(rc)
     return out

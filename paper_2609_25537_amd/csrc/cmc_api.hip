@@ -43,25 +43,29 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 namespace cmc {
 
 // Key-axis split plan.  Aim for about kTargetWG workgroups in flight (a few
-// per CU on 256 CUs) without cutting a split below kGranule keys; the plan
-// depends only on sizes, so the workspace query and the launch always agree.
+// per CU on 256 CUs) without cutting a split below kGranule keys (4 waves x
+// 16-key blocks); the plan depends only on sizes, so the workspace query and
+// the launch always agree.
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
     constexpr long long kTargetWG = 1024;
-    constexpr long long kGranule = 32;
+    constexpr long long kGranule = 64;
+    constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
     DecodePlan pl;
     const long long L = (long long)k + W;
     const long long pairs = (long long)B * Hkv;
     if (L <= 0 || pairs <= 0) return pl;
     const long long s_target = std::max(1LL, (kTargetWG + pairs - 1) / pairs);
     long long chunk = (L + s_target - 1) / s_target;
+    chunk = std::max(chunk, (L + kMaxSplits - 1) / kMaxSplits);
     chunk = ((chunk + kGranule - 1) / kGranule) * kGranule;
     const long long S = (L + chunk - 1) / chunk;
     const int G = Hq / Hkv;
     pl.S = (int)S;
     pl.chunk = (int)chunk;
-    pl.ml_bytes = align256((size_t)(pairs * S * G * 2) * sizeof(float));
-    pl.acc_bytes = align256((size_t)(pairs * S * G * Dh) * sizeof(float));
-    pl.total = pl.ml_bytes + pl.acc_bytes;
+    pl.counter_bytes = align256((size_t)(B + pairs) * sizeof(unsigned));
+    pl.ml_bytes = S > 1 ? align256((size_t)(pairs * S * G * 2) * sizeof(float)) : 0;
+    pl.acc_bytes = S > 1 ? align256((size_t)(pairs * S * G * Dh) * sizeof(float)) : 0;
+    pl.total = pl.counter_bytes + pl.ml_bytes + pl.acc_bytes;
     return pl;
 }
 
@@ -159,37 +163,46 @@ size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W) 
     return cmc::plan_decode(B, Hq, Hkv, Dh, k, W).total;
 }
 
-cmc_status cmc_two_tier_decode(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
-                               int k, const void *win_k, const void *win_v, const int32_t *win_count,
-                               int W, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
-                               float scale, float *out, void *workspace, size_t workspace_bytes,
-                               void *stream) {
+}  // extern "C"
+
+namespace {
+
+cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                       int k, void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
+                       const void *new_v, int T_new, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                       float scale, float *out, void *workspace, size_t workspace_bytes, void *stream) {
     if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
-        return fail(CMC_ERR_UNSUPPORTED, "decode: unknown kv_dtype %d", (int)kv_dtype);
+        return fail(CMC_ERR_UNSUPPORTED, "%s: unknown kv_dtype %d", fn, (int)kv_dtype);
     if (B < 0 || Hq < 1 || Hkv < 1 || k < 0 || W < 0 || N < 0)
-        return fail(CMC_ERR_INVALID_ARGUMENT, "decode: need B >= 0, Hq, Hkv >= 1, k, W, N >= 0");
-    if (Hq % Hkv != 0) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
+        return fail(CMC_ERR_INVALID_ARGUMENT, "%s: need B >= 0, Hq, Hkv >= 1, k, W, N >= 0", fn);
+    if (Hq % Hkv != 0) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: Hq=%d not a multiple of Hkv=%d", fn, Hq, Hkv);
     const int G = Hq / Hkv;
     if (G != 1 && G != 2 && G != 4 && G != 8)
-        return fail(CMC_ERR_UNSUPPORTED, "decode: Hq/Hkv=%d not in {1,2,4,8}", G);
-    if (!supported_dh(Dh)) return fail(CMC_ERR_UNSUPPORTED, "decode: Dh=%d not in {64,128,256}", Dh);
-    if ((long long)k + W < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: empty cache (k + W = 0)");
-    if (!idx && k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: k=%d exceeds N=%d with idx == NULL", k, N);
-    if (k > 0 && N < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: k=%d rows requested from an empty pool", k);
-    if (!(scale == scale) || isinf(scale)) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: scale must be finite");
-    if (B > 65535 || Hkv > 65535) return fail(CMC_ERR_UNSUPPORTED, "decode: B and Hkv must be <= 65535");
+        return fail(CMC_ERR_UNSUPPORTED, "%s: Hq/Hkv=%d not in {1,2,4,8}", fn, G);
+    if (!supported_dh(Dh)) return fail(CMC_ERR_UNSUPPORTED, "%s: Dh=%d not in {64,128,256}", fn, Dh);
+    if ((long long)k + W < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: empty cache (k + W = 0)", fn);
+    if (!idx && k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: k=%d exceeds N=%d with idx == NULL", fn, k, N);
+    if (k > 0 && N < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: k=%d rows requested from an empty pool", fn, k);
+    if (!(scale == scale) || isinf(scale)) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: scale must be finite", fn);
+    if (T_new < 0 || (W > 0 && T_new > W))
+        return fail(CMC_ERR_INVALID_ARGUMENT, "%s: need 0 <= T_new <= W (got T_new=%d W=%d)", fn, T_new, W);
+    if (B > 65535 || Hkv > 65535) return fail(CMC_ERR_UNSUPPORTED, "%s: B and Hkv must be <= 65535", fn);
+    if (W == 0) T_new = 0;  // no Tier-2: appending is a no-op
     if (B == 0) return ok();
-    if (!q || !out) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: q and out must be non-null");
-    if (k > 0 && (!cme_k || !cme_v)) return fail(CMC_ERR_INVALID_ARGUMENT, "decode: null Tier-1 pool");
+    if (!q || !out) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: q and out must be non-null", fn);
+    if (k > 0 && (!cme_k || !cme_v)) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: null Tier-1 pool", fn);
     if (W > 0 && (!win_k || !win_v || !win_count))
-        return fail(CMC_ERR_INVALID_ARGUMENT, "decode: null Tier-2 window");
+        return fail(CMC_ERR_INVALID_ARGUMENT, "%s: null Tier-2 window", fn);
+    if (T_new > 0 && (!new_k || !new_v)) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: null new rows", fn);
     if (misaligned(q) || misaligned(cme_k) || misaligned(cme_v) || misaligned(idx) || misaligned(win_k) ||
-        misaligned(win_v) || misaligned(win_count) || misaligned(out) || misaligned(workspace))
-        return fail(CMC_ERR_UNSUPPORTED, "decode: every pointer must be 16-byte aligned");
+        misaligned(win_v) || misaligned(win_count) || misaligned(out) || misaligned(workspace) ||
+        misaligned(new_k) || misaligned(new_v))
+        return fail(CMC_ERR_UNSUPPORTED, "%s: every pointer must be 16-byte aligned", fn);
     const cmc::DecodePlan pl = cmc::plan_decode(B, Hq, Hkv, Dh, k, W);
     if (!workspace || workspace_bytes < pl.total)
-        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "decode: workspace of %zu bytes needed, %zu given", pl.total,
+        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "%s: workspace of %zu bytes needed, %zu given", fn, pl.total,
                     workspace ? workspace_bytes : (size_t)0);
+    char *ws = static_cast<char *>(workspace);
     cmc::DecodeParams p{};
     p.q = q;
     p.cme_k = cme_k;
@@ -198,21 +211,52 @@ cmc_status cmc_two_tier_decode(const float *q, const void *cme_k, const void *cm
     p.win_k = W > 0 ? win_k : nullptr;
     p.win_v = W > 0 ? win_v : nullptr;
     p.win_count = W > 0 ? win_count : nullptr;
+    p.new_k = T_new > 0 ? new_k : nullptr;
+    p.new_v = T_new > 0 ? new_v : nullptr;
     p.out = out;
-    p.part_ml = static_cast<float *>(workspace);
-    p.part_acc = reinterpret_cast<float *>(static_cast<char *>(workspace) + pl.ml_bytes);
+    p.seq_counter = reinterpret_cast<unsigned *>(ws);
+    p.pair_counter = reinterpret_cast<unsigned *>(ws) + B;
+    p.part_ml = reinterpret_cast<float *>(ws + pl.counter_bytes);
+    p.part_acc = reinterpret_cast<float *>(ws + pl.counter_bytes + pl.ml_bytes);
     p.k = k;
     p.W = W;
     p.B = B;
     p.Hq = Hq;
     p.Hkv = Hkv;
     p.N = N;
+    p.T_new = T_new;
     p.S = pl.S;
     p.chunk = pl.chunk;
     p.qscale = cmc::decode_qscale(scale);
     hipError_t e = cmc::launch_two_tier_decode(p, kv_dtype == CMC_BF16, G, Dh, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+cmc_status cmc_two_tier_decode(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                               int k, const void *win_k, const void *win_v, const int32_t *win_count,
+                               int W, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                               float scale, float *out, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+    // Nothing is appended (T_new = 0), so the window is only read.
+    return decode_impl("decode", q, cme_k, cme_v, idx, k, const_cast<void *>(win_k), const_cast<void *>(win_v),
+                       const_cast<int32_t *>(win_count), W, nullptr, nullptr, 0, kv_dtype, B, Hq, Hkv, Dh, N,
+                       scale, out, workspace, workspace_bytes, stream);
+}
+
+cmc_status cmc_decode_step(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx, int k,
+                           void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
+                           const void *new_v, int T_new, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh,
+                           int N, float scale, float *out, void *workspace, size_t workspace_bytes,
+                           void *stream) {
+    if (W > 0 && T_new < 1)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step: need 1 <= T_new <= W (got T_new=%d W=%d)", T_new, W);
+    return decode_impl("decode_step", q, cme_k, cme_v, idx, k, win_k, win_v, win_count, W, new_k, new_v, T_new,
+                       kv_dtype, B, Hq, Hkv, Dh, N, scale, out, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

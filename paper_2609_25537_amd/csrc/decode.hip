@@ -1,22 +1,45 @@
 // Two-tier decode attention (Sec. 2.5, KV cache assembly): one decode step of
 // softmax attention over the key list [Tier-1 pool rows idx[0..k-1]] ++
-// [Tier-2 ring slots 0..min(count,W)-1], split over the key axis.
+// [Tier-2 ring slots 0..min(count,W)-1], optionally fused with the ring append
+// of this step's new rows, in ONE launch.
 //
-// Pass 1 (decode_split_kernel): grid (S, Hkv, B), 256 threads.  Workgroup s
-// owns keys [s*chunk, (s+1)*chunk) of the virtual list of sequence b and all
-// G = Hq/Hkv query heads that share kv head h, so every K/V byte is read
-// from HBM once per step and reused G times from registers.  Each 16-byte
-// lane load covers Vec16<T>::N elements of one row; LPR lanes cover a row
-// (a 256-byte bf16 row of Dh = 128 is 16 lanes, four rows per wave load).
-// Scores use the lane's slice of q (pre-scaled by scale*log2 e) and a DPP
-// butterfly over the row's lanes; softmax is online per wave (a running
-// max per head, rescaled once per block of U row-loads); the four waves are
-// combined through LDS and the workgroup writes one (m, l, acc[Dh]) partial
-// per head.
+// Grid (S, Hkv, B), 256 threads (4 waves).  Workgroup s owns keys
+// [s*chunk, (s+1)*chunk) of sequence b's virtual key list and all G = Hq/Hkv
+// query heads sharing kv head h, so each K/V byte is read from HBM once per
+// step and reused G times on chip.
 //
-// Pass 2 (decode_merge_kernel): grid (Hkv, B); combines the S partials of
-// each head in fixed split order: M = max m_s, out = sum 2^(m_s-M) acc_s /
-// sum 2^(m_s-M) l_s.  A head whose key list is empty gets zeros.
+// Fused append: with T_new > 0, the rows appended this step go to slots
+// (count + t) mod W.  The workgroup owning such a slot reads the row from
+// new_k/new_v instead of the ring and writes it into the ring; count is
+// advanced by the last workgroup of the sequence to arrive, after every
+// workgroup has read it.  The result equals cmc_window_append followed by
+// the decode.
+//
+// Main loop, two variants:
+//   MFMA (bf16 K/V, G <= 4): a wave takes 16 keys per block.  S = Q K^T is one
+//     v_mfma_f32_16x16x32_bf16 chain per Dh/32 slice, with the 16 A-rows
+//     holding the G query heads repeated (row m = head m % G), so every lane
+//     ends with all G scores of key (lane % 16).  q is split into bf16
+//     hi + lo parts (two MFMAs per slice), which keeps the logit error at the
+//     level of fp32 accumulation.  P V runs on the VALU in fp32: the block is
+//     split into two halves of 8 keys, lane l owning key (l & 7) and Dh/8
+//     dims; its p values come from its own lane or lane l ^ 8 (one DPP row
+//     rotate).
+//   VALU (fp32 K/V, or G = 8): 16-byte lane loads, LPR lanes per row, dot
+//     products reduced by a DPP butterfly.
+// Both keep an online softmax per wave (running max in log2 units, q
+// pre-scaled by scale*log2 e), then combine the four waves through LDS.
+//
+// Split merge, inside the same launch: with S == 1 the workgroup writes the
+// output directly.  With S > 1 every workgroup publishes (m, l, acc[Dh]) per
+// head to the workspace and arrives on a per-(b, kv head) counter; the last
+// to arrive merges the S partials in fixed split order (so results are
+// bit-identical run to run), writes the output and re-arms the counter.
+// Publication uses agent-coherent relaxed atomics plus a store-completion
+// wait instead of device-scope fences (see coherent_store).  A head whose key
+// list is empty gets zeros.
+#include <limits.h>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -25,29 +48,285 @@ namespace cmc {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kMergeBatch = 8;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// K/V row pointers of one key; rk/rv are set (to the ring slot the row must
+// be written to) only for a row appended in this call.
+template <typename T>
+struct RowPtrs {
+    const T *k, *v;
+    T *rk, *rv;
+};
+
+// Where the rows of sequence b's virtual key list live, for one kv head:
+// rows [0, k) are pool rows idx[row] (clamped into the pool), rows k.. are
+// ring slots row - k, except that the T_new slots written in this call
+// ((count + t) mod W) are read from the new rows.
+template <typename T>
+struct RowMap {
+    int stride;               // elements per row (Dh)
+    const T *poolK, *poolV;   // pool of this (b, kv head)
+    T *winK, *winV;           // ring of this (b, kv head)
+    const T *newK, *newV;     // appended rows of this (b, kv head)
+    const int32_t *idx;       // this sequence's index list, or nullptr
+    int k, W, nmax, slot0, T_new;
+};
+
+// Row lookup on values already in registers (free functions over scalars:
+// selecting between fields of a struct in memory would keep it on the
+// stack).  fetch_row() issues the only memory access of a lookup -- the
+// index-list entry of a pool row -- so callers can prefetch it one block
+// ahead; row_ptrs() is pure arithmetic on its result.
+__device__ __forceinline__ int fetch_row(int row, const int32_t *idx, int k) {
+    return (row < k && idx) ? idx[row] : row;
+}
+
+template <typename T>
+__device__ __forceinline__ RowPtrs<T> row_ptrs(int row, int r, const T *poolK, const T *poolV, T *winK,
+                                               T *winV, const T *newK, const T *newV, int k, int W, int nmax,
+                                               int slot0, int T_new, int stride) {
+    const bool in_pool = row < k;
+    r = r < 0 ? 0 : (r > nmax ? nmax : r);
+    const int slot = row - k;
+    int t = slot - slot0;
+    t += t < 0 ? W : 0;
+    const bool is_new = !in_pool && t < T_new;
+    const size_t op = (size_t)r * stride, ow = (size_t)slot * stride, on = (size_t)t * stride;
+    RowPtrs<T> o;
+    o.k = in_pool ? poolK + op : (is_new ? newK + on : winK + ow);
+    o.v = in_pool ? poolV + op : (is_new ? newV + on : winV + ow);
+    o.rk = is_new ? winK + ow : nullptr;
+    o.rv = is_new ? winV + ow : nullptr;
+    return o;
+}
+
+// Unpacks a RowMap into locals and defines LOCATE(row) over them.
+#define CMC_UNPACK_ROWMAP(rm)                                                            \
+    const auto poolK_ = (rm).poolK;                                                      \
+    const auto poolV_ = (rm).poolV;                                                      \
+    const auto winK_ = (rm).winK;                                                        \
+    const auto winV_ = (rm).winV;                                                        \
+    const auto newK_ = (rm).newK;                                                        \
+    const auto newV_ = (rm).newV;                                                        \
+    const int32_t *idx_ = (rm).idx;                                                      \
+    const int k_ = (rm).k, W_ = (rm).W, nmax_ = (rm).nmax, slot0_ = (rm).slot0,          \
+              tnew_ = (rm).T_new, stride_ = (rm).stride
+#define FETCH(row) fetch_row(row, idx_, k_)
+#define PTRS(row, r) \
+    row_ptrs(row, r, poolK_, poolV_, winK_, winV_, newK_, newV_, k_, W_, nmax_, slot0_, tnew_, stride_)
+#define LOCATE(row) PTRS(row, FETCH(row))
+
+template <typename T>
+__device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, int kvh, int DH, int slot0) {
+    RowMap<T> m;
+    const size_t head = (size_t)b * p.Hkv + kvh;
+    m.poolK = static_cast<const T *>(p.cme_k) + head * (size_t)p.N * DH;
+    m.poolV = static_cast<const T *>(p.cme_v) + head * (size_t)p.N * DH;
+    m.winK = p.W > 0 ? static_cast<T *>(p.win_k) + head * (size_t)p.W * DH : nullptr;
+    m.winV = p.W > 0 ? static_cast<T *>(p.win_v) + head * (size_t)p.W * DH : nullptr;
+    m.newK = p.T_new > 0 ? static_cast<const T *>(p.new_k) + head * (size_t)p.T_new * DH : nullptr;
+    m.newV = p.T_new > 0 ? static_cast<const T *>(p.new_v) + head * (size_t)p.T_new * DH : nullptr;
+    m.idx = p.idx ? p.idx + (size_t)b * p.k : nullptr;
+    m.k = p.k;
+    m.W = p.W;
+    m.nmax = p.N > 0 ? p.N - 1 : 0;
+    m.slot0 = slot0;
+    m.T_new = p.T_new;
+    m.stride = DH;
+    return m;
+}
+
+// 2^x with the hardware instruction alone (no denormal-result fix-up; a
+// softmax weight below 2^-126 contributes nothing at fp32 precision anyway).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ uint4 ld16(const void *p) { return *reinterpret_cast<const uint4 *>(p); }
+__device__ __forceinline__ void st16(void *p, const uint4 &v) { *reinterpret_cast<uint4 *>(p) = v; }
+
+// Per-wave online-softmax state for G heads and VEC output dims per lane.
+template <int G, int VEC>
+struct WaveState {
+    float m[G], l[G], acc[G][VEC];
+    __device__ __forceinline__ void init() {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            m[g] = -INFINITY;
+            l[g] = 0.f;
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[g][i] = 0.f;
+        }
+    }
+};
+
+// --------------------------------------------------------------- MFMA loop
+
+template <int DH, int G>
+__device__ __forceinline__ void mfma_loop(const DecodeParams &p, const RowMap<uint16_t> &rm, int b, int kvh,
+                                          int c0, int c1, WaveState<G, DH / 8> &st) {
+    constexpr int SL = DH / 32;      // MFMA k-slices
+    constexpr int VD = DH / 8;       // P V output dims per lane
+    constexpr int VQ = DH / 64;      // 16-byte V loads per lane per half block
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, q4 = lane >> 4, r8 = lane & 7, c8 = lane >> 3;
+    CMC_UNPACK_ROWMAP(rm);
+
+    // A operand: the lane's slice of query head (r16 % G), pre-scaled, as bf16 hi + lo.
+    bf16x8 qa_hi[SL], qa_lo[SL];
+    {
+        const float *qp = p.q + ((size_t)b * p.Hq + (size_t)kvh * G + (r16 % G)) * DH + 8 * q4;
+#pragma unroll
+        for (int i = 0; i < SL; ++i) {
+            const float4 x0 = *reinterpret_cast<const float4 *>(qp + 32 * i);
+            const float4 x1 = *reinterpret_cast<const float4 *>(qp + 32 * i + 4);
+            const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = xs[e] * p.qscale;
+                const __bf16 h = (__bf16)v;
+                qa_hi[i][e] = h;
+                qa_lo[i][e] = (__bf16)(v - (float)h);
+            }
+        }
+    }
+
+    constexpr int BSTRIDE = kWaves * 16;
+    // Rows of a block: the lane's K row blk + r16 (MFMA B layout, dims
+    // 32i + 8*q4 .. +7) and its V rows blk + 8h + r8 for the two halves
+    // (dims VD*c8 .. +VD-1).  Index-list entries are fetched one block ahead
+    // of the K/V rows, and the K/V rows one block ahead of their use.
+#define CMC_FETCH_BLOCK(b0, ik, iv0, iv1) \
+    do {                                  \
+        ik = FETCH((b0) + r16);           \
+        iv0 = FETCH((b0) + r8);           \
+        iv1 = FETCH((b0) + 8 + r8);       \
+    } while (0)
+#define CMC_LOAD_BLOCK(B0_, IK_, IV0_, IV1_, KK_, VV_, RK_, RV0_, RV1_)                                         \
+    do {                                                                                             \
+        RK_ = nullptr;                                                                                \
+        RV0_ = RV1_ = nullptr;                                                                         \
+        if ((B0_) + r16 < c1) {                                                                       \
+            const RowPtrs<uint16_t> rp = PTRS((B0_) + r16, IK_);                                       \
+            RK_ = rp.rk;                                                                              \
+            _Pragma("unroll") for (int i = 0; i < SL; ++i) KK_[i] = ld16(rp.k + 32 * i + 8 * q4);      \
+        } else {                                                                                     \
+            _Pragma("unroll") for (int i = 0; i < SL; ++i) KK_[i] = make_uint4(0, 0, 0, 0);           \
+        }                                                                                            \
+        _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+            const int vrow = (B0_) + 8 * h + r8;                                                      \
+            if (vrow < c1) {                                                                         \
+                const RowPtrs<uint16_t> rp = PTRS(vrow, h ? IV1_ : IV0_);                              \
+                if (h) RV1_ = rp.rv; else RV0_ = rp.rv;                                                \
+                _Pragma("unroll") for (int j = 0; j < VQ; ++j) VV_[h][j] = ld16(rp.v + VD * c8 + 8 * j); \
+            } else {                                                                                 \
+                _Pragma("unroll") for (int j = 0; j < VQ; ++j) VV_[h][j] = make_uint4(0, 0, 0, 0);    \
+            }                                                                                        \
+        }                                                                                            \
+    } while (0)
+
+    // One 16-key block: S = Q K^T by MFMA, online softmax (rescaling the
+    // accumulators only when a head's running max grows -- a wave-uniform
+    // branch, since every lane row holds the same scores), P V on the VALU,
+    // then the ring write of rows appended in this call (their data has
+    // already been waited for, so the stores stall nothing).
+#define CMC_COMPUTE_BLOCK(B0_, KR_, VR_, RK_, RV0_, RV1_)                                              \
+    do {                                                                                             \
+        const bool kval = (B0_) + r16 < c1;                                                          \
+        floatx4 c = {0.f, 0.f, 0.f, 0.f};                                                            \
+        _Pragma("unroll") for (int i = 0; i < SL; ++i) {                                             \
+            const bf16x8 kbf = __builtin_bit_cast(bf16x8, KR_[i]);                                    \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_hi[i], kbf, c, 0, 0, 0);                  \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_lo[i], kbf, c, 0, 0, 0);                  \
+        }                                                                                            \
+        float pk[G];                                                                                 \
+        _Pragma("unroll") for (int g = 0; g < G; ++g) {                                              \
+            const float sc = kval ? c[g] : -INFINITY;                                                \
+            const float mb = lane_reduce<OpMax, 1, 16>(sc);                                          \
+            if (mb > st.m[g]) {                                                                      \
+                const float alpha = fast_exp2(st.m[g] - mb);                                         \
+                st.l[g] *= alpha;                                                                    \
+                _Pragma("unroll") for (int i = 0; i < VD; ++i) st.acc[g][i] *= alpha;                \
+                st.m[g] = mb;                                                                        \
+            }                                                                                        \
+            pk[g] = fast_exp2(sc - st.m[g]);                                                         \
+            st.l[g] += pk[g];                                                                        \
+        }                                                                                            \
+        const bool hi_half = (lane & 8) != 0;                                                        \
+        _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+            float pv[G];                                                                             \
+            _Pragma("unroll") for (int g = 0; g < G; ++g) {                                          \
+                const float other = dpp_mov<0x128>(pk[g]); /* row rotate 8 == lane ^ 8 */           \
+                pv[g] = (hi_half == (h == 1)) ? pk[g] : other;                                       \
+            }                                                                                        \
+            _Pragma("unroll") for (int j = 0; j < VQ; ++j) {                                         \
+                float vf[8];                                                                         \
+                Vec16<uint16_t>::widen(VR_[h][j], vf);                                               \
+                _Pragma("unroll") for (int g = 0; g < G; ++g)                                        \
+                    _Pragma("unroll") for (int e = 0; e < 8; ++e)                                    \
+                        st.acc[g][8 * j + e] = fmaf(pv[g], vf[e], st.acc[g][8 * j + e]);             \
+            }                                                                                        \
+        }                                                                                            \
+        if (RK_) { _Pragma("unroll") for (int i = 0; i < SL; ++i) st16(RK_ + 32 * i + 8 * q4, KR_[i]); } \
+        if (RV0_) { _Pragma("unroll") for (int j = 0; j < VQ; ++j) st16(RV0_ + VD * c8 + 8 * j, VR_[0][j]); } \
+        if (RV1_) { _Pragma("unroll") for (int j = 0; j < VQ; ++j) st16(RV1_ + VD * c8 + 8 * j, VR_[1][j]); } \
+    } while (0)
+
+    // Two register sets used in turn (the loop is unrolled by two so the
+    // block being loaded and the block being computed never need a copy).
+    int blk = c0 + wave * 16;
+    int ik, iv0, iv1;
+    uint4 kA[SL], vA[2][VQ], kB[SL], vB[2][VQ];
+    uint16_t *rka = nullptr, *rva0 = nullptr, *rva1 = nullptr;
+    uint16_t *rkb = nullptr, *rvb0 = nullptr, *rvb1 = nullptr;
+    CMC_FETCH_BLOCK(blk, ik, iv0, iv1);
+    if (blk < c1) CMC_LOAD_BLOCK(blk, ik, iv0, iv1, kA, vA, rka, rva0, rva1);
+    CMC_FETCH_BLOCK(blk + BSTRIDE, ik, iv0, iv1);
+    while (blk < c1) {
+        int nb = blk + BSTRIDE;
+        if (nb < c1) {
+            CMC_LOAD_BLOCK(nb, ik, iv0, iv1, kB, vB, rkb, rvb0, rvb1);
+            CMC_FETCH_BLOCK(nb + BSTRIDE, ik, iv0, iv1);
+        }
+        CMC_COMPUTE_BLOCK(blk, kA, vA, rka, rva0, rva1);
+        blk = nb;
+        if (blk >= c1) break;
+        nb = blk + BSTRIDE;
+        if (nb < c1) {
+            CMC_LOAD_BLOCK(nb, ik, iv0, iv1, kA, vA, rka, rva0, rva1);
+            CMC_FETCH_BLOCK(nb + BSTRIDE, ik, iv0, iv1);
+        }
+        CMC_COMPUTE_BLOCK(blk, kB, vB, rkb, rvb0, rvb1);
+        blk = nb;
+    }
+#undef CMC_FETCH_BLOCK
+#undef CMC_LOAD_BLOCK
+#undef CMC_COMPUTE_BLOCK
+    // Wave totals: l over the 16 keys of one lane row (rows hold copies),
+    // acc over the 8 keys sharing a dim group.
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        st.l[g] = lane_reduce<OpSum, 1, 16>(st.l[g]);
+#pragma unroll
+        for (int i = 0; i < VD; ++i) st.acc[g][i] = lane_reduce<OpSum, 1, 8>(st.acc[g][i]);
+    }
+}
+
+// --------------------------------------------------------------- VALU loop
 
 template <typename T, int DH, int G, int U>
-__global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
+__device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T> &rm, int b, int kvh, int c0,
+                                          int c1, WaveState<G, Vec16<T>::N> &st) {
     constexpr int VEC = Vec16<T>::N;
-    constexpr int LPR = DH / VEC;      // lanes per row
-    constexpr int RPW = kWave / LPR;   // rows per wave load
-    constexpr int WAVES = 4;
-    static_assert(LPR >= 1 && LPR <= kWave && (kWave % LPR) == 0, "row layout");
-
-    const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    constexpr int LPR = DH / VEC;
+    constexpr int RPW = kWave / LPR;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int grp = lane / LPR, e = lane % LPR;
+    CMC_UNPACK_ROWMAP(rm);
 
-    int valid = 0;
-    if (p.W > 0) {
-        valid = p.win_count[b];
-        valid = valid < 0 ? 0 : (valid > p.W ? p.W : valid);
-    }
-    const int L = p.k + valid;
-    const int c0 = s * p.chunk;
-    const int c1 = min(c0 + p.chunk, L);
-
-    // This lane's slice of the G query rows, pre-scaled for exp2.
     float qf[G][VEC];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -55,7 +334,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
             p.q + ((size_t)b * p.Hq + (size_t)kvh * G + g) * DH + e * VEC);
 #pragma unroll
         for (int i = 0; i < VEC / 4; ++i) {
-            float4 t = qp[i];
+            const float4 t = qp[i];
             qf[g][4 * i + 0] = t.x * p.qscale;
             qf[g][4 * i + 1] = t.y * p.qscale;
             qf[g][4 * i + 2] = t.z * p.qscale;
@@ -63,24 +342,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
         }
     }
 
-    const size_t head = (size_t)b * p.Hkv + kvh;
-    const T *poolK = static_cast<const T *>(p.cme_k) + head * (size_t)p.N * DH + e * VEC;
-    const T *poolV = static_cast<const T *>(p.cme_v) + head * (size_t)p.N * DH + e * VEC;
-    const T *winK = p.W > 0 ? static_cast<const T *>(p.win_k) + head * (size_t)p.W * DH + e * VEC : nullptr;
-    const T *winV = p.W > 0 ? static_cast<const T *>(p.win_v) + head * (size_t)p.W * DH + e * VEC : nullptr;
-    const int32_t *idxb = p.idx ? p.idx + (size_t)b * p.k : nullptr;
-    const int nmax = p.N > 0 ? p.N - 1 : 0;
-
-    float m[G], l[G], acc[G][VEC];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        m[g] = -INFINITY;
-        l[g] = 0.f;
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) acc[g][i] = 0.f;
-    }
-
-    constexpr int STRIDE = WAVES * RPW;  // rows between a wave's consecutive loads
+    constexpr int STRIDE = kWaves * RPW;
     for (int r0 = c0 + wave * RPW; r0 < c1; r0 += STRIDE * U) {
         uint4 kr[U], vr[U];
         bool ok[U];
@@ -88,25 +350,17 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
         for (int u = 0; u < U; ++u) {
             const int row = r0 + u * STRIDE + grp;
             ok[u] = row < c1;
-            kr[u] = make_uint4(0, 0, 0, 0);
-            vr[u] = make_uint4(0, 0, 0, 0);
+            kr[u] = vr[u] = make_uint4(0, 0, 0, 0);
             if (ok[u]) {
-                const T *kp, *vp;
-                if (row < p.k) {
-                    int r = idxb ? idxb[row] : row;
-                    r = r < 0 ? 0 : (r > nmax ? nmax : r);
-                    kp = poolK + (size_t)r * DH;
-                    vp = poolV + (size_t)r * DH;
-                } else {
-                    const int slot = row - p.k;
-                    kp = winK + (size_t)slot * DH;
-                    vp = winV + (size_t)slot * DH;
+                const RowPtrs<T> rp = LOCATE(row);
+                kr[u] = ld16(rp.k + e * VEC);
+                vr[u] = ld16(rp.v + e * VEC);
+                if (rp.rk) {
+                    st16(rp.rk + e * VEC, kr[u]);
+                    st16(rp.rv + e * VEC, vr[u]);
                 }
-                kr[u] = *reinterpret_cast<const uint4 *>(kp);
-                vr[u] = *reinterpret_cast<const uint4 *>(vp);
             }
         }
-
         float sc[U][G];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -121,123 +375,226 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeParams p) {
                 sc[u][g] = ok[u] ? d : -INFINITY;
             }
         }
-
         float vf[U][VEC];
 #pragma unroll
         for (int u = 0; u < U; ++u) Vec16<T>::widen(vr[u], vf[u]);
-
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             float mb = sc[0][g];
 #pragma unroll
             for (int u = 1; u < U; ++u) mb = fmaxf(mb, sc[u][g]);
-            mb = lane_reduce<OpMax, LPR, kWave>(mb);    // max over the wave's rows
-            const float mn = fmaxf(m[g], mb);            // finite: row r0 is valid
-            const float alpha = exp2f(m[g] - mn);
-            l[g] *= alpha;
+            mb = lane_reduce<OpMax, LPR, kWave>(mb);
+            const float mn = fmaxf(st.m[g], mb);
+            const float alpha = exp2f(st.m[g] - mn);
+            st.l[g] *= alpha;
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) acc[g][i] *= alpha;
+            for (int i = 0; i < VEC; ++i) st.acc[g][i] *= alpha;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const float pu = exp2f(sc[u][g] - mn);
-                l[g] += pu;
+                st.l[g] += pu;
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) acc[g][i] = fmaf(pu, vf[u][i], acc[g][i]);
+                for (int i = 0; i < VEC; ++i) st.acc[g][i] = fmaf(pu, vf[u][i], st.acc[g][i]);
             }
-            m[g] = mn;
+            st.m[g] = mn;
         }
     }
-
-    // Sum the row groups of each wave (m is already wave-uniform).
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        l[g] = lane_reduce<OpSum, LPR, kWave>(l[g]);
+        st.l[g] = lane_reduce<OpSum, LPR, kWave>(st.l[g]);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) acc[g][i] = lane_reduce<OpSum, LPR, kWave>(acc[g][i]);
+        for (int i = 0; i < VEC; ++i) st.acc[g][i] = lane_reduce<OpSum, LPR, kWave>(st.acc[g][i]);
+    }
+}
+
+// ------------------------------------------------------------------ kernel
+
+// Cross-workgroup publication without device-scope fences.  The partials are
+// written and read with relaxed agent-scope atomic accesses (coherent across
+// the XCDs' L2 caches, unlike plain accesses), the writer waits until its
+// stores have completed (s_waitcnt) before arriving on the counter, and the
+// reader issues its loads only after the arrival count has returned.  An
+// agent-scope fence would instead write back and invalidate the whole L2 of
+// the XCD for every workgroup, which costs microseconds each.
+__device__ __forceinline__ void coherent_store(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float coherent_load(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Combine the four waves' (m, l, acc) of head g, dim d; returns the joint max.
+template <int G, int DH>
+__device__ __forceinline__ float combine_waves(const float (&sm)[kWaves][G], const float (&sl)[kWaves][G],
+                                               const float (&sa)[kWaves][G][DH], int g, int d, float &num,
+                                               float &den) {
+    float M = sm[0][g];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm[w][g]);
+    num = 0.f;
+    den = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float f = exp2f(sm[w][g] - M);
+            num = fmaf(f, sa[w][g][d], num);
+            den = fmaf(f, sl[w][g], den);
+        }
+    }
+    return M;
+}
+
+template <typename T, int DH, int G, bool MF>
+__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+    constexpr int VEC = MF ? DH / 8 : Vec16<T>::N;   // output dims a lane accumulates
+    const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+
+    int cnt0 = 0, cnt_raw = 0, valid = 0, slot0 = 0;
+    if (p.W > 0) {
+        cnt_raw = p.win_count[b];
+        cnt0 = cnt_raw < 0 ? 0 : cnt_raw;
+        const long long cnt1 = (long long)cnt0 + p.T_new;
+        valid = cnt1 < p.W ? (int)cnt1 : p.W;
+        slot0 = cnt0 % p.W;
+    }
+    const int L = p.k + valid;
+    const int c0 = s * p.chunk;
+    const int c1 = min(c0 + p.chunk, L);
+    const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, slot0);
+
+    WaveState<G, VEC> st;
+    st.init();
+    if constexpr (MF) {
+        mfma_loop<DH, G>(p, rm, b, kvh, c0, c1, st);
+    } else {
+        constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
+        valu_loop<T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
 
-    // Combine the four waves through LDS.
-    __shared__ float s_acc[WAVES][G][DH];
-    __shared__ float s_m[WAVES][G], s_l[WAVES][G];
-    if (grp == 0) {
+    // Lanes holding each dim group after the wave reduction.
+    constexpr int LPR = MF ? 8 : DH / Vec16<T>::N;         // lanes per dim group stride
+    const bool holder = MF ? ((lane & 7) == 0) : (lane < LPR);
+    const int dbase = MF ? (lane >> 3) * VEC : lane * VEC;
+
+    __shared__ float s_acc[kWaves][G][DH];
+    __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+    if (holder) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) s_acc[wave][g][dbase + i] = st.acc[g][i];
+    }
+    if (lane == 0) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) s_acc[wave][g][e * VEC + i] = acc[g][i];
-            if (e == 0) {
-                s_m[wave][g] = m[g];
-                s_l[wave][g] = l[g];
-            }
+            s_m[wave][g] = st.m[g];
+            s_l[wave][g] = st.l[g];
         }
     }
     __syncthreads();
 
-    const size_t part = (head * p.S + s) * G;
-    for (int t = threadIdx.x; t < G * DH; t += 256) {
-        const int g = t / DH, d = t % DH;
-        float M = s_m[0][g];
-#pragma unroll
-        for (int w = 1; w < WAVES; ++w) M = fmaxf(M, s_m[w][g]);
-        float num = 0.f, den = 0.f;
-        if (M != -INFINITY) {
-#pragma unroll
-            for (int w = 0; w < WAVES; ++w) {
-                const float f = exp2f(s_m[w][g] - M);
-                num = fmaf(f, s_acc[w][g][d], num);
-                den = fmaf(f, s_l[w][g], den);
+    const size_t head = (size_t)b * p.Hkv + kvh;
+    float *outp = p.out + ((size_t)b * p.Hq + (size_t)kvh * G) * DH;
+    __shared__ int s_last;
+    if (p.S == 1) {
+        for (int t = threadIdx.x; t < G * DH; t += kThreads) {
+            const int g = t / DH, d = t % DH;
+            float num, den;
+            combine_waves<G, DH>(s_m, s_l, s_acc, g, d, num, den);
+            outp[t] = den > 0.f ? num / den : 0.f;
+        }
+    } else {
+        // Publish this split's partial with agent-coherent stores, wait for
+        // them to complete, then arrive on the (b, kv head) counter.
+        const size_t part = (head * p.S + s) * G;
+        for (int t = threadIdx.x; t < G * DH; t += kThreads) {
+            const int g = t / DH, d = t % DH;
+            float num, den;
+            const float M = combine_waves<G, DH>(s_m, s_l, s_acc, g, d, num, den);
+            coherent_store(&p.part_acc[(part + g) * DH + d], num);
+            if (d == 0) {
+                coherent_store(&p.part_ml[(part + g) * 2 + 0], M);
+                coherent_store(&p.part_ml[(part + g) * 2 + 1], den);
             }
         }
-        p.part_acc[(part + g) * DH + d] = num;
-        if (d == 0) {
-            p.part_ml[(part + g) * 2 + 0] = M;
-            p.part_ml[(part + g) * 2 + 1] = den;
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const unsigned prev = __hip_atomic_fetch_add(&p.pair_counter[head], 1u, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+            s_last = prev == (unsigned)(p.S - 1);
         }
-    }
-}
-
-template <int DH, int G>
-__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams p) {
-    const int kvh = blockIdx.x, b = blockIdx.y;
-    const size_t head = (size_t)b * p.Hkv + kvh;
-    for (int t = threadIdx.x; t < G * DH; t += 256) {
-        const int g = t / DH, d = t % DH;
+        __syncthreads();
+        if (!s_last) return;  // workgroup-uniform
+        // The last split merges all S partials in fixed split order: the
+        // (m, l) pairs are staged in LDS with one parallel load, the acc
+        // partials are fetched kMergeBatch at a time so their loads overlap.
         const float *ml = p.part_ml + head * p.S * G * 2;
         const float *ac = p.part_acc + head * p.S * G * DH;
-        float M = -INFINITY;
-        for (int s = 0; s < p.S; ++s) M = fmaxf(M, ml[(s * G + g) * 2]);
-        float o = 0.f;
-        if (M != -INFINITY) {
+        float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= kWaves*G*DH floats (S <= 2*DH)
+        for (int t = threadIdx.x; t < p.S * G * 2; t += kThreads) s_ml[t] = coherent_load(&ml[t]);
+        __syncthreads();
+        for (int t = threadIdx.x; t < G * DH; t += kThreads) {
+            const int g = t / DH, d = t % DH;
+            float M = -INFINITY;
+            for (int q = 0; q < p.S; ++q) M = fmaxf(M, s_ml[(q * G + g) * 2]);
             float num = 0.f, den = 0.f;
-            for (int s = 0; s < p.S; ++s) {
-                const float f = exp2f(ml[(s * G + g) * 2] - M);
-                den = fmaf(f, ml[(s * G + g) * 2 + 1], den);
-                num = fmaf(f, ac[(s * G + g) * DH + d], num);
+            if (M != -INFINITY) {
+                for (int q0 = 0; q0 < p.S; q0 += kMergeBatch) {
+                    float a[kMergeBatch];
+#pragma unroll
+                    for (int j = 0; j < kMergeBatch; ++j)
+                        a[j] = q0 + j < p.S ? coherent_load(&ac[((q0 + j) * G + g) * DH + d]) : 0.f;
+#pragma unroll
+                    for (int j = 0; j < kMergeBatch; ++j) {
+                        if (q0 + j < p.S) {
+                            const int q = q0 + j;
+                            const float f = exp2f(s_ml[(q * G + g) * 2] - M);
+                            den = fmaf(f, s_ml[(q * G + g) * 2 + 1], den);
+                            num = fmaf(f, a[j], num);
+                        }
+                    }
+                }
             }
-            o = num / den;
+            outp[t] = den > 0.f ? num / den : 0.f;
         }
-        p.out[((size_t)b * p.Hq + (size_t)kvh * G + g) * DH + d] = o;
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&p.pair_counter[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    // Advance the ring count once every workgroup of the sequence has read
+    // it: each (b, kv head) arrives once -- the single split, or the last of
+    // its S splits, every one of which read the count before arriving on the
+    // pair counter.  The single-split increment depends on the loaded count,
+    // so it cannot be issued before that load returns.  The last arrival
+    // writes the new count and re-arms the counter.
+    if (p.T_new > 0 && p.W > 0 && threadIdx.x == 0) {
+        const unsigned one = (unsigned)(cnt_raw != INT_MIN);  // == 1
+        const unsigned prev = __hip_atomic_fetch_add(&p.seq_counter[b], one, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        if (prev == (unsigned)(p.Hkv - 1)) {
+            p.win_count[b] = cnt0 + p.T_new;
+            __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 
 template <typename T, int DH, int G>
-hipError_t launch_typed(const DecodeParams &p, hipStream_t stream) {
-    constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
-    dim3 g1(p.S, p.Hkv, p.B);
-    decode_split_kernel<T, DH, G, U><<<g1, 256, 0, stream>>>(p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    dim3 g2(p.Hkv, p.B);
-    decode_merge_kernel<DH, G><<<g2, 256, 0, stream>>>(p);
+hipError_t launch3(const DecodeParams &p, hipStream_t stream) {
+    dim3 grid(p.S, p.Hkv, p.B);
+    constexpr bool kMf = sizeof(T) == 2 && G <= 4;
+    decode_kernel<T, DH, G, kMf><<<grid, kThreads, 0, stream>>>(p);
     return hipGetLastError();
 }
 
 template <typename T, int DH>
 hipError_t launch_g(const DecodeParams &p, int G, hipStream_t stream) {
     switch (G) {
-        case 1: return launch_typed<T, DH, 1>(p, stream);
-        case 2: return launch_typed<T, DH, 2>(p, stream);
-        case 4: return launch_typed<T, DH, 4>(p, stream);
-        case 8: return launch_typed<T, DH, 8>(p, stream);
+        case 1: return launch3<T, DH, 1>(p, stream);
+        case 2: return launch3<T, DH, 2>(p, stream);
+        case 4: return launch3<T, DH, 4>(p, stream);
+        case 8: return launch3<T, DH, 8>(p, stream);
     }
     return hipErrorInvalidValue;
 }

@@ -12,22 +12,27 @@ struct DecodeParams {
     const void *cme_k;        // [B][Hkv][N][Dh]
     const void *cme_v;
     const int32_t *idx;       // [B][k] or nullptr
-    const void *win_k;        // [B][Hkv][W][Dh]
-    const void *win_v;
-    const int32_t *win_count; // [B]
+    void *win_k;              // [B][Hkv][W][Dh]; written only for rows appended this call
+    void *win_v;
+    int32_t *win_count;       // [B]; advanced by T_new when T_new > 0
+    const void *new_k;        // [B][Hkv][T_new][Dh] rows appended by this call, or nullptr
+    const void *new_v;
     float *out;               // [B][Hq][Dh]
     float *part_ml;           // [B][Hkv][S][G][2]   (running max in log2 units, denominator)
     float *part_acc;          // [B][Hkv][S][G][Dh]  (unnormalised numerator)
-    int k, W, B, Hq, Hkv, N;
+    unsigned *pair_counter;   // [B][Hkv] split arrivals, zero between calls
+    unsigned *seq_counter;    // [B] kv-head arrivals, zero between calls
+    int k, W, B, Hq, Hkv, N, T_new;
     int S, chunk;             // key-axis splits and keys per split
     float qscale;             // scale * log2(e)
 };
 
 // Key-axis split plan; depends only on sizes, so the workspace query and the
-// launch agree.
+// launch agree.  Workspace layout: [sequence counters | pair counters]
+// (zero between calls), then the per-split partials.
 struct DecodePlan {
     int S = 0, chunk = 0;
-    size_t ml_bytes = 0, acc_bytes = 0, total = 0;
+    size_t counter_bytes = 0, ml_bytes = 0, acc_bytes = 0, total = 0;
 };
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W);
 

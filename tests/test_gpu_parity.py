@@ -127,7 +127,7 @@ def _logit_bound_tol(q, keys_f64, scale, vmax, Dh):
 
 
 def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_none=False, scale=None,
-                 kv_std=1.0, derived_tol=False):
+                 kv_std=1.0, derived_tol=False, fused=False, t_new=1):
     rng = np.random.default_rng(seed)
     f = lambda *s: (rng.standard_normal(s) * kv_std).astype(np.float32)
     cv = _bf16 if dtype == "bf16" else (lambda x: x)
@@ -146,18 +146,31 @@ def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_n
     scale = 1.0 / math.sqrt(Dh) if scale is None else scale
     d = dict(pk=to_dev(pk), pv=to_dev(pv), idx=None if idx is None else to_dev(idx),
              wk=to_dev(wk) if W else None, wv=to_dev(wv) if W else None, wc=to_dev(cnt) if W else None)
+    ws = cmc.decode_workspace(B, Hq, Hkv, Dh, k, W, DEV)
     worst = 0.0
     for step in range(steps):
-        say(f"decode {dtype} B={B} Hq={Hq} Hkv={Hkv} Dh={Dh} N={N} k={k} W={W} fill={fill} step={step}")
+        say(f"decode {dtype} B={B} Hq={Hq} Hkv={Hkv} Dh={Dh} N={N} k={k} W={W} fill={fill} "
+            f"fused={fused} t_new={t_new} step={step}")
+        nk = nv = None
         if W:
-            nk, nv = cv(f(B, Hkv, 1, Dh)), cv(f(B, Hkv, 1, Dh))
+            nk, nv = cv(f(B, Hkv, t_new, Dh)), cv(f(B, Hkv, t_new, Dh))
             orc.window_append(wk, wv, cnt, nk, nv)
-            cmc.cmc_window_append(d["wk"], d["wv"], d["wc"], to_dev(nk), to_dev(nv))
+            if not fused:
+                cmc.cmc_window_append(d["wk"], d["wv"], d["wc"], to_dev(nk), to_dev(nv))
         q = f(B, Hq, Dh)
         ref = orc.two_tier_decode(q, pk, pv, idx, k, wk, wv, cnt, W, scale)
-        out = cmc.cmc_two_tier_decode(to_dev(q), d["pk"], d["pv"], d["idx"], k, d["wk"], d["wv"], d["wc"],
-                                      scale, W=W)
+        if fused:
+            out = cmc.cmc_decode_step(to_dev(q), d["pk"], d["pv"], d["idx"], k, d["wk"], d["wv"], d["wc"],
+                                      None if nk is None else to_dev(nk), None if nv is None else to_dev(nv),
+                                      scale, W=W, workspace=ws)
+        else:
+            out = cmc.cmc_two_tier_decode(to_dev(q), d["pk"], d["pv"], d["idx"], k, d["wk"], d["wv"], d["wc"],
+                                          scale, W=W, workspace=ws)
         torch.cuda.synchronize()
+        assert not ws[:4 * (B + B * Hkv)].any(), "arrival counters must return to zero"
+        if W:
+            assert (to_host(d["wk"]) == wk).all() and (to_host(d["wv"]) == wv).all(), "ring contents"
+            assert (to_host(d["wc"]) == cnt).all(), "ring count"
         err = max_abs(to_host(out), ref)
         worst = max(worst, err)
         tol = tol_for(dtype)
@@ -177,11 +190,22 @@ def test_decode_head_shapes(orc, dtype, Dh, G):
     _decode_case(orc, B=2, Hq=2 * G, Hkv=2, Dh=Dh, N=97, k=37, W=19, fill=11, dtype=dtype, seed=Dh + G)
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("k,W,fill", [(1, 0, 0), (0, 5, 2), (0, 64, 64), (300, 0, 0), (5, 1, 0),
                                       (2000, 3000, 2999), (513, 700, 0)])
-def test_decode_key_counts(orc, k, W, fill):
+def test_decode_key_counts(orc, k, W, fill, fused):
     _decode_case(orc, B=2, Hq=8, Hkv=2, Dh=128, N=max(k, 1) + 50, k=k, W=W, fill=fill, dtype="bf16",
-                 seed=k * 7 + W)
+                 seed=k * 7 + W, fused=fused)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Dh,G", [(64, 4), (128, 4), (128, 1), (256, 1), (128, 8), (64, 2)])
+@pytest.mark.parametrize("t_new,W,fill", [(1, 7, 0), (2, 9, 9), (3, 300, 100), (5, 5, 3)])
+def test_decode_step_fused(orc, dtype, Dh, G, t_new, W, fill):
+    """Append fused into the decode launch equals append then decode, and
+    the ring contents/count match the oracle's after every step."""
+    _decode_case(orc, B=3, Hq=2 * G, Hkv=2, Dh=Dh, N=300, k=120, W=W, fill=fill, dtype=dtype,
+                 seed=Dh * G + t_new + W, steps=4, fused=True, t_new=t_new)
 
 
 def test_decode_empty_window_zero_output(orc):
