@@ -63,6 +63,8 @@ def parse():
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from Python instead of replaying a captured HIP graph")
     ap.add_argument("--out", default=None, help="also append the JSON line to this file")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run plain device-to-device copies of MIB MiB (calibrates byte counters) and exit")
     return ap.parse_args()
 
 
@@ -199,6 +201,16 @@ def main():
     import torch
     from paper_2609_25537_amd import cmc
     from paper_2609_25537_amd import workloads as wl
+
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
 
     cmc.lib()  # fail loudly before any work if the HIP library is missing
     dev = torch.device("cuda:0")

@@ -42,12 +42,14 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 namespace cmc {
 
-// Key-axis split plan.  Aim for about kTargetWG workgroups in flight (a few
-// per CU on 256 CUs) without cutting a split below kGranule keys (4 waves x
-// 16-key blocks); the plan depends only on sizes, so the workspace query and
-// the launch always agree.
+// Key-axis split plan.  Aim for about kTargetWG workgroups: the decode kernel
+// keeps two workgroups resident per CU, so 512 fill the 256 CUs in one round;
+// a (sequence, kv head) pair is split only when there are fewer pairs than
+// that, and never below kGranule keys (4 waves x 16-key blocks) per split.
+// The plan depends only on sizes, so the workspace query and the launch
+// always agree.
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
-    constexpr long long kTargetWG = 1024;
+    constexpr long long kTargetWG = 512;
     constexpr long long kGranule = 64;
     constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
     DecodePlan pl;

@@ -141,6 +141,15 @@ __device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, i
     return m;
 }
 
+// Orders this wave's LDS writes before its following LDS reads (and reads
+// before later writes): LDS operations of one wave execute in order, so only
+// the compiler must be kept from moving them across this point.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // 2^x with the hardware instruction alone (no denormal-result fix-up; a
 // softmax weight below 2^-126 contributes nothing at fp32 precision anyway).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -164,83 +173,132 @@ struct WaveState {
 };
 
 // --------------------------------------------------------------- MFMA loop
+//
+// The MFMA path walks the key list in three phases, each a contiguous run of
+// rows addressed from one uniform base with 32-bit offsets:
+//   pool  rows [0, k):           pool row idx[row] (clamped into the pool);
+//   ring  rows [k, k + n_old):   the n_old = min(count, W - T_new) ring slots
+//                                that survive this call's append, starting
+//                                at slot (count - n_old) mod W;
+//   new   rows [k + n_old, L):   the T_new rows appended in this call, read
+//                                from new_k/new_v and written to ring slots
+//                                (count + t) mod W.
+// That is the same key set as [pool rows] ++ [ring slots after the append];
+// softmax attention does not depend on key order.
 
+struct PoolRows {
+    const int32_t *idx;  // this sequence's index list, or nullptr
+    int nmax;
+    __device__ __forceinline__ int key(int row) const { return idx ? idx[row] : row; }
+    __device__ __forceinline__ int slot(int, int key) const { return key < 0 ? 0 : (key > nmax ? nmax : key); }
+};
+struct RingRows {
+    int first, s_old, W;  // row `first` is ring slot s_old
+    __device__ __forceinline__ int key(int row) const { return row; }
+    __device__ __forceinline__ int slot(int row, int) const {
+        const int sl = s_old + (row - first);
+        return sl >= W ? sl - W : sl;
+    }
+};
+struct NewRows {
+    int first, slot0, W;  // row `first` is appended row 0, bound for ring slot slot0
+    __device__ __forceinline__ int key(int row) const { return row; }
+    __device__ __forceinline__ int slot(int row, int) const { return row - first; }
+    __device__ __forceinline__ int ring_slot(int row) const {
+        const int sl = slot0 + (row - first);
+        return sl >= W ? sl - W : sl;
+    }
+};
+
+// q's A operand: this lane's slice of query head (lane % 16) % G, pre-scaled,
+// as bf16 hi + lo parts.
 template <int DH, int G>
-__device__ __forceinline__ void mfma_loop(const DecodeParams &p, const RowMap<uint16_t> &rm, int b, int kvh,
-                                          int c0, int c1, WaveState<G, DH / 8> &st) {
-    constexpr int SL = DH / 32;      // MFMA k-slices
-    constexpr int VD = DH / 8;       // P V output dims per lane
-    constexpr int VQ = DH / 64;      // 16-byte V loads per lane per half block
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int r16 = lane & 15, q4 = lane >> 4, r8 = lane & 7, c8 = lane >> 3;
-    CMC_UNPACK_ROWMAP(rm);
-
-    // A operand: the lane's slice of query head (r16 % G), pre-scaled, as bf16 hi + lo.
-    bf16x8 qa_hi[SL], qa_lo[SL];
-    {
-        const float *qp = p.q + ((size_t)b * p.Hq + (size_t)kvh * G + (r16 % G)) * DH + 8 * q4;
+__device__ __forceinline__ void load_q_operand(const DecodeParams &p, int b, int kvh, bf16x8 (&qa_hi)[DH / 32],
+                                               bf16x8 (&qa_lo)[DH / 32]) {
+    const int lane = threadIdx.x & 63;
+    const int r16 = lane & 15, q4 = lane >> 4;
+    const float *qp = p.q + ((size_t)b * p.Hq + (size_t)kvh * G + (r16 % G)) * DH + 8 * q4;
 #pragma unroll
-        for (int i = 0; i < SL; ++i) {
-            const float4 x0 = *reinterpret_cast<const float4 *>(qp + 32 * i);
-            const float4 x1 = *reinterpret_cast<const float4 *>(qp + 32 * i + 4);
-            const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    for (int i = 0; i < DH / 32; ++i) {
+        const float4 x0 = *reinterpret_cast<const float4 *>(qp + 32 * i);
+        const float4 x1 = *reinterpret_cast<const float4 *>(qp + 32 * i + 4);
+        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = xs[e] * p.qscale;
-                const __bf16 h = (__bf16)v;
-                qa_hi[i][e] = h;
-                qa_lo[i][e] = (__bf16)(v - (float)h);
-            }
+        for (int e = 0; e < 8; ++e) {
+            const float v = xs[e] * p.qscale;
+            const __bf16 h = (__bf16)v;
+            qa_hi[i][e] = h;
+            qa_lo[i][e] = (__bf16)(v - (float)h);
         }
     }
+}
 
+// One phase: rows [r0, r1) from bases kbase/vbase (bytes).  A wave takes 16
+// rows per block.  K: the lane's row blk + (lane % 16) in the MFMA B layout
+// (dims 32i + 8*(lane/16) .. +7).  V: four quarters of 4 rows; in quarter qq
+// the lane owns row blk + 4qq + (lane % 4) and dims (DH/16)*(lane/4) ..
+// +DH/16-1, so each lane accumulates DH/16 output dims per head.  The p
+// values travel from the score layout (lane r holds key r's G weights) to
+// the V layout through a 16 x G slot of LDS private to the wave.  Keys
+// (index-list entries) are fetched one block ahead of the K/V rows, and the
+// K/V rows one block ahead of their use.
+template <int DH, int G, class Rows, bool RING_WRITE>
+__device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, const char *kbase, const char *vbase,
+                                           char *ringK, char *ringV, const bf16x8 (&qa_hi)[DH / 32],
+                                           const bf16x8 (&qa_lo)[DH / 32], float *s_p,
+                                           WaveState<G, DH / 16> &st) {
+    constexpr int SL = DH / 32, VD = DH / 16, RB = DH * 2;
+    constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
+    constexpr int VW = VB >= 16 ? VB / 16 : 1; // 16-byte words (or one 8-byte word)
     constexpr int BSTRIDE = kWaves * 16;
-    // Rows of a block: the lane's K row blk + r16 (MFMA B layout, dims
-    // 32i + 8*q4 .. +7) and its V rows blk + 8h + r8 for the two halves
-    // (dims VD*c8 .. +VD-1).  Index-list entries are fetched one block ahead
-    // of the K/V rows, and the K/V rows one block ahead of their use.
-#define CMC_FETCH_BLOCK(b0, ik, iv0, iv1) \
-    do {                                  \
-        ik = FETCH((b0) + r16);           \
-        iv0 = FETCH((b0) + r8);           \
-        iv1 = FETCH((b0) + 8 + r8);       \
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, q4 = lane >> 4, kq = lane & 3, dg = lane >> 2;
+    const uint32_t koff = 16u * q4;        // + 64 * i for slice i
+    const uint32_t voff = (uint32_t)VB * dg;
+
+    int blk = r0 + wave * 16;
+    if (blk >= r1) return;  // wave-uniform
+
+#define CMC_KEYS(B0_, K_, V_)                                                   \
+    do {                                                                       \
+        K_ = (B0_) + r16 < r1 ? rows.key((B0_) + r16) : 0;                     \
+        _Pragma("unroll") for (int qq = 0; qq < 4; ++qq)                       \
+            V_[qq] = (B0_) + 4 * qq + kq < r1 ? rows.key((B0_) + 4 * qq + kq) : 0; \
     } while (0)
-#define CMC_LOAD_BLOCK(B0_, IK_, IV0_, IV1_, KK_, VV_, RK_, RV0_, RV1_)                                         \
+#define CMC_LOAD(B0_, K_, V_, KR_, VR_)                                                                \
     do {                                                                                             \
-        RK_ = nullptr;                                                                                \
-        RV0_ = RV1_ = nullptr;                                                                         \
-        if ((B0_) + r16 < c1) {                                                                       \
-            const RowPtrs<uint16_t> rp = PTRS((B0_) + r16, IK_);                                       \
-            RK_ = rp.rk;                                                                              \
-            _Pragma("unroll") for (int i = 0; i < SL; ++i) KK_[i] = ld16(rp.k + 32 * i + 8 * q4);      \
+        if ((B0_) + r16 < r1) {                                                                      \
+            const uint32_t o = (uint32_t)rows.slot((B0_) + r16, K_) * RB + koff;                    \
+            _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = ld16(kbase + o + 64 * i);        \
         } else {                                                                                     \
-            _Pragma("unroll") for (int i = 0; i < SL; ++i) KK_[i] = make_uint4(0, 0, 0, 0);           \
+            _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = make_uint4(0, 0, 0, 0);          \
         }                                                                                            \
-        _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
-            const int vrow = (B0_) + 8 * h + r8;                                                      \
-            if (vrow < c1) {                                                                         \
-                const RowPtrs<uint16_t> rp = PTRS(vrow, h ? IV1_ : IV0_);                              \
-                if (h) RV1_ = rp.rv; else RV0_ = rp.rv;                                                \
-                _Pragma("unroll") for (int j = 0; j < VQ; ++j) VV_[h][j] = ld16(rp.v + VD * c8 + 8 * j); \
+        _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
+            const int vrow = (B0_) + 4 * qq + kq;                                                    \
+            if (vrow < r1) {                                                                         \
+                const uint32_t o = (uint32_t)rows.slot(vrow, V_[qq]) * RB + voff;                   \
+                if constexpr (VB >= 16) {                                                            \
+                    _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = ld16(vbase + o + 16 * j); \
+                } else {                                                                             \
+                    const uint2 t = *reinterpret_cast<const uint2 *>(vbase + o);                     \
+                    VR_[qq][0] = make_uint4(t.x, t.y, 0, 0);                                         \
+                }                                                                                    \
             } else {                                                                                 \
-                _Pragma("unroll") for (int j = 0; j < VQ; ++j) VV_[h][j] = make_uint4(0, 0, 0, 0);    \
+                _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = make_uint4(0, 0, 0, 0);  \
             }                                                                                        \
         }                                                                                            \
     } while (0)
-
-    // One 16-key block: S = Q K^T by MFMA, online softmax (rescaling the
-    // accumulators only when a head's running max grows -- a wave-uniform
-    // branch, since every lane row holds the same scores), P V on the VALU,
-    // then the ring write of rows appended in this call (their data has
-    // already been waited for, so the stores stall nothing).
-#define CMC_COMPUTE_BLOCK(B0_, KR_, VR_, RK_, RV0_, RV1_)                                              \
+    // S = Q K^T by MFMA; online softmax rescaling the accumulators only when
+    // a head's running max grows (wave-uniform: every lane row holds the same
+    // scores); P V on the VALU.
+#define CMC_COMPUTE(B0_, KR_, VR_)                                                                     \
     do {                                                                                             \
-        const bool kval = (B0_) + r16 < c1;                                                          \
+        const bool kval = (B0_) + r16 < r1;                                                          \
         floatx4 c = {0.f, 0.f, 0.f, 0.f};                                                            \
         _Pragma("unroll") for (int i = 0; i < SL; ++i) {                                             \
-            const bf16x8 kbf = __builtin_bit_cast(bf16x8, KR_[i]);                                    \
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_hi[i], kbf, c, 0, 0, 0);                  \
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_lo[i], kbf, c, 0, 0, 0);                  \
+            const bf16x8 kbf = __builtin_bit_cast(bf16x8, KR_[i]);                                   \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_hi[i], kbf, c, 0, 0, 0);                 \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_lo[i], kbf, c, 0, 0, 0);                 \
         }                                                                                            \
         float pk[G];                                                                                 \
         _Pragma("unroll") for (int g = 0; g < G; ++g) {                                              \
@@ -255,63 +313,116 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, const RowMap<ui
             pk[g] = fast_exp2(sc - st.m[g]);                                                         \
             st.l[g] += pk[g];                                                                        \
         }                                                                                            \
-        const bool hi_half = (lane & 8) != 0;                                                        \
-        _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+        if (q4 == 0) {                                                                               \
+            _Pragma("unroll") for (int g = 0; g < G; ++g) s_p[r16 * G + g] = pk[g];                 \
+        }                                                                                            \
+        wave_lds_sync();                                                                             \
+        _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
             float pv[G];                                                                             \
-            _Pragma("unroll") for (int g = 0; g < G; ++g) {                                          \
-                const float other = dpp_mov<0x128>(pk[g]); /* row rotate 8 == lane ^ 8 */           \
-                pv[g] = (hi_half == (h == 1)) ? pk[g] : other;                                       \
-            }                                                                                        \
-            _Pragma("unroll") for (int j = 0; j < VQ; ++j) {                                         \
+            _Pragma("unroll") for (int g = 0; g < G; ++g) pv[g] = s_p[(4 * qq + kq) * G + g];         \
+            _Pragma("unroll") for (int j = 0; j < VW; ++j) {                                         \
                 float vf[8];                                                                         \
-                Vec16<uint16_t>::widen(VR_[h][j], vf);                                               \
+                Vec16<uint16_t>::widen(VR_[qq][j], vf);                                              \
                 _Pragma("unroll") for (int g = 0; g < G; ++g)                                        \
-                    _Pragma("unroll") for (int e = 0; e < 8; ++e)                                    \
+                    _Pragma("unroll") for (int e = 0; e < (VD < 8 ? VD : 8); ++e)                    \
                         st.acc[g][8 * j + e] = fmaf(pv[g], vf[e], st.acc[g][8 * j + e]);             \
             }                                                                                        \
         }                                                                                            \
-        if (RK_) { _Pragma("unroll") for (int i = 0; i < SL; ++i) st16(RK_ + 32 * i + 8 * q4, KR_[i]); } \
-        if (RV0_) { _Pragma("unroll") for (int j = 0; j < VQ; ++j) st16(RV0_ + VD * c8 + 8 * j, VR_[0][j]); } \
-        if (RV1_) { _Pragma("unroll") for (int j = 0; j < VQ; ++j) st16(RV1_ + VD * c8 + 8 * j, VR_[1][j]); } \
+        wave_lds_sync();                                                                             \
+        if constexpr (RING_WRITE) {                                                                  \
+            if ((B0_) + r16 < r1) {                                                                  \
+                const uint32_t o = (uint32_t)rows.ring_slot((B0_) + r16) * RB + koff;                \
+                _Pragma("unroll") for (int i = 0; i < SL; ++i) st16(ringK + o + 64 * i, KR_[i]);     \
+            }                                                                                        \
+            _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                       \
+                const int vrow = (B0_) + 4 * qq + kq;                                                \
+                if (vrow < r1) {                                                                     \
+                    const uint32_t o = (uint32_t)rows.ring_slot(vrow) * RB + voff;                   \
+                    if constexpr (VB >= 16) {                                                        \
+                        _Pragma("unroll") for (int j = 0; j < VW; ++j) st16(ringV + o + 16 * j, VR_[qq][j]); \
+                    } else {                                                                         \
+                        *reinterpret_cast<uint2 *>(ringV + o) = make_uint2(VR_[qq][0].x, VR_[qq][0].y); \
+                    }                                                                                \
+                }                                                                                    \
+            }                                                                                        \
+        }                                                                                            \
     } while (0)
 
-    // Two register sets used in turn (the loop is unrolled by two so the
-    // block being loaded and the block being computed never need a copy).
-    int blk = c0 + wave * 16;
-    int ik, iv0, iv1;
-    uint4 kA[SL], vA[2][VQ], kB[SL], vB[2][VQ];
-    uint16_t *rka = nullptr, *rva0 = nullptr, *rva1 = nullptr;
-    uint16_t *rkb = nullptr, *rvb0 = nullptr, *rvb1 = nullptr;
-    CMC_FETCH_BLOCK(blk, ik, iv0, iv1);
-    if (blk < c1) CMC_LOAD_BLOCK(blk, ik, iv0, iv1, kA, vA, rka, rva0, rva1);
-    CMC_FETCH_BLOCK(blk + BSTRIDE, ik, iv0, iv1);
-    while (blk < c1) {
+    // Two register sets used in turn: the next block's K/V loads are in
+    // flight while this block computes (the loop is unrolled by two so no
+    // registers are copied).
+    int kk, kv[4];
+    uint4 kA[SL], vA[4][VW], kB[SL], vB[4][VW];
+    CMC_KEYS(blk, kk, kv);
+    CMC_LOAD(blk, kk, kv, kA, vA);
+    CMC_KEYS(blk + BSTRIDE, kk, kv);
+#pragma unroll 1
+    while (true) {
         int nb = blk + BSTRIDE;
-        if (nb < c1) {
-            CMC_LOAD_BLOCK(nb, ik, iv0, iv1, kB, vB, rkb, rvb0, rvb1);
-            CMC_FETCH_BLOCK(nb + BSTRIDE, ik, iv0, iv1);
+        if (nb < r1) {
+            CMC_LOAD(nb, kk, kv, kB, vB);
+            CMC_KEYS(nb + BSTRIDE, kk, kv);
         }
-        CMC_COMPUTE_BLOCK(blk, kA, vA, rka, rva0, rva1);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch above this block's compute
+        CMC_COMPUTE(blk, kA, vA);
         blk = nb;
-        if (blk >= c1) break;
+        if (blk >= r1) break;
         nb = blk + BSTRIDE;
-        if (nb < c1) {
-            CMC_LOAD_BLOCK(nb, ik, iv0, iv1, kA, vA, rka, rva0, rva1);
-            CMC_FETCH_BLOCK(nb + BSTRIDE, ik, iv0, iv1);
+        if (nb < r1) {
+            CMC_LOAD(nb, kk, kv, kA, vA);
+            CMC_KEYS(nb + BSTRIDE, kk, kv);
         }
-        CMC_COMPUTE_BLOCK(blk, kB, vB, rkb, rvb0, rvb1);
+        __builtin_amdgcn_sched_barrier(0);
+        CMC_COMPUTE(blk, kB, vB);
         blk = nb;
+        if (blk >= r1) break;
     }
-#undef CMC_FETCH_BLOCK
-#undef CMC_LOAD_BLOCK
-#undef CMC_COMPUTE_BLOCK
+#undef CMC_KEYS
+#undef CMC_LOAD
+#undef CMC_COMPUTE
+}
+
+template <int DH, int G>
+__device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int c0, int c1, int cnt0,
+                                          int slot0, float *s_p, WaveState<G, DH / 16> &st) {
+    bf16x8 qa_hi[DH / 32], qa_lo[DH / 32];
+    load_q_operand<DH, G>(p, b, kvh, qa_hi, qa_lo);
+    const size_t head = (size_t)b * p.Hkv + kvh;
+    const int T_new = p.W > 0 ? p.T_new : 0;
+    const int n_old = p.W > 0 ? min(cnt0, p.W - T_new) : 0;
+    const int pool_end = p.k, ring_end = p.k + n_old;
+
+    // pool rows
+    {
+        const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
+        const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
+        const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
+        mfma_phase<DH, G, PoolRows, false>(c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qa_hi, qa_lo,
+                                           s_p, st);
+    }
+    if (p.W > 0) {
+        char *wk = static_cast<char *>(p.win_k) + head * (size_t)p.W * DH * 2;
+        char *wv = static_cast<char *>(p.win_v) + head * (size_t)p.W * DH * 2;
+        // surviving ring slots
+        const int s_old = (int)(((long long)cnt0 - n_old) % p.W);
+        const RingRows rr{pool_end, s_old, p.W};
+        mfma_phase<DH, G, RingRows, false>(max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr, nullptr,
+                                           qa_hi, qa_lo, s_p, st);
+        // rows appended in this call
+        if (T_new > 0) {
+            const NewRows nr{ring_end, slot0, p.W};
+            const char *nk = static_cast<const char *>(p.new_k) + head * (size_t)T_new * DH * 2;
+            const char *nv = static_cast<const char *>(p.new_v) + head * (size_t)T_new * DH * 2;
+            mfma_phase<DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st);
+        }
+    }
     // Wave totals: l over the 16 keys of one lane row (rows hold copies),
-    // acc over the 8 keys sharing a dim group.
+    // acc over the 4 keys sharing a dim group.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         st.l[g] = lane_reduce<OpSum, 1, 16>(st.l[g]);
 #pragma unroll
-        for (int i = 0; i < VD; ++i) st.acc[g][i] = lane_reduce<OpSum, 1, 8>(st.acc[g][i]);
+        for (int i = 0; i < DH / 16; ++i) st.acc[g][i] = lane_reduce<OpSum, 1, 4>(st.acc[g][i]);
     }
 }
 
@@ -446,7 +557,7 @@ __device__ __forceinline__ float combine_waves(const float (&sm)[kWaves][G], con
 
 template <typename T, int DH, int G, bool MF>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
-    constexpr int VEC = MF ? DH / 8 : Vec16<T>::N;   // output dims a lane accumulates
+    constexpr int VEC = MF ? DH / 16 : Vec16<T>::N;  // output dims a lane accumulates
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
@@ -466,16 +577,17 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
-        mfma_loop<DH, G>(p, rm, b, kvh, c0, c1, st);
+        __shared__ float s_pw[kWaves][16 * G];
+        mfma_loop<DH, G>(p, b, kvh, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
 
     // Lanes holding each dim group after the wave reduction.
-    constexpr int LPR = MF ? 8 : DH / Vec16<T>::N;         // lanes per dim group stride
-    const bool holder = MF ? ((lane & 7) == 0) : (lane < LPR);
-    const int dbase = MF ? (lane >> 3) * VEC : lane * VEC;
+    constexpr int LPR = MF ? 4 : DH / Vec16<T>::N;         // lanes per dim group stride
+    const bool holder = MF ? ((lane & 3) == 0) : (lane < LPR);
+    const int dbase = MF ? (lane >> 2) * VEC : lane * VEC;
 
     __shared__ float s_acc[kWaves][G][DH];
     __shared__ float s_m[kWaves][G], s_l[kWaves][G];
