@@ -65,6 +65,13 @@ def parse():
     ap.add_argument("--out", default=None, help="also append the JSON line to this file")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run plain device-to-device copies of MIB MiB (calibrates byte counters) and exit")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE output directories (decode kernel of "
+                         "--workload, and a --copy-probe run) into the per-launch HBM traffic record in "
+                         "profiles/decode_traffic.json; runs on the CPU")
+    ap.add_argument("--copy-probe-mib", type=int, default=1024, help="size the copy probe ran with")
+    ap.add_argument("--launch-reps", type=int, default=500,
+                    help="back-to-back decode launches timed for the roofline figure")
     return ap.parse_args()
 
 
@@ -192,8 +199,53 @@ def cpu_baseline(w, budget_s: float):
                        f"({per_step * 1e3:.2f} ms/step), extrapolated to one full pass")}
 
 
+def _counter_values(d, counter, kernel):
+    import csv
+    import glob
+    vals = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter and r["Kernel_Name"].startswith(kernel):
+                vals.append(float(r["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} samples for {kernel} under {d}")
+    return sorted(vals)[len(vals) // 2], len(vals)
+
+
+def pmc_summary(args):
+    """Per-launch HBM traffic of the decode kernel from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), each scaled by what the same counter reads
+    for a plain device copy of known size."""
+    from paper_2609_25537_amd import workloads as wl
+    w = wl.get(args.workload)
+    fd, wd, cfd, cwd = args.pmc_summary
+    known_kib = args.copy_probe_mib * 1024.0
+    copy_fetch, _ = _counter_values(cfd, "FETCH_SIZE", "__amd_rocclr_copyBuffer")
+    copy_write, _ = _counter_values(cwd, "WRITE_SIZE", "__amd_rocclr_copyBuffer")
+    fetch, nf = _counter_values(fd, "FETCH_SIZE", "decode_kernel")
+    write, nw = _counter_values(wd, "WRITE_SIZE", "decode_kernel")
+    fs, ws = known_kib / copy_fetch, known_kib / copy_write
+    fetch_b, write_b = fetch * fs * 1024, write * ws * 1024
+    rec = {"kernel_hash": decode_kernel_hash(), "bytes_per_launch": round(fetch_b + write_b),
+           "fetch_bytes": round(fetch_b), "write_bytes": round(write_b),
+           "fetch_kib_raw": fetch, "write_kib_raw": write, "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+           "dispatches": [nf, nw], "algorithmic_bytes": decode_bytes(w)}
+    data = {}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    data[w.name] = rec
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps({w.name: rec}))
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               "(each sequence shards independently across GPUs, see the design notes).", file=sys.stderr)
@@ -247,7 +299,7 @@ def main():
     tokens = w.B * steps * args.steps
     value = tokens / (ms * 1e-3)
 
-    t_launch = time_decode_launch(inp)
+    t_launch = time_decode_launch(inp, args.launch_reps)
     nbytes = decode_bytes(w)
     achieved = nbytes / t_launch / 1e9
     traffic = None

@@ -397,8 +397,10 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
-        mfma_phase<DH, G, PoolRows, false>(c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qa_hi, qa_lo,
-                                           s_p, st);
+        // The list always holds all k pool rows, so this phase's end does not
+        // depend on the ring count: its loads need not wait for that load.
+        mfma_phase<DH, G, PoolRows, false>(c0, min(c0 + p.chunk, pool_end), rows, kb, vb, nullptr, nullptr,
+                                           qa_hi, qa_lo, s_p, st);
     }
     if (p.W > 0) {
         char *wk = static_cast<char *>(p.win_k) + head * (size_t)p.W * DH * 2;

@@ -1,0 +1,68 @@
+"""Parity at the workloads' full sizes, in the launch configuration the
+benchmark times (one cmc_decode_step per step, the library's own split
+plan): selection bit-exact for every sequence, then all decode steps run on
+the GPU while the oracle advances its own ring every step and recomputes the
+attention at sampled steps -- the first ones, those around the ring wrap,
+and the last."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_25537_amd import cmc
+from paper_2609_25537_amd import workloads as wl
+from tests.gpu_util import DEV, max_abs, say, to_dev, to_host, tol_for
+from tests.inputs import accepted_attempts
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_full(orc, name, sample_extra=()):
+    w = wl.get(name)
+    say(f"{name}: generating inputs")
+    att = accepted_attempts(w, orc)
+    keys, qv = wl.sel_keys(w), wl.q_vecs(w, att)
+    ref_idx, _, gap = orc.select(keys, qv, w.k)
+    assert (gap >= w.gap_min).all()
+    say(f"{name}: select on GPU")
+    idx = cmc.cmc_select_cmes(to_dev(keys), to_dev(qv), w.k)
+    torch.cuda.synchronize()
+    assert (to_host(idx) == ref_idx).all(), "selected index sets differ"
+    del keys
+    pk, pv = wl.pool_kv(w)
+    wk, wv, cnt = wl.window_kv(w)
+    d_pk, d_pv, d_wk, d_wv, d_wc = map(to_dev, (pk, pv, wk, wv, cnt))
+    ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, DEV)
+    out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=DEV)
+    samples = sorted({0, 1, w.W - 1, w.W, w.W + 1, w.steps - 1, *sample_extra})
+    worst = 0.0
+    for t in range(w.steps):
+        nk, nv = wl.step_new_kv(w, t)
+        orc.window_append(wk, wv, cnt, nk, nv)
+        sampled = t in samples
+        q = wl.step_q(w, t) if sampled else None
+        d_q = to_dev(q) if sampled else to_dev(np.zeros((w.B, w.Hq, w.Dh), np.float32))
+        cmc.cmc_decode_step(d_q, d_pk, d_pv, idx, w.k, d_wk, d_wv, d_wc, to_dev(nk), to_dev(nv), w.scale,
+                            out=out, workspace=ws)
+        if sampled:
+            say(f"{name}: step {t}")
+            ref = orc.two_tier_decode(q, pk, pv, ref_idx, w.k, wk, wv, cnt, w.W, w.scale)
+            torch.cuda.synchronize()
+            err = max_abs(to_host(out), ref)
+            worst = max(worst, err)
+            assert err <= tol_for(w.kv_dtype), f"step {t}: max abs err {err:.3e}"
+    torch.cuda.synchronize()
+    assert (to_host(d_wc) == cnt).all()
+    assert (to_host(d_wk) == wk).all() and (to_host(d_wv) == wv).all(), "ring contents after all steps"
+    say(f"{name}: worst max-abs error {worst:.3e}")
+
+
+def test_full_llama3_8b_layer(orc):
+    _run_full(orc, "llama3_8b_layer", sample_extra=(2, 100, 1500))
+
+
+def test_full_mistral7b_batch64(orc):
+    _run_full(orc, "mistral7b_batch64")
+
+
+def test_full_long_wide_d256(orc):
+    _run_full(orc, "long_wide_d256")
