@@ -16,7 +16,9 @@ import os
 from typing import Optional
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIBRARY = os.path.join(_PKG, "libcmc.so")
+# CMC_LIBRARY may name another build of the same library (e.g. one built with
+# different tuning knobs); by default the in-tree build is used.
+LIBRARY = os.environ.get("CMC_LIBRARY") or os.path.join(_PKG, "libcmc.so")
 
 CMC_OK = 0
 CMC_ERR_INVALID_ARGUMENT = 1

@@ -40,6 +40,11 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 }  // namespace
 
+// Build-time tuning knob: the number of decode workgroups the split plan aims for.
+#ifndef CMC_DECODE_TARGET_WG
+#define CMC_DECODE_TARGET_WG 512
+#endif
+
 namespace cmc {
 
 // Key-axis split plan.  Aim for about kTargetWG workgroups: the decode kernel
@@ -49,7 +54,7 @@ namespace cmc {
 // The plan depends only on sizes, so the workspace query and the launch
 // always agree.
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
-    constexpr long long kTargetWG = 512;
+    constexpr long long kTargetWG = CMC_DECODE_TARGET_WG;
     constexpr long long kGranule = 64;
     constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
     DecodePlan pl;

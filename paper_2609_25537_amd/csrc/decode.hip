@@ -47,10 +47,15 @@ namespace cmc {
 
 namespace {
 
+// Build-time tuning knob: smallest query-group size that takes the MFMA path
+// (smaller groups use the VALU path).
+#ifndef CMC_MFMA_MIN_G
+#define CMC_MFMA_MIN_G 1
+#endif
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * kWave;
-constexpr int kMergeBatch = 8;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -576,6 +581,18 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     const int c1 = min(c0 + p.chunk, L);
     const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, slot0);
 
+    // Ring count: every workgroup of the sequence arrives on a counter as
+    // soon as it has read the count (the increment depends on the loaded
+    // value, so it is issued only after that load returns); the last of the
+    // Hkv * S arrivals writes the advanced count and re-arms the counter,
+    // after the main loop.  No data is published through the counter, so no
+    // fence is needed.
+    const bool bump = p.T_new > 0 && p.W > 0;
+    unsigned seq_prev = 0;
+    if (bump && threadIdx.x == 0)
+        seq_prev = __hip_atomic_fetch_add(&p.seq_counter[b], (unsigned)(cnt_raw != INT_MIN) /* == 1 */,
+                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
@@ -584,6 +601,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
+    }
+
+    if (bump && threadIdx.x == 0 && seq_prev == (unsigned)(p.Hkv * p.S - 1)) {
+        p.win_count[b] = cnt0 + p.T_new;
+        __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
     // Lanes holding each dim group after the wave reduction.
@@ -641,32 +663,55 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         }
         __syncthreads();
         if (!s_last) return;  // workgroup-uniform
-        // The last split merges all S partials in fixed split order: the
-        // (m, l) pairs are staged in LDS with one parallel load, the acc
-        // partials are fetched kMergeBatch at a time so their loads overlap.
+        // The last split merges all S partials in fixed split order.  Its
+        // first batch of acc partials (up to kMB splits per output) and all
+        // (m, l) pairs are requested together, so the merge costs one round
+        // trip when S <= kMB; the (m, l) pairs are staged in LDS.
+        constexpr int kPairs = (G * DH + kThreads - 1) / kThreads;  // outputs per thread
+        constexpr int kMB = kPairs >= 8 ? 4 : 32 / kPairs;
         const float *ml = p.part_ml + head * p.S * G * 2;
         const float *ac = p.part_acc + head * p.S * G * DH;
         float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= kWaves*G*DH floats (S <= 2*DH)
+        float a[kPairs][kMB];
+#pragma unroll
+        for (int pr = 0; pr < kPairs; ++pr) {
+            const int t = threadIdx.x + pr * kThreads;
+            const int g = t / DH, d = t % DH;
+#pragma unroll
+            for (int j = 0; j < kMB; ++j)
+                a[pr][j] = (t < G * DH && j < p.S) ? coherent_load(&ac[(j * G + g) * DH + d]) : 0.f;
+        }
         for (int t = threadIdx.x; t < p.S * G * 2; t += kThreads) s_ml[t] = coherent_load(&ml[t]);
         __syncthreads();
-        for (int t = threadIdx.x; t < G * DH; t += kThreads) {
+#pragma unroll
+        for (int pr = 0; pr < kPairs; ++pr) {
+            const int t = threadIdx.x + pr * kThreads;
+            if (t >= G * DH) continue;
             const int g = t / DH, d = t % DH;
             float M = -INFINITY;
             for (int q = 0; q < p.S; ++q) M = fmaxf(M, s_ml[(q * G + g) * 2]);
             float num = 0.f, den = 0.f;
             if (M != -INFINITY) {
-                for (int q0 = 0; q0 < p.S; q0 += kMergeBatch) {
-                    float a[kMergeBatch];
 #pragma unroll
-                    for (int j = 0; j < kMergeBatch; ++j)
-                        a[j] = q0 + j < p.S ? coherent_load(&ac[((q0 + j) * G + g) * DH + d]) : 0.f;
+                for (int j = 0; j < kMB; ++j) {
+                    if (j < p.S) {
+                        const float f = exp2f(s_ml[(j * G + g) * 2] - M);
+                        den = fmaf(f, s_ml[(j * G + g) * 2 + 1], den);
+                        num = fmaf(f, a[pr][j], num);
+                    }
+                }
+                for (int q0 = kMB; q0 < p.S; q0 += kMB) {
+                    float x[kMB];
 #pragma unroll
-                    for (int j = 0; j < kMergeBatch; ++j) {
+                    for (int j = 0; j < kMB; ++j)
+                        x[j] = q0 + j < p.S ? coherent_load(&ac[((q0 + j) * G + g) * DH + d]) : 0.f;
+#pragma unroll
+                    for (int j = 0; j < kMB; ++j) {
                         if (q0 + j < p.S) {
                             const int q = q0 + j;
                             const float f = exp2f(s_ml[(q * G + g) * 2] - M);
                             den = fmaf(f, s_ml[(q * G + g) * 2 + 1], den);
-                            num = fmaf(f, a[j], num);
+                            num = fmaf(f, x[j], num);
                         }
                     }
                 }
@@ -677,27 +722,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
             __hip_atomic_store(&p.pair_counter[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
-    // Advance the ring count once every workgroup of the sequence has read
-    // it: each (b, kv head) arrives once -- the single split, or the last of
-    // its S splits, every one of which read the count before arriving on the
-    // pair counter.  The single-split increment depends on the loaded count,
-    // so it cannot be issued before that load returns.  The last arrival
-    // writes the new count and re-arms the counter.
-    if (p.T_new > 0 && p.W > 0 && threadIdx.x == 0) {
-        const unsigned one = (unsigned)(cnt_raw != INT_MIN);  // == 1
-        const unsigned prev = __hip_atomic_fetch_add(&p.seq_counter[b], one, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-        if (prev == (unsigned)(p.Hkv - 1)) {
-            p.win_count[b] = cnt0 + p.T_new;
-            __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
 }
 
 template <typename T, int DH, int G>
 hipError_t launch3(const DecodeParams &p, hipStream_t stream) {
     dim3 grid(p.S, p.Hkv, p.B);
-    constexpr bool kMf = sizeof(T) == 2 && G <= 4;
+    constexpr bool kMf = sizeof(T) == 2 && G >= CMC_MFMA_MIN_G && G <= 4;
     decode_kernel<T, DH, G, kMf><<<grid, kThreads, 0, stream>>>(p);
     return hipGetLastError();
 }

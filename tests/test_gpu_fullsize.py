@@ -56,13 +56,16 @@ def _run_full(orc, name, sample_extra=()):
     say(f"{name}: worst max-abs error {worst:.3e}")
 
 
+@pytest.mark.timeout(300)
 def test_full_llama3_8b_layer(orc):
     _run_full(orc, "llama3_8b_layer", sample_extra=(2, 100, 1500))
 
 
+@pytest.mark.timeout(600)
 def test_full_mistral7b_batch64(orc):
     _run_full(orc, "mistral7b_batch64")
 
 
+@pytest.mark.timeout(900)
 def test_full_long_wide_d256(orc):
     _run_full(orc, "long_wide_d256")
