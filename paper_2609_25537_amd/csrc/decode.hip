@@ -147,13 +147,11 @@ __device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, i
 }
 
 // Orders this wave's LDS writes before its following LDS reads (and reads
-// before later writes): LDS operations of one wave execute in order, so only
-// the compiler must be kept from moving them across this point.
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
+// before later writes).  LDS operations of one wave execute in order, so only
+// the compiler must be kept from moving memory accesses across this point; a
+// fence would also wait for every outstanding global load, including the
+// next block's prefetch.
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("" ::: "memory"); }
 
 // 2^x with the hardware instruction alone (no denormal-result fix-up; a
 // softmax weight below 2^-126 contributes nothing at fp32 precision anyway).
@@ -264,32 +262,29 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     int blk = r0 + wave * 16;
     if (blk >= r1) return;  // wave-uniform
 
-#define CMC_KEYS(B0_, K_, V_)                                                   \
-    do {                                                                       \
-        K_ = (B0_) + r16 < r1 ? rows.key((B0_) + r16) : 0;                     \
-        _Pragma("unroll") for (int qq = 0; qq < 4; ++qq)                       \
-            V_[qq] = (B0_) + 4 * qq + kq < r1 ? rows.key((B0_) + 4 * qq + kq) : 0; \
+    // Rows past the phase end are clamped to its last row and loaded anyway
+    // (branch-free loads keep the compiler's wait counts exact, so a block's
+    // prefetch is never waited for early); their scores are masked to -inf,
+    // so they contribute p = 0.
+#define CMC_KEYS(B0_, K_, V_)                                               \
+    do {                                                                   \
+        K_ = rows.key(min((B0_) + r16, r1 - 1));                           \
+        _Pragma("unroll") for (int qq = 0; qq < 4; ++qq)                   \
+            V_[qq] = rows.key(min((B0_) + 4 * qq + kq, r1 - 1));           \
     } while (0)
 #define CMC_LOAD(B0_, K_, V_, KR_, VR_)                                                                \
     do {                                                                                             \
-        if ((B0_) + r16 < r1) {                                                                      \
-            const uint32_t o = (uint32_t)rows.slot((B0_) + r16, K_) * RB + koff;                    \
+        {                                                                                            \
+            const uint32_t o = (uint32_t)rows.slot(min((B0_) + r16, r1 - 1), K_) * RB + koff;       \
             _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = ld16(kbase + o + 64 * i);        \
-        } else {                                                                                     \
-            _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = make_uint4(0, 0, 0, 0);          \
         }                                                                                            \
         _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
-            const int vrow = (B0_) + 4 * qq + kq;                                                    \
-            if (vrow < r1) {                                                                         \
-                const uint32_t o = (uint32_t)rows.slot(vrow, V_[qq]) * RB + voff;                   \
-                if constexpr (VB >= 16) {                                                            \
-                    _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = ld16(vbase + o + 16 * j); \
-                } else {                                                                             \
-                    const uint2 t = *reinterpret_cast<const uint2 *>(vbase + o);                     \
-                    VR_[qq][0] = make_uint4(t.x, t.y, 0, 0);                                         \
-                }                                                                                    \
+            const uint32_t o = (uint32_t)rows.slot(min((B0_) + 4 * qq + kq, r1 - 1), V_[qq]) * RB + voff; \
+            if constexpr (VB >= 16) {                                                                \
+                _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = ld16(vbase + o + 16 * j);  \
             } else {                                                                                 \
-                _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = make_uint4(0, 0, 0, 0);  \
+                const uint2 t = *reinterpret_cast<const uint2 *>(vbase + o);                         \
+                VR_[qq][0] = make_uint4(t.x, t.y, 0, 0);                                             \
             }                                                                                        \
         }                                                                                            \
     } while (0)
@@ -355,28 +350,33 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 
     // Two register sets used in turn: the next block's K/V loads are in
     // flight while this block computes (the loop is unrolled by two so no
-    // registers are copied).
-    int kk, kv[4];
+    // registers are copied).  Index-list entries are fetched two blocks
+    // ahead and issued before the next block's K/V loads: loads retire in
+    // issue order, so waiting for the entries then never waits for the
+    // prefetched K/V rows.
+    int kc, kvc[4], kn, kvn[4];
     uint4 kA[SL], vA[4][VW], kB[SL], vB[4][VW];
-    CMC_KEYS(blk, kk, kv);
-    CMC_LOAD(blk, kk, kv, kA, vA);
-    CMC_KEYS(blk + BSTRIDE, kk, kv);
+    CMC_KEYS(blk, kc, kvc);
+    CMC_LOAD(blk, kc, kvc, kA, vA);
+    CMC_KEYS(blk + BSTRIDE, kc, kvc);
 #pragma unroll 1
     while (true) {
         int nb = blk + BSTRIDE;
-        if (nb < r1) {
-            CMC_LOAD(nb, kk, kv, kB, vB);
-            CMC_KEYS(nb + BSTRIDE, kk, kv);
-        }
+        CMC_KEYS(nb + BSTRIDE, kn, kvn);
+        CMC_LOAD(nb, kc, kvc, kB, vB);
+        kc = kn;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) kvc[i] = kvn[i];
         __builtin_amdgcn_sched_barrier(0);  // keep the prefetch above this block's compute
         CMC_COMPUTE(blk, kA, vA);
         blk = nb;
         if (blk >= r1) break;
         nb = blk + BSTRIDE;
-        if (nb < r1) {
-            CMC_LOAD(nb, kk, kv, kA, vA);
-            CMC_KEYS(nb + BSTRIDE, kk, kv);
-        }
+        CMC_KEYS(nb + BSTRIDE, kn, kvn);
+        CMC_LOAD(nb, kc, kvc, kA, vA);
+        kc = kn;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) kvc[i] = kvn[i];
         __builtin_amdgcn_sched_barrier(0);
         CMC_COMPUTE(blk, kB, vB);
         blk = nb;
