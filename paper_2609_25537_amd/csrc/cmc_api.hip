@@ -44,6 +44,10 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 #ifndef CMC_DECODE_TARGET_WG
 #define CMC_DECODE_TARGET_WG 512
 #endif
+// Build-time tuning knob: smallest number of keys per split.
+#ifndef CMC_DECODE_GRANULE
+#define CMC_DECODE_GRANULE 64
+#endif
 
 namespace cmc {
 
@@ -55,7 +59,7 @@ namespace cmc {
 // always agree.
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
     constexpr long long kTargetWG = CMC_DECODE_TARGET_WG;
-    constexpr long long kGranule = 64;
+    constexpr long long kGranule = CMC_DECODE_GRANULE;
     constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
     DecodePlan pl;
     const long long L = (long long)k + W;

@@ -36,7 +36,7 @@
 // to arrive merges the S partials in fixed split order (so results are
 // bit-identical run to run), writes the output and re-arms the counter.
 // Publication uses agent-coherent relaxed atomics plus a store-completion
-// wait instead of device-scope fences (see coherent_store).  A head whose key
+// wait instead of device-scope fences (see coherent_store2).  A head whose key
 // list is empty gets zeros.
 #include <limits.h>
 
@@ -534,11 +534,15 @@ __device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T>
 // reader issues its loads only after the arrival count has returned.  An
 // agent-scope fence would instead write back and invalidate the whole L2 of
 // the XCD for every workgroup, which costs microseconds each.
-__device__ __forceinline__ void coherent_store(float *p, float v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Two adjacent floats (8-byte aligned) as one 64-bit coherent access.
+__device__ __forceinline__ void coherent_store2(float *p, float a, float b) {
+    const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+    __hip_atomic_store(reinterpret_cast<uint64_t *>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float coherent_load(const float *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ float2 coherent_load2(const float *p) {
+    const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t *>(p), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+    return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
 
 // Combine the four waves' (m, l, acc) of head g, dim d; returns the joint max.
@@ -641,18 +645,17 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
             outp[t] = den > 0.f ? num / den : 0.f;
         }
     } else {
-        // Publish this split's partial with agent-coherent stores, wait for
-        // them to complete, then arrive on the (b, kv head) counter.
+        // Publish this split's partial with agent-coherent 64-bit stores (two
+        // dims per thread), wait for them to complete, then arrive on the
+        // (b, kv head) counter.
         const size_t part = (head * p.S + s) * G;
-        for (int t = threadIdx.x; t < G * DH; t += kThreads) {
-            const int g = t / DH, d = t % DH;
-            float num, den;
-            const float M = combine_waves<G, DH>(s_m, s_l, s_acc, g, d, num, den);
-            coherent_store(&p.part_acc[(part + g) * DH + d], num);
-            if (d == 0) {
-                coherent_store(&p.part_ml[(part + g) * 2 + 0], M);
-                coherent_store(&p.part_ml[(part + g) * 2 + 1], den);
-            }
+        for (int t = threadIdx.x; t < G * DH / 2; t += kThreads) {
+            const int g = (2 * t) / DH, d = (2 * t) % DH;
+            float n0, n1, den;
+            const float M = combine_waves<G, DH>(s_m, s_l, s_acc, g, d, n0, den);
+            combine_waves<G, DH>(s_m, s_l, s_acc, g, d + 1, n1, den);
+            coherent_store2(&p.part_acc[(part + g) * DH + d], n0, n1);
+            if (d == 0) coherent_store2(&p.part_ml[(part + g) * 2], M, den);
         }
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
@@ -664,59 +667,68 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         __syncthreads();
         if (!s_last) return;  // workgroup-uniform
         // The last split merges all S partials in fixed split order.  Its
-        // first batch of acc partials (up to kMB splits per output) and all
+        // first batch of acc partials (up to kMB splits per dim pair) and all
         // (m, l) pairs are requested together, so the merge costs one round
         // trip when S <= kMB; the (m, l) pairs are staged in LDS.
-        constexpr int kPairs = (G * DH + kThreads - 1) / kThreads;  // outputs per thread
-        constexpr int kMB = kPairs >= 8 ? 4 : 32 / kPairs;
+        constexpr int kPairs = (G * DH / 2 + kThreads - 1) / kThreads;  // dim pairs per thread
+        constexpr int kMB = kPairs >= 4 ? 8 : 16;
         const float *ml = p.part_ml + head * p.S * G * 2;
         const float *ac = p.part_acc + head * p.S * G * DH;
         float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= kWaves*G*DH floats (S <= 2*DH)
-        float a[kPairs][kMB];
+        float2 a[kPairs][kMB];
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
             const int t = threadIdx.x + pr * kThreads;
-            const int g = t / DH, d = t % DH;
+            const int g = (2 * t) / DH, d = (2 * t) % DH;
 #pragma unroll
             for (int j = 0; j < kMB; ++j)
-                a[pr][j] = (t < G * DH && j < p.S) ? coherent_load(&ac[(j * G + g) * DH + d]) : 0.f;
+                a[pr][j] = (t < G * DH / 2 && j < p.S) ? coherent_load2(&ac[(j * G + g) * DH + d])
+                                                       : make_float2(0.f, 0.f);
         }
-        for (int t = threadIdx.x; t < p.S * G * 2; t += kThreads) s_ml[t] = coherent_load(&ml[t]);
+        for (int t = threadIdx.x; t < p.S * G; t += kThreads) {
+            const float2 v = coherent_load2(&ml[2 * t]);
+            s_ml[2 * t] = v.x;
+            s_ml[2 * t + 1] = v.y;
+        }
         __syncthreads();
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
             const int t = threadIdx.x + pr * kThreads;
-            if (t >= G * DH) continue;
-            const int g = t / DH, d = t % DH;
+            if (t >= G * DH / 2) continue;
+            const int g = (2 * t) / DH, d = (2 * t) % DH;
             float M = -INFINITY;
             for (int q = 0; q < p.S; ++q) M = fmaxf(M, s_ml[(q * G + g) * 2]);
-            float num = 0.f, den = 0.f;
+            float n0 = 0.f, n1 = 0.f, den = 0.f;
             if (M != -INFINITY) {
 #pragma unroll
                 for (int j = 0; j < kMB; ++j) {
                     if (j < p.S) {
                         const float f = exp2f(s_ml[(j * G + g) * 2] - M);
                         den = fmaf(f, s_ml[(j * G + g) * 2 + 1], den);
-                        num = fmaf(f, a[pr][j], num);
+                        n0 = fmaf(f, a[pr][j].x, n0);
+                        n1 = fmaf(f, a[pr][j].y, n1);
                     }
                 }
                 for (int q0 = kMB; q0 < p.S; q0 += kMB) {
-                    float x[kMB];
+                    float2 x[kMB];
 #pragma unroll
                     for (int j = 0; j < kMB; ++j)
-                        x[j] = q0 + j < p.S ? coherent_load(&ac[((q0 + j) * G + g) * DH + d]) : 0.f;
+                        x[j] = q0 + j < p.S ? coherent_load2(&ac[((q0 + j) * G + g) * DH + d])
+                                            : make_float2(0.f, 0.f);
 #pragma unroll
                     for (int j = 0; j < kMB; ++j) {
                         if (q0 + j < p.S) {
                             const int q = q0 + j;
                             const float f = exp2f(s_ml[(q * G + g) * 2] - M);
                             den = fmaf(f, s_ml[(q * G + g) * 2 + 1], den);
-                            num = fmaf(f, x[j], num);
+                            n0 = fmaf(f, x[j].x, n0);
+                            n1 = fmaf(f, x[j].y, n1);
                         }
                     }
                 }
             }
-            outp[t] = den > 0.f ? num / den : 0.f;
+            const float inv = den > 0.f ? 1.f / den : 0.f;
+            *reinterpret_cast<float2 *>(&outp[g * DH + d]) = make_float2(n0 * inv, n1 * inv);
         }
         if (threadIdx.x == 0)
             __hip_atomic_store(&p.pair_counter[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
