@@ -52,6 +52,10 @@ namespace {
 #ifndef CMC_MFMA_MIN_G
 #define CMC_MFMA_MIN_G 1
 #endif
+// Build-time tuning knob: widest head that double-buffers its K/V rows.
+#ifndef CMC_DOUBLE_BUFFER_MAX_DH
+#define CMC_DOUBLE_BUFFER_MAX_DH 128
+#endif
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kWaves = 4;
@@ -254,6 +258,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
     constexpr int VW = VB >= 16 ? VB / 16 : 1; // 16-byte words (or one 8-byte word)
     constexpr int BSTRIDE = kWaves * 16;
+    constexpr bool kDoubleBuffer = DH <= CMC_DOUBLE_BUFFER_MAX_DH;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r16 = lane & 15, q4 = lane >> 4, kq = lane & 3, dg = lane >> 2;
     const uint32_t koff = 16u * q4;        // + 64 * i for slice i
@@ -355,6 +360,19 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     // issue order, so waiting for the entries then never waits for the
     // prefetched K/V rows.
     int kc, kvc[4], kn, kvn[4];
+    if constexpr (!kDoubleBuffer) {
+        // Wide heads: one register set (two would cost an extra wave per SIMD
+        // of occupancy); the index entries are still fetched a block ahead.
+        uint4 kr[SL], vr[4][VW];
+        CMC_KEYS(blk, kc, kvc);
+#pragma unroll 1
+        for (; blk < r1; blk += BSTRIDE) {
+            CMC_LOAD(blk, kc, kvc, kr, vr);
+            CMC_KEYS(blk + BSTRIDE, kc, kvc);
+            CMC_COMPUTE(blk, kr, vr);
+        }
+        return;
+    }
     uint4 kA[SL], vA[4][VW], kB[SL], vB[4][VW];
     CMC_KEYS(blk, kc, kvc);
     CMC_LOAD(blk, kc, kvc, kA, vA);
