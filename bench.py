@@ -72,6 +72,8 @@ def parse():
     ap.add_argument("--copy-probe-mib", type=int, default=1024, help="size the copy probe ran with")
     ap.add_argument("--launch-reps", type=int, default=500,
                     help="back-to-back decode launches timed for the roofline figure")
+    ap.add_argument("--baseline-steps", type=int, default=4,
+                    help="stack workloads: timed decode steps of the uncompressed-cache baseline (0: skip it)")
     return ap.parse_args()
 
 
@@ -241,6 +243,161 @@ def pmc_summary(args):
     print(json.dumps({w.name: rec}))
 
 
+class StackLayer:
+    """Device-resident inputs of one decoder layer of a stack workload."""
+
+    def __init__(self, w, layer, P, dev):
+        import torch
+        from paper_2609_25537_amd import workloads as wl
+        bf = torch.bfloat16 if w.kv_dtype == "bf16" else torch.float32
+        dn = lambda role, ids, shape, dt=bf: wl.device_normal(w.seed, role, ids, shape, w.kv_std, dev, dt)
+        self.pk = dn("cme_k", (layer,), (w.B, w.Hkv, w.N, w.Dh))
+        self.pv = dn("cme_v", (layer,), (w.B, w.Hkv, w.N, w.Dh))
+        self.wk = dn("win_k", (layer,), (w.B, w.Hkv, w.W, w.Dh))
+        self.wv = dn("win_v", (layer,), (w.B, w.Hkv, w.W, w.Dh))
+        self.wc = torch.full((w.B,), w.W, dtype=torch.int32, device=dev)
+        self.q = [dn("q", (layer, t), (w.B, w.Hq, w.Dh), torch.float32) for t in range(P)]
+        self.nk = [dn("new_k", (layer, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]
+        self.nv = [dn("new_v", (layer, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]
+
+
+def run_stack(args, w, dev):
+    """A decoder stack of w.layers layers sharing one index list: one pass is
+    the selection plus w.steps decode steps, each running the two-tier decode
+    of every layer.  Then the same kernel over an uncompressed cache of
+    w.full_ctx prefilled tokens (k = 0, a ring that never wraps), timed for
+    a few steps.  Inputs are drawn on the device (see workloads)."""
+    import torch
+    from paper_2609_25537_amd import cmc
+    from paper_2609_25537_amd import workloads as wl
+    steps = args.decode_steps or w.steps
+    P = min(steps, args.step_pool or 16)
+    gb = 1e9
+    torch.cuda.reset_peak_memory_stats()
+    keys = wl.device_normal(w.seed, "sel_keys", (0,), (w.B, w.N, w.D), 1.0, dev, torch.float32)
+    qv = wl.device_normal(w.seed, "q_vec", (0,), (w.B, w.D), 1.0, dev, torch.float32)
+    idx = torch.empty((w.B, w.k), dtype=torch.int32, device=dev)
+    sel_ws = torch.empty(max(1, cmc.cmc_select_workspace_bytes(w.B, w.N)), dtype=torch.uint8, device=dev)
+    layers = [StackLayer(w, l, P, dev) for l in range(w.layers)]
+    out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=dev)
+    ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, dev)
+    torch.cuda.synchronize()
+
+    def step_fn(j):
+        def f():
+            for Ly in layers:
+                cmc.cmc_decode_step(Ly.q[j], Ly.pk, Ly.pv, idx, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
+                                    w.scale, out=out, workspace=ws)
+        return f
+
+    cmc.cmc_select_cmes(keys, qv, w.k, idx_out=idx, workspace=sel_ws)
+    graphs = [capture(step_fn(j)) for j in range(P)]
+
+    def one_pass():
+        cmc.cmc_select_cmes(keys, qv, w.k, idx_out=idx, workspace=sel_ws)
+        for t in range(steps):
+            graphs[t % P].replay()
+
+    for _ in range(args.warmup):
+        one_pass()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(args.steps):
+        one_pass()
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    peak_two_tier = torch.cuda.max_memory_allocated() / gb
+
+    # Average duration of one layer's decode launch (graph replay).  The
+    # launches rotate over the layers, as a decode step does: one layer's
+    # K/V (about 200 MB) fits in the 256 MB last-level cache, so repeating a
+    # single layer would time cache hits rather than HBM.
+    def launches():
+        for r in range(args.launch_reps):
+            Ly, j = layers[r % len(layers)], (r // len(layers)) % P
+            cmc.cmc_decode_step(Ly.q[j], Ly.pk, Ly.pv, idx, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
+                                w.scale, out=out, workspace=ws)
+    g = capture(launches)
+    g.replay()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.synchronize()
+    a.record(st)
+    g.replay()
+    b.record(st)
+    b.synchronize()
+    t_launch = a.elapsed_time(b) / args.launch_reps * 1e-3
+
+    del graphs, g, layers, keys, qv, sel_ws, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    res = {"ms": ms, "steps": steps, "P": P, "t_launch": t_launch, "baseline": None,
+           "footprint_GB": {"two_tier_peak_allocated": round(peak_two_tier, 2)}}
+    if args.baseline_steps <= 0:
+        return res
+
+    # Uncompressed baseline: the same decode kernel over every cached token.
+    Wb = w.full_ctx + steps
+    bf = torch.bfloat16 if w.kv_dtype == "bf16" else torch.float32
+    base = []
+    for l in range(w.layers):
+        bk = torch.empty((w.B, w.Hkv, Wb, w.Dh), dtype=bf, device=dev)
+        bv = torch.empty_like(bk)
+        bk[:, :, :w.full_ctx] = wl.device_normal(w.seed, "full_k", (l,), (w.B, w.Hkv, w.full_ctx, w.Dh),
+                                                 w.kv_std, dev, bf)
+        bv[:, :, :w.full_ctx] = wl.device_normal(w.seed, "full_v", (l,), (w.B, w.Hkv, w.full_ctx, w.Dh),
+                                                 w.kv_std, dev, bf)
+        q = wl.device_normal(w.seed, "q", (l, 0), (w.B, w.Hq, w.Dh), w.kv_std, dev, torch.float32)
+        nk = wl.device_normal(w.seed, "new_k", (l, 0), (w.B, w.Hkv, 1, w.Dh), w.kv_std, dev, bf)
+        nv = wl.device_normal(w.seed, "new_v", (l, 0), (w.B, w.Hkv, 1, w.Dh), w.kv_std, dev, bf)
+        base.append((bk, bv, torch.full((w.B,), w.full_ctx, dtype=torch.int32, device=dev), q, nk, nv))
+    pool0 = torch.zeros((w.B, w.Hkv, 1, w.Dh), dtype=bf, device=dev)
+    bws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, 0, Wb, dev)
+    torch.cuda.synchronize()
+
+    def base_step():
+        for bk, bv, bc, q, nk, nv in base:
+            cmc.cmc_decode_step(q, pool0, pool0, None, 0, bk, bv, bc, nk, nv, w.scale, out=out, workspace=bws)
+
+    base_step()
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(args.baseline_steps):
+        base_step()
+    e1.record(st)
+    torch.cuda.synchronize()
+    base_ms = e0.elapsed_time(e1) / args.baseline_steps
+    peak_base = torch.cuda.max_memory_allocated() / gb
+    # After the warm-up step the timed steps attend full_ctx + 2 ... keys; the
+    # key count grows by one per step, so scale the measured per-step time by
+    # the mean key count of a whole pass (full_ctx + 1 ... full_ctx + steps).
+    keys_t = w.full_ctx + 2 + (args.baseline_steps - 1) / 2
+    base_pass_ms = base_ms * steps * ((w.full_ctx + (steps + 1) / 2) / keys_t)
+    del base, pool0, bws
+    torch.cuda.empty_cache()
+
+    kv_row = w.Dh * w.kv_bytes * 2
+    analytic = {
+        "two_tier_compact": w.layers * w.B * w.Hkv * (w.k + w.W) * kv_row / gb,
+        "two_tier_resident_pool": w.layers * w.B * w.Hkv * (w.N + w.W) * kv_row / gb,
+        "baseline_first_step": w.layers * w.B * w.Hkv * (w.full_ctx + 1) * kv_row / gb,
+        "baseline_last_step": w.layers * w.B * w.Hkv * (w.full_ctx + steps) * kv_row / gb,
+    }
+    return {
+        "ms": ms, "steps": steps, "P": P, "t_launch": t_launch,
+        "baseline": {"ms_per_step": round(base_ms, 3), "steps_timed": args.baseline_steps,
+                     "mean_keys_per_sequence_timed": keys_t,
+                     "extrapolated_pass_ms": round(base_pass_ms, 1),
+                     "tokens_per_s": round(w.B * steps / (base_pass_ms * 1e-3), 1)},
+        "footprint_GB": {"two_tier_peak_allocated": round(peak_two_tier, 2),
+                         "baseline_peak_allocated": round(peak_base, 2),
+                         **{k: round(v, 2) for k, v in analytic.items()}},
+    }
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -275,7 +432,7 @@ def main():
     dev = torch.device("cuda:0")
     w = wl.get(args.workload)
     if w.layers != 1:
-        raise SystemExit(f"workload {w.name} has {w.layers} layers; use bench_stack mode (not in this build yet)")
+        return main_stack(args, w, dev)
     steps = args.decode_steps or w.steps
     pool = args.step_pool or (steps if w.B * w.Hq * w.Dh * 4 <= (1 << 20) else 64)
     inp = Inputs(w, steps, pool, dev)
@@ -343,6 +500,38 @@ def main():
                    "kv_dtype": w.kv_dtype, "step_input_sets": inp.P, "graph": bool(graph)},
         "roofline": roofline,
         "cpu_baseline": cpu,
+    }
+    txt = json.dumps(line)
+    print(txt, flush=True)
+    if args.out:
+        with open(args.out, "a") as f:
+            f.write(txt + "\n")
+
+
+def main_stack(args, w, dev):
+    r = run_stack(args, w, dev)
+    steps = r["steps"]
+    ms_per_pass = r["ms"] / args.steps
+    value = w.B * steps * args.steps / (r["ms"] * 1e-3)
+    nbytes = decode_bytes(w)
+    achieved = nbytes / r["t_launch"] / 1e9
+    line = {
+        "metric": "two-tier decode tokens/s and achieved HBM GB/s (% of MI355X peak)",
+        "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_pass, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.kv_dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Dh": w.Dh, "N": w.N, "D": w.D,
+                   "k": w.k, "W": w.W, "decode_steps": steps, "layers": w.layers, "kv_dtype": w.kv_dtype,
+                   "step_input_sets": r["P"], "graph": True, "full_ctx": w.full_ctx},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "decode_kernel (cmc_decode_step), one layer, layers rotating", "bytes_per_launch": nbytes,
+                     "launch_us": round(r["t_launch"] * 1e6, 3)},
+        "uncompressed_baseline": r["baseline"],
+        "speedup_vs_uncompressed": (round(r["baseline"]["extrapolated_pass_ms"] / ms_per_pass, 2)
+                                    if r["baseline"] else None),
+        "footprint_GB": r["footprint_GB"],
+        "cpu_baseline": None,
     }
     txt = json.dumps(line)
     print(txt, flush=True)

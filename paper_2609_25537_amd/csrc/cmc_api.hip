@@ -40,36 +40,54 @@ size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 }  // namespace
 
-// Build-time tuning knob: the number of decode workgroups the split plan aims for.
+// Build-time tuning knob: the number of 4-wave decode workgroups the split
+// plan aims for.
 #ifndef CMC_DECODE_TARGET_WG
 #define CMC_DECODE_TARGET_WG 512
 #endif
-// Build-time tuning knob: smallest number of keys per split.
+// Build-time tuning knob: smallest number of keys per split of 4-wave
+// workgroups (one 16-key block per wave).
 #ifndef CMC_DECODE_GRANULE
 #define CMC_DECODE_GRANULE 64
+#endif
+// Build-time tuning knob: fewest (sequence, kv head) pairs that take one
+// 8-wave workgroup each (up to 256 pairs).
+#ifndef CMC_DECODE_WIDE_MIN_PAIRS
+#define CMC_DECODE_WIDE_MIN_PAIRS 192
 #endif
 
 namespace cmc {
 
-// Key-axis split plan.  Aim for about kTargetWG workgroups: the decode kernel
-// keeps two workgroups resident per CU, so 512 fill the 256 CUs in one round;
-// a (sequence, kv head) pair is split only when there are fewer pairs than
-// that, and never below kGranule keys (4 waves x 16-key blocks) per split.
+// Key-axis split plan.  The decode kernel keeps eight waves resident per CU
+// (two per SIMD), so about 2048 waves fill the 256 CUs in one round.
+//   - With 192..256 (sequence, kv head) pairs, each pair gets one 8-wave
+//     workgroup (S = 1): one round and no cross-workgroup merge.
+//   - Otherwise workgroups have 4 waves, two resident per CU, and the plan
+//     aims for about kTargetWG of them: a pair is split only when there are
+//     fewer pairs than that, never below kGranule keys per split.
 // The plan depends only on sizes, so the workspace query and the launch
 // always agree.
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
     constexpr long long kTargetWG = CMC_DECODE_TARGET_WG;
     constexpr long long kGranule = CMC_DECODE_GRANULE;
+    constexpr long long kWideMinPairs = CMC_DECODE_WIDE_MIN_PAIRS;
     constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
     DecodePlan pl;
     const long long L = (long long)k + W;
     const long long pairs = (long long)B * Hkv;
     if (L <= 0 || pairs <= 0) return pl;
-    const long long s_target = std::max(1LL, (kTargetWG + pairs - 1) / pairs);
-    long long chunk = (L + s_target - 1) / s_target;
-    chunk = std::max(chunk, (L + kMaxSplits - 1) / kMaxSplits);
-    chunk = ((chunk + kGranule - 1) / kGranule) * kGranule;
-    const long long S = (L + chunk - 1) / chunk;
+    long long S, chunk;
+    if (pairs >= kWideMinPairs && pairs <= 256 && decode_waves_ok(8, Hq / Hkv, Dh)) {
+        pl.waves = 8;
+        S = 1;
+        chunk = L;
+    } else {
+        const long long s_target = std::max(1LL, (kTargetWG + pairs - 1) / pairs);
+        chunk = (L + s_target - 1) / s_target;
+        chunk = std::max(chunk, (L + kMaxSplits - 1) / kMaxSplits);
+        chunk = ((chunk + kGranule - 1) / kGranule) * kGranule;
+        S = (L + chunk - 1) / chunk;
+    }
     const int G = Hq / Hkv;
     pl.S = (int)S;
     pl.chunk = (int)chunk;
@@ -238,6 +256,7 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     p.T_new = T_new;
     p.S = pl.S;
     p.chunk = pl.chunk;
+    p.waves = pl.waves;
     p.qscale = cmc::decode_qscale(scale);
     hipError_t e = cmc::launch_two_tier_decode(p, kv_dtype == CMC_BF16, G, Dh, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "decode launch");

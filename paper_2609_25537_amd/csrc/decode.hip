@@ -3,7 +3,7 @@
 // [Tier-2 ring slots 0..min(count,W)-1], optionally fused with the ring append
 // of this step's new rows, in ONE launch.
 //
-// Grid (S, Hkv, B), 256 threads (4 waves).  Workgroup s owns keys
+// Grid (S, Hkv, B), 4 or 8 waves per workgroup (chosen by the split plan).  Workgroup s owns keys
 // [s*chunk, (s+1)*chunk) of sequence b's virtual key list and all G = Hq/Hkv
 // query heads sharing kv head h, so each K/V byte is read from HBM once per
 // step and reused G times on chip.
@@ -28,7 +28,7 @@
 //   VALU (fp32 K/V, or G = 8): 16-byte lane loads, LPR lanes per row, dot
 //     products reduced by a DPP butterfly.
 // Both keep an online softmax per wave (running max in log2 units, q
-// pre-scaled by scale*log2 e), then combine the four waves through LDS.
+// pre-scaled by scale*log2 e), then combine the waves through LDS.
 //
 // Split merge, inside the same launch: with S == 1 the workgroup writes the
 // output directly.  With S > 1 every workgroup publishes (m, l, acc[Dh]) per
@@ -58,8 +58,6 @@ namespace {
 #endif
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * kWave;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -249,7 +247,7 @@ __device__ __forceinline__ void load_q_operand(const DecodeParams &p, int b, int
 // the V layout through a 16 x G slot of LDS private to the wave.  Keys
 // (index-list entries) are fetched one block ahead of the K/V rows, and the
 // K/V rows one block ahead of their use.
-template <int DH, int G, class Rows, bool RING_WRITE>
+template <int NW, int DH, int G, class Rows, bool RING_WRITE>
 __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, const char *kbase, const char *vbase,
                                            char *ringK, char *ringV, const bf16x8 (&qa_hi)[DH / 32],
                                            const bf16x8 (&qa_lo)[DH / 32], float *s_p,
@@ -257,7 +255,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     constexpr int SL = DH / 32, VD = DH / 16, RB = DH * 2;
     constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
     constexpr int VW = VB >= 16 ? VB / 16 : 1; // 16-byte words (or one 8-byte word)
-    constexpr int BSTRIDE = kWaves * 16;
+    constexpr int BSTRIDE = NW * 16;
     constexpr bool kDoubleBuffer = DH <= CMC_DOUBLE_BUFFER_MAX_DH;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r16 = lane & 15, q4 = lane >> 4, kq = lane & 3, dg = lane >> 2;
@@ -405,7 +403,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 #undef CMC_COMPUTE
 }
 
-template <int DH, int G>
+template <int NW, int DH, int G>
 __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int c0, int c1, int cnt0,
                                           int slot0, float *s_p, WaveState<G, DH / 16> &st) {
     bf16x8 qa_hi[DH / 32], qa_lo[DH / 32];
@@ -422,7 +420,7 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
         // The list always holds all k pool rows, so this phase's end does not
         // depend on the ring count: its loads need not wait for that load.
-        mfma_phase<DH, G, PoolRows, false>(c0, min(c0 + p.chunk, pool_end), rows, kb, vb, nullptr, nullptr,
+        mfma_phase<NW, DH, G, PoolRows, false>(c0, min(c0 + p.chunk, pool_end), rows, kb, vb, nullptr, nullptr,
                                            qa_hi, qa_lo, s_p, st);
     }
     if (p.W > 0) {
@@ -431,14 +429,14 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         // surviving ring slots
         const int s_old = (int)(((long long)cnt0 - n_old) % p.W);
         const RingRows rr{pool_end, s_old, p.W};
-        mfma_phase<DH, G, RingRows, false>(max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr, nullptr,
+        mfma_phase<NW, DH, G, RingRows, false>(max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr, nullptr,
                                            qa_hi, qa_lo, s_p, st);
         // rows appended in this call
         if (T_new > 0) {
             const NewRows nr{ring_end, slot0, p.W};
             const char *nk = static_cast<const char *>(p.new_k) + head * (size_t)T_new * DH * 2;
             const char *nv = static_cast<const char *>(p.new_v) + head * (size_t)T_new * DH * 2;
-            mfma_phase<DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st);
+            mfma_phase<NW, DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st);
         }
     }
     // Wave totals: l over the 16 keys of one lane row (rows hold copies),
@@ -453,7 +451,7 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
 
 // --------------------------------------------------------------- VALU loop
 
-template <typename T, int DH, int G, int U>
+template <int NW, typename T, int DH, int G, int U>
 __device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T> &rm, int b, int kvh, int c0,
                                           int c1, WaveState<G, Vec16<T>::N> &st) {
     constexpr int VEC = Vec16<T>::N;
@@ -478,7 +476,7 @@ __device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T>
         }
     }
 
-    constexpr int STRIDE = kWaves * RPW;
+    constexpr int STRIDE = NW * RPW;
     for (int r0 = c0 + wave * RPW; r0 < c1; r0 += STRIDE * U) {
         uint4 kr[U], vr[U];
         bool ok[U];
@@ -563,19 +561,19 @@ __device__ __forceinline__ float2 coherent_load2(const float *p) {
     return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
 
-// Combine the four waves' (m, l, acc) of head g, dim d; returns the joint max.
-template <int G, int DH>
-__device__ __forceinline__ float combine_waves(const float (&sm)[kWaves][G], const float (&sl)[kWaves][G],
-                                               const float (&sa)[kWaves][G][DH], int g, int d, float &num,
+// Combine the waves' (m, l, acc) of head g, dim d; returns the joint max.
+template <int NW, int G, int DH>
+__device__ __forceinline__ float combine_waves(const float (&sm)[NW][G], const float (&sl)[NW][G],
+                                               const float (&sa)[NW][G][DH], int g, int d, float &num,
                                                float &den) {
     float M = sm[0][g];
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm[w][g]);
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, sm[w][g]);
     num = 0.f;
     den = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
+        for (int w = 0; w < NW; ++w) {
             const float f = exp2f(sm[w][g] - M);
             num = fmaf(f, sa[w][g][d], num);
             den = fmaf(f, sl[w][g], den);
@@ -584,8 +582,9 @@ __device__ __forceinline__ float combine_waves(const float (&sm)[kWaves][G], con
     return M;
 }
 
-template <typename T, int DH, int G, bool MF>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+template <int NW, typename T, int DH, int G, bool MF>
+__global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
+    constexpr int kThreads = NW * kWave;
     constexpr int VEC = MF ? DH / 16 : Vec16<T>::N;  // output dims a lane accumulates
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -618,11 +617,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
-        __shared__ float s_pw[kWaves][16 * G];
-        mfma_loop<DH, G>(p, b, kvh, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
+        __shared__ float s_pw[NW][16 * G];
+        mfma_loop<NW, DH, G>(p, b, kvh, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
-        valu_loop<T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
+        valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
 
     if (bump && threadIdx.x == 0 && seq_prev == (unsigned)(p.Hkv * p.S - 1)) {
@@ -635,8 +634,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     const bool holder = MF ? ((lane & 3) == 0) : (lane < LPR);
     const int dbase = MF ? (lane >> 2) * VEC : lane * VEC;
 
-    __shared__ float s_acc[kWaves][G][DH];
-    __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+    __shared__ float s_acc[NW][G][DH];
+    __shared__ float s_m[NW][G], s_l[NW][G];
     if (holder) {
 #pragma unroll
         for (int g = 0; g < G; ++g)
@@ -659,7 +658,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int t = threadIdx.x; t < G * DH; t += kThreads) {
             const int g = t / DH, d = t % DH;
             float num, den;
-            combine_waves<G, DH>(s_m, s_l, s_acc, g, d, num, den);
+            combine_waves<NW, G, DH>(s_m, s_l, s_acc, g, d, num, den);
             outp[t] = den > 0.f ? num / den : 0.f;
         }
     } else {
@@ -670,8 +669,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int t = threadIdx.x; t < G * DH / 2; t += kThreads) {
             const int g = (2 * t) / DH, d = (2 * t) % DH;
             float n0, n1, den;
-            const float M = combine_waves<G, DH>(s_m, s_l, s_acc, g, d, n0, den);
-            combine_waves<G, DH>(s_m, s_l, s_acc, g, d + 1, n1, den);
+            const float M = combine_waves<NW, G, DH>(s_m, s_l, s_acc, g, d, n0, den);
+            combine_waves<NW, G, DH>(s_m, s_l, s_acc, g, d + 1, n1, den);
             coherent_store2(&p.part_acc[(part + g) * DH + d], n0, n1);
             if (d == 0) coherent_store2(&p.part_ml[(part + g) * 2], M, den);
         }
@@ -692,7 +691,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         constexpr int kMB = kPairs >= 4 ? 8 : 16;
         const float *ml = p.part_ml + head * p.S * G * 2;
         const float *ac = p.part_acc + head * p.S * G * DH;
-        float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= kWaves*G*DH floats (S <= 2*DH)
+        float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= NW*G*DH floats (S <= 2*DH)
         float2 a[kPairs][kMB];
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
@@ -758,7 +757,14 @@ template <typename T, int DH, int G>
 hipError_t launch3(const DecodeParams &p, hipStream_t stream) {
     dim3 grid(p.S, p.Hkv, p.B);
     constexpr bool kMf = sizeof(T) == 2 && G >= CMC_MFMA_MIN_G && G <= 4;
-    decode_kernel<T, DH, G, kMf><<<grid, kThreads, 0, stream>>>(p);
+    if (p.waves == 4) {
+        decode_kernel<4, T, DH, G, kMf><<<grid, 4 * kWave, 0, stream>>>(p);
+    } else if constexpr (decode_waves_ok(8, G, DH)) {
+        if (p.waves != 8) return hipErrorInvalidValue;
+        decode_kernel<8, T, DH, G, kMf><<<grid, 8 * kWave, 0, stream>>>(p);
+    } else {
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

@@ -7,6 +7,14 @@
 
 namespace cmc {
 
+// A decode workgroup has 4 or 8 waves, each streaming its own 16-key blocks;
+// the workgroup combines them in LDS.  8 waves (at most 256 VGPRs each) are
+// built only for heads whose kernels fit that without spilling: Dh <= 128,
+// or Dh = 256 with one query head per kv head.
+constexpr bool decode_waves_ok(int waves, int G, int Dh) {
+    return waves == 4 || (waves == 8 && (Dh <= 128 || G == 1));
+}
+
 struct DecodeParams {
     const float *q;           // [B][Hq][Dh]
     const void *cme_k;        // [B][Hkv][N][Dh]
@@ -24,6 +32,7 @@ struct DecodeParams {
     unsigned *seq_counter;    // [B] kv-head arrivals, zero between calls
     int k, W, B, Hq, Hkv, N, T_new;
     int S, chunk;             // key-axis splits and keys per split
+    int waves;                // waves per workgroup: 4 or 8
     float qscale;             // scale * log2(e)
 };
 
@@ -31,7 +40,7 @@ struct DecodeParams {
 // launch agree.  Workspace layout: [sequence counters | pair counters]
 // (zero between calls), then the per-split partials.
 struct DecodePlan {
-    int S = 0, chunk = 0;
+    int S = 0, chunk = 0, waves = 4;
     size_t counter_bytes = 0, ml_bytes = 0, acc_bytes = 0, total = 0;
 };
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W);

@@ -254,3 +254,27 @@ def step_new_kv(w: Workload, step: int, layer: int = 0, t_new: int = 1):
 def kv_to_f32(w: Workload, x: np.ndarray) -> np.ndarray:
     """K/V tensor as exact fp32 values (bf16 widened)."""
     return bf16_bits_to_f32(x) if w.kv_dtype == "bf16" else np.asarray(x, np.float32)
+
+
+# ------------------------------------------------- device-side generation
+#
+# The 32-layer stack (tens of GB of K/V) is drawn directly on the GPU with
+# torch's counter-based generator, one stream per (seed, role, ids) as above.
+# These draws are not bit-identical to the numpy ones; they feed timing
+# runs only (parity for that shape runs a single layer from the numpy
+# streams).
+
+def _device_seed(seed: int, role: str, ids: Sequence[int]) -> int:
+    ss = np.random.SeedSequence([int(seed), ROLE[role], *[int(i) for i in ids]])
+    return int(ss.generate_state(1, np.uint64)[0] & np.uint64((1 << 63) - 1))
+
+
+def device_normal(seed: int, role: str, ids: Sequence[int], shape, std: float, device, dtype):
+    """N(0, std^2) draws generated on `device`, returned in `dtype`."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(_device_seed(seed, role, ids))
+    x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    if std != 1.0:
+        x.mul_(std)
+    return x.to(dtype)

@@ -208,6 +208,23 @@ def test_decode_step_fused(orc, dtype, Dh, G, t_new, W, fill):
                  seed=Dh * G + t_new + W, steps=4, fused=True, t_new=t_new)
 
 
+@pytest.mark.parametrize("B,Hkv,G,Dh,dtype,N,k,W,fill", [
+    (48, 4, 4, 128, "bf16", 64, 37, 75, 75),      # 192 pairs: one 8-wave workgroup each
+    (32, 8, 4, 128, "bf16", 400, 300, 500, 500),  # 256 pairs, several blocks per wave, ragged tail
+    (32, 8, 4, 128, "bf16", 20, 0, 16, 3),        # 256 pairs, fewer keys than waves
+    (64, 4, 8, 64, "bf16", 40, 20, 33, 10),       # VALU path (G = 8), ring not yet full
+    (32, 8, 1, 256, "bf16", 100, 64, 128, 128),   # wide head, G = 1
+    (32, 8, 2, 256, "bf16", 40, 30, 50, 50),      # wide head, G = 2: stays on 4 waves
+    (40, 5, 2, 128, "f32", 50, 45, 60, 60),       # 200 pairs, fp32
+    (64, 4, 1, 64, "f32", 30, 10, 0, 0),          # 256 pairs, no window
+])
+def test_decode_wide_workgroups(orc, B, Hkv, G, Dh, dtype, N, k, W, fill):
+    """Batches with 192..256 (sequence, kv head) pairs run one 8-wave
+    workgroup per pair; results match the oracle like every other plan."""
+    _decode_case(orc, B=B, Hq=G * Hkv, Hkv=Hkv, Dh=Dh, N=N, k=k, W=W, fill=fill, dtype=dtype,
+                 seed=B * Hkv + G + Dh, steps=3, fused=W > 0)
+
+
 def test_decode_empty_window_zero_output(orc):
     """k = 0 and an empty ring: zeros, like the oracle."""
     _decode_case(orc, B=1, Hq=4, Hkv=4, Dh=64, N=10, k=0, W=4, fill=0, dtype="f32", seed=1, steps=1)
