@@ -104,31 +104,60 @@ class Inputs:
         nkv = [wl.step_new_kv(w, t) for t in range(self.P)]
         self.nk = [to_dev(a, dev) for a, _ in nkv]
         self.nv = [to_dev(b, dev) for _, b in nkv]
-        self.idx = torch.empty((w.B, w.k), dtype=torch.int32, device=dev)
+        self.idx = torch.empty((w.B, w.idx_stride), dtype=torch.int32, device=dev)
         self.out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=dev)
+        if w.ragged:
+            rs = wl.ragged_sizes(w)
+            self.n_rows, self.q_rows = to_dev(rs["n_rows"], dev), to_dev(rs["q_rows"], dev)
+            self.k_out = torch.empty((w.B,), dtype=torch.int32, device=dev)
         from paper_2609_25537_amd import cmc
         self.sel_ws = torch.empty(max(1, cmc.cmc_select_workspace_bytes(w.B, w.N)), dtype=torch.uint8, device=dev)
-        self.dec_ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, dev)
+        self.dec_ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.idx_stride, w.W, dev)
+
+    def select(self):
+        from paper_2609_25537_amd import cmc
+        w = self.w
+        if w.ragged:
+            cmc.cmc_select_cmes_ragged(self.keys, self.qv, self.n_rows, w.k, q_rows=self.q_rows,
+                                       idx_stride=w.idx_stride, idx_out=self.idx, k_out=self.k_out,
+                                       workspace=self.sel_ws)
+        else:
+            cmc.cmc_select_cmes(self.keys, self.qv, w.k, idx_out=self.idx, workspace=self.sel_ws)
+
+    def decode_step(self, j):
+        from paper_2609_25537_amd import cmc
+        w = self.w
+        if w.ragged:
+            cmc.cmc_decode_step_ragged(self.q[j], self.pk, self.pv, self.idx, self.k_out, w.idx_stride, self.wk,
+                                       self.wv, self.wc, self.nk[j], self.nv[j], w.scale, out=self.out,
+                                       workspace=self.dec_ws)
+        else:
+            cmc.cmc_decode_step(self.q[j], self.pk, self.pv, self.idx, w.k, self.wk, self.wv, self.wc, self.nk[j],
+                                self.nv[j], w.scale, out=self.out, workspace=self.dec_ws)
 
 
 def run_pass(inp: Inputs, steps: int):
     """One pass of the hot path: select once, then `steps` decode iterations."""
-    from paper_2609_25537_amd import cmc
-    w = inp.w
-    cmc.cmc_select_cmes(inp.keys, inp.qv, w.k, idx_out=inp.idx, workspace=inp.sel_ws)
+    inp.select()
     for t in range(steps):
-        j = t % inp.P
-        cmc.cmc_decode_step(inp.q[j], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, inp.nk[j], inp.nv[j],
-                            w.scale, out=inp.out, workspace=inp.dec_ws)
+        inp.decode_step(t % inp.P)
 
 
 def decode_bytes(w) -> int:
-    """Algorithmic bytes of one decode-step launch: K and V of the k + W
-    keys (ring full, the newest row read from the appended input), the
-    appended row written into the ring, q, out and the index list."""
-    kv = w.B * w.Hkv * (w.k + w.W) * w.Dh * w.kv_bytes * 2
-    ring_write = w.B * w.Hkv * w.Dh * w.kv_bytes * 2
-    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2 + w.B * w.k * 4
+    """Algorithmic bytes of one decode-step launch with the ring full: K and
+    V of the k + W keys of each sequence (the newest row read from the
+    appended input; a ragged sequence has its own k_b + q_b pool rows), the
+    appended row written into the ring, q, out and the index entries."""
+    from paper_2609_25537_amd import workloads as wl
+    if w.ragged:
+        rs = wl.ragged_sizes(w)
+        pool = int(np.minimum(rs["n_rows"], w.k).sum() + rs["q_rows"].sum())
+    else:
+        pool = w.B * w.k
+    row = w.Dh * w.kv_bytes * 2
+    kv = w.Hkv * (pool + w.B * w.W) * row
+    ring_write = w.B * w.Hkv * row
+    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2 + pool * 4
 
 
 def capture(fn):
@@ -155,9 +184,7 @@ def time_decode_launch(inp: Inputs, reps: int = 500):
 
     def launches():
         for r in range(reps):
-            j = r % inp.P
-            cmc.cmc_decode_step(inp.q[j], inp.pk, inp.pv, inp.idx, w.k, inp.wk, inp.wv, inp.wc, inp.nk[j],
-                                inp.nv[j], w.scale, out=inp.out, workspace=inp.dec_ws)
+            inp.decode_step(r % inp.P)
 
     g = capture(launches)
     s = torch.cuda.current_stream()
@@ -180,8 +207,12 @@ def cpu_baseline(w, budget_s: float):
     from paper_2609_25537_amd import workloads as wl
     orc = oracle.default()
     keys, qv = wl.sel_keys(w), wl.q_vecs(w)
+    rs = wl.ragged_sizes(w)
     t0 = time.perf_counter()
-    idx, _, _ = orc.select(keys, qv, w.k)
+    if w.ragged:
+        idx, k_out = orc.select_ragged(keys, qv, rs["n_rows"], w.k, rs["q_rows"], w.idx_stride)
+    else:
+        idx, _, _ = orc.select(keys, qv, w.k)
     t_sel = time.perf_counter() - t0
     pk, pv = wl.pool_kv(w)
     wk, wv, cnt = wl.window_kv(w)
@@ -191,7 +222,10 @@ def cpu_baseline(w, budget_s: float):
         q = wl.step_q(w, n)
         t0 = time.perf_counter()
         orc.window_append(wk, wv, cnt, nk, nv)
-        orc.two_tier_decode(q, pk, pv, idx, w.k, wk, wv, cnt, w.W, w.scale)
+        if w.ragged:
+            orc.two_tier_decode_ragged(q, pk, pv, idx, k_out, w.idx_stride, wk, wv, cnt, w.W, w.scale)
+        else:
+            orc.two_tier_decode(q, pk, pv, idx, w.k, wk, wv, cnt, w.W, w.scale)
         t_dec += time.perf_counter() - t0
         n += 1
     per_step = t_dec / n
@@ -497,7 +531,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Dh": w.Dh, "N": w.N,
                    "D": w.D, "k": w.k, "W": w.W, "decode_steps": steps, "layers": w.layers,
-                   "kv_dtype": w.kv_dtype, "step_input_sets": inp.P, "graph": bool(graph)},
+                   "kv_dtype": w.kv_dtype, "step_input_sets": inp.P, "graph": bool(graph),
+                   **({"ragged": {"ctx_tokens": [w.ctx_min, w.ctx_max], "ratio": w.ratio,
+                                  "question_rows": [w.q_min, w.q_max]}} if w.ragged else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

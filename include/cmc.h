@@ -15,6 +15,7 @@
  *   cmc_window_append    Tier-2 ring-buffer append (every step)
  *   cmc_two_tier_decode  decode attention over [selected rows || window]
  *   cmc_decode_step      append + decode fused into one launch (every step)
+ *   *_ragged             the same with per-sequence sizes (ragged batches)
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -85,6 +86,42 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec,
                            int B, int N, int D, int k,
                            int32_t *idx_out, float *scores_out,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Ragged batches: the selection of cmc_select_cmes with a per-sequence
+ * candidate count, plus the question rows that the assembled cache keeps
+ * beside the selected rows (Sec. 2.5, KV cache assembly: the prefill input is
+ * [M* || C_local || q], so the cache holds K + W + |q| rows; the number of
+ * memory rows per sequence follows from its context length, Sec. 2.3).
+ *
+ *   n_rows     [B] int32 (device)  candidates of sequence b: rows [0, n_b) of
+ *                                  sel_keys[b] (n_b clamped into [0, N] on the
+ *                                  device; rows past it score -inf in
+ *                                  scores_out and are never selected)
+ *   q_rows     [B] int32 (device)  question rows pinned after the selection, or
+ *                                  NULL for none: q_b rows, clamped into
+ *                                  [0, idx_stride - k_b]
+ *   idx_out    [B][idx_stride] int32  row b = the k_b = min(k, n_b) selected
+ *                                  rows ascending (the order and tie rule of
+ *                                  cmc_select_cmes), then n_b, n_b+1, ...,
+ *                                  n_b+q_b-1 (the question's rows, which the
+ *                                  caller stores in the K/V pool right after
+ *                                  sequence b's memory rows), then -1 up to
+ *                                  idx_stride
+ *   k_out      [B] int32           k_b + q_b (the k_len of the ragged decode
+ *                                  calls), or NULL
+ *   sel_keys, q_vec, scores_out, workspace: as cmc_select_cmes (N is the row
+ *   stride of sel_keys and scores_out)
+ *
+ * Limits: B >= 0, N >= 0, k >= 0, idx_stride >= k, D >= 4 and D % 4 == 0,
+ * N <= 32768.  k may exceed N (then k_b = n_b).  With n_b = N and no question
+ * rows the result equals cmc_select_cmes.
+ */
+cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec,
+                                  const int32_t *n_rows, const int32_t *q_rows,
+                                  int B, int N, int D, int k, int idx_stride,
+                                  int32_t *idx_out, int32_t *k_out, float *scores_out,
+                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Tier-2 window.                                                           */
@@ -186,6 +223,36 @@ cmc_status cmc_decode_step(const float *q,
                            cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
                            float scale, float *out,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Ragged batches (Sec. 2.5, KV cache assembly, with per-sequence sizes): as
+ * cmc_two_tier_decode and cmc_decode_step, except that sequence b's Tier-1
+ * key rows are its first k_b entries of idx, k_b = k_len[b] clamped into
+ * [0, k] on the device; k is the row stride of idx.  k_len is typically the
+ * k_out of cmc_select_cmes_ragged (selected rows plus pinned question rows).
+ * The window fill is per sequence through win_count, as always.  A sequence
+ * whose key list is empty gets a zero row.  Same workspace, limits and
+ * arithmetic as the uniform calls (the workspace is sized by k and W).
+ *
+ *   k_len      [B] int32 (device), non-NULL
+ */
+cmc_status cmc_two_tier_decode_ragged(const float *q,
+                                      const void *cme_k, const void *cme_v,
+                                      const int32_t *idx, const int32_t *k_len, int k,
+                                      const void *win_k, const void *win_v,
+                                      const int32_t *win_count, int W,
+                                      cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                                      float scale, float *out,
+                                      void *workspace, size_t workspace_bytes, void *stream);
+
+cmc_status cmc_decode_step_ragged(const float *q,
+                                  const void *cme_k, const void *cme_v,
+                                  const int32_t *idx, const int32_t *k_len, int k,
+                                  void *win_k, void *win_v, int32_t *win_count, int W,
+                                  const void *new_k, const void *new_v, int T_new,
+                                  cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                                  float scale, float *out,
+                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                             */

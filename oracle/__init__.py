@@ -9,7 +9,9 @@ Functions follow Sec. 2.5 of the paper ("Inference with Two-Tier KV Cache
 Policy"): ``select`` (Tier-1 cosine score and top-K in document order),
 ``window_start`` (Tier-2 window equation), ``window_append`` (the ring that
 keeps the cache bounded by K + W + |q|) and ``two_tier_decode`` (softmax
-attention over the assembled cache).
+attention over the assembled cache), plus ``select_ragged`` and
+``two_tier_decode_ragged`` (the same definitions per sequence, for batches
+whose sequences differ in size).
 
 ``Oracle(path)`` binds any build of the same source (the tests use it to
 load deliberately mutated builds and show that the pins reject them); the
@@ -162,6 +164,57 @@ class Oracle:
         _check(rc, "two_tier_decode")
         return out
 
+    # ------------------------------------------------------- ragged batches
+    #
+    # A ragged batch is the uniform definition applied to each sequence on
+    # its own sizes (Sec. 2.3: the number of memory rows follows from the
+    # context length; Sec. 2.5: the assembled cache is [M* || C_local || q],
+    # so the question's rows stay beside the selected ones).
+
+    def select_ragged(self, sel_keys: np.ndarray, q_vec: np.ndarray, n_rows: np.ndarray, k: int,
+                      q_rows: Optional[np.ndarray] = None, idx_stride: Optional[int] = None
+                      ) -> Tuple[np.ndarray, np.ndarray]:
+        """Sequence b: candidates are its rows [0, n_b) (n_b clamped into
+        [0, N]); it keeps k_b = min(k, n_b) of them by the Tier-1 rule
+        (select on those rows alone), then lists its q_b question rows n_b,
+        ..., n_b + q_b - 1 (q_b clamped into [0, idx_stride - k_b]), then -1
+        up to idx_stride.  Returns (idx [B][idx_stride] int32, k_out [B] =
+        k_b + q_b)."""
+        keys = np.ascontiguousarray(sel_keys, np.float32)
+        B, N, D = keys.shape
+        stride = k if idx_stride is None else int(idx_stride)
+        idx = np.full((B, stride), -1, np.int32)
+        k_out = np.zeros((B,), np.int32)
+        for b in range(B):
+            nb = min(max(int(n_rows[b]), 0), N)
+            kb = min(k, nb)
+            if kb > 0:
+                sel, _, _ = self.select(keys[b:b + 1, :nb], np.asarray(q_vec, np.float32)[b:b + 1], kb)
+                idx[b, :kb] = sel[0]
+            qb = 0 if q_rows is None else min(max(int(q_rows[b]), 0), stride - kb)
+            idx[b, kb:kb + qb] = nb + np.arange(qb, dtype=np.int32)
+            k_out[b] = kb + qb
+        return idx, k_out
+
+    def two_tier_decode_ragged(self, q: np.ndarray, cme_k: np.ndarray, cme_v: np.ndarray,
+                               idx: Optional[np.ndarray], k_len: np.ndarray, k: int,
+                               win_k: Optional[np.ndarray], win_v: Optional[np.ndarray],
+                               win_count: Optional[np.ndarray], W: int, scale: float) -> np.ndarray:
+        """Two-tier decode where sequence b's pool rows are its first k_b =
+        k_len[b] (clamped into [0, k]) entries of idx (or rows 0..k_b-1 when
+        idx is None); k is the row stride of idx."""
+        B = q.shape[0]
+        out = np.zeros(q.shape, np.float64)
+        for b in range(B):
+            kb = min(max(int(k_len[b]), 0), k)
+            sl = slice(b, b + 1)
+            ib = None if idx is None else np.ascontiguousarray(idx[sl, :kb])
+            wk = wv = wc = None
+            if W > 0:
+                wk, wv, wc = win_k[sl], win_v[sl], win_count[sl]
+            out[sl] = self.two_tier_decode(q[sl], cme_k[sl], cme_v[sl], ib, kb, wk, wv, wc, W, scale)
+        return out
+
 
 _default: Optional[Oracle] = None
 
@@ -197,3 +250,11 @@ def window_append(win_k, win_v, win_count, new_k, new_v):
 
 def two_tier_decode(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, W, scale):
     return default().two_tier_decode(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, W, scale)
+
+
+def select_ragged(sel_keys, q_vec, n_rows, k, q_rows=None, idx_stride=None):
+    return default().select_ragged(sel_keys, q_vec, n_rows, k, q_rows, idx_stride)
+
+
+def two_tier_decode_ragged(q, cme_k, cme_v, idx, k_len, k, win_k, win_v, win_count, W, scale):
+    return default().two_tier_decode_ragged(q, cme_k, cme_v, idx, k_len, k, win_k, win_v, win_count, W, scale)

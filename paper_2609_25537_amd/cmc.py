@@ -6,7 +6,8 @@ step of the computation runs in the library's HIP kernels; there is no
 fallback path, and a missing library raises.
 
 Names match the C entry points: ``cmc_select_cmes``, ``cmc_window_append``,
-``cmc_two_tier_decode``, the two workspace queries and ``cmc_window_start``.
+``cmc_two_tier_decode``, ``cmc_decode_step``, their ``*_ragged`` variants,
+the two workspace queries and ``cmc_window_start``.
 bf16 K/V tensors (torch.bfloat16) are passed through as their raw bits.
 """
 from __future__ import annotations
@@ -29,9 +30,10 @@ CMC_F32 = 0
 CMC_BF16 = 1
 
 EXPORTED = [
-    "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_window_append", "cmc_window_start",
-    "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step", "cmc_status_string",
-    "cmc_last_error", "cmc_version",
+    "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_window_append",
+    "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
+    "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_status_string", "cmc_last_error",
+    "cmc_version",
 ]
 
 
@@ -69,6 +71,14 @@ def lib() -> ctypes.CDLL:
         L.cmc_decode_step.argtypes = [P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
                                       ctypes.c_float, P, P, SZ, P]
         L.cmc_decode_step.restype = I
+        L.cmc_select_cmes_ragged.argtypes = [P, P, P, P, I, I, I, I, I, P, P, P, P, SZ, P]
+        L.cmc_select_cmes_ragged.restype = I
+        L.cmc_two_tier_decode_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
+                                                 ctypes.c_float, P, P, SZ, P]
+        L.cmc_two_tier_decode_ragged.restype = I
+        L.cmc_decode_step_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
+                                             ctypes.c_float, P, P, SZ, P]
+        L.cmc_decode_step_ragged.restype = I
         L.cmc_status_string.argtypes = [I]
         L.cmc_status_string.restype = ctypes.c_char_p
         L.cmc_last_error.argtypes = []
@@ -160,6 +170,43 @@ def cmc_select_cmes(sel_keys, q_vec, k: int, idx_out=None, scores_out=None, work
     return idx_out
 
 
+def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_stride: Optional[int] = None,
+                           idx_out=None, k_out=None, scores_out=None, workspace=None, stream=None):
+    """Ragged Tier-1 selection: sequence b's candidates are its first
+    n_rows[b] rows; q_rows[b] pinned question rows (pool rows n_b ..) follow
+    the selected ones.  n_rows/q_rows [B] int32 (device).  Returns
+    (idx_out [B][idx_stride] int32, k_out [B] int32)."""
+    import torch
+    _need(sel_keys.dim() == 3 and sel_keys.is_contiguous(), "sel_keys must be contiguous [B][N][D]")
+    B, N, D = sel_keys.shape
+    _need(q_vec.shape == (B, D) and q_vec.is_contiguous(), "q_vec must be contiguous [B][D]")
+    _need(sel_keys.dtype == torch.float32 and q_vec.dtype == torch.float32, "fp32 inputs expected")
+    _need(n_rows.shape == (B,) and n_rows.dtype == torch.int32 and n_rows.is_contiguous(), "n_rows [B] int32")
+    if q_rows is not None:
+        _need(q_rows.shape == (B,) and q_rows.dtype == torch.int32 and q_rows.is_contiguous(), "q_rows [B] int32")
+    stride = int(k if idx_stride is None else idx_stride)
+    dev = sel_keys.device
+    if idx_out is None:
+        idx_out = torch.empty((B, stride), dtype=torch.int32, device=dev)
+    _need(idx_out.shape == (B, stride) and idx_out.dtype == torch.int32 and idx_out.is_contiguous(),
+          "idx_out must be contiguous int32 [B][idx_stride]")
+    if k_out is None:
+        k_out = torch.empty((B,), dtype=torch.int32, device=dev)
+    _need(k_out.shape == (B,) and k_out.dtype == torch.int32, "k_out [B] int32")
+    if scores_out is not None:
+        _need(scores_out.shape == (B, N) and scores_out.dtype == torch.float32, "scores_out [B][N] fp32")
+    ws_bytes = 0
+    if scores_out is None and workspace is None:
+        workspace = torch.empty(max(1, cmc_select_workspace_bytes(B, N)), dtype=torch.uint8, device=dev)
+    if workspace is not None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_select_cmes_ragged(_ptr(sel_keys), _ptr(q_vec), _ptr(n_rows), _ptr(q_rows), B, N, D,
+                                      int(k), stride, _ptr(idx_out), _ptr(k_out), _ptr(scores_out),
+                                      _ptr(workspace), ws_bytes, _stream(stream))
+    _check(rc)
+    return idx_out, k_out
+
+
 # ---------------------------------------------------------------- window
 
 def cmc_window_start(ctx_len: int, W: int, alpha: int) -> int:
@@ -196,53 +243,15 @@ def decode_workspace(B: int, Hq: int, Hkv: int, Dh: int, k: int, W: int, device)
                        device=device)
 
 
-def cmc_two_tier_decode(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, scale: float,
-                        out=None, workspace=None, W: Optional[int] = None, stream=None):
-    """One decode step over [pool rows idx || ring slots].  q [B][Hq][Dh] fp32,
-    cme_* [B][Hkv][N][Dh], idx [B][k] int32 or None, win_* [B][Hkv][W][Dh] or
-    None (W = 0), win_count [B] int32.  Returns out [B][Hq][Dh] fp32."""
+def _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, workspace, W, k_len):
+    """Checks shared by the decode wrappers; returns the C call's sizes and
+    the (possibly allocated) out and workspace."""
     import torch
     _need(q.dim() == 3 and q.is_contiguous() and q.dtype == torch.float32, "q must be contiguous fp32 [B][Hq][Dh]")
     B, Hq, Dh = q.shape
     _need(cme_k.dim() == 4 and cme_k.is_contiguous() and cme_v.is_contiguous(), "cme_k/v [B][Hkv][N][Dh]")
     _need(cme_k.shape[0] == B and cme_k.shape[3] == Dh and cme_v.shape == cme_k.shape, "pool shape")
-    Hkv, N = cme_k.shape[1], cme_k.shape[2]
     _need(cme_v.dtype == cme_k.dtype, "cme_v dtype must match cme_k")
-    if W is None:
-        W = 0 if win_k is None else win_k.shape[2]
-    if W > 0:
-        _need(win_k.shape == (B, Hkv, W, Dh) and win_v.shape == win_k.shape, "window shape")
-        _need(win_k.dtype == cme_k.dtype == win_v.dtype, "window dtype must match pool")
-        _need(win_k.is_contiguous() and win_v.is_contiguous(), "window must be contiguous")
-        _need(win_count is not None and win_count.shape == (B,) and win_count.dtype == torch.int32,
-              "win_count [B] int32")
-    if idx is not None:
-        _need(idx.shape == (B, k) and idx.dtype == torch.int32 and idx.is_contiguous(), "idx [B][k] int32")
-    if out is None:
-        out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
-    _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
-    if workspace is None:
-        workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
-    ws_bytes = workspace.numel() * workspace.element_size()
-    rc = lib().cmc_two_tier_decode(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k),
-                                   _ptr(win_k) if W > 0 else None, _ptr(win_v) if W > 0 else None,
-                                   _ptr(win_count) if W > 0 else None, int(W), _kv_dtype(cme_k),
-                                   B, Hq, Hkv, Dh, N, float(scale), _ptr(out), _ptr(workspace),
-                                   ws_bytes, _stream(stream))
-    _check(rc)
-    return out
-
-
-def cmc_decode_step(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, new_k, new_v, scale: float,
-                    out=None, workspace=None, W: Optional[int] = None, stream=None):
-    """Ring append of new_k/new_v [B][Hkv][T][Dh] followed by the two-tier
-    decode, in one launch.  Same arguments as cmc_two_tier_decode plus the
-    new rows.  Returns out [B][Hq][Dh] fp32."""
-    import torch
-    _need(q.dim() == 3 and q.is_contiguous() and q.dtype == torch.float32, "q must be contiguous fp32 [B][Hq][Dh]")
-    B, Hq, Dh = q.shape
-    _need(cme_k.dim() == 4 and cme_k.is_contiguous() and cme_v.is_contiguous(), "cme_k/v [B][Hkv][N][Dh]")
-    _need(cme_k.shape[0] == B and cme_k.shape[3] == Dh and cme_v.shape == cme_k.shape, "pool shape")
     Hkv, N = cme_k.shape[1], cme_k.shape[2]
     if W is None:
         W = 0 if win_k is None else win_k.shape[2]
@@ -253,23 +262,74 @@ def cmc_decode_step(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, new_k
         _need(win_k.is_contiguous() and win_v.is_contiguous(), "window must be contiguous")
         _need(win_count is not None and win_count.shape == (B,) and win_count.dtype == torch.int32,
               "win_count [B] int32")
-        _need(new_k.dim() == 4 and new_k.shape[:2] == (B, Hkv) and new_k.shape[3] == Dh, "new_k [B][Hkv][T][Dh]")
-        _need(new_v.shape == new_k.shape and new_k.dtype == new_v.dtype == cme_k.dtype, "new_k/v must match")
-        _need(new_k.is_contiguous() and new_v.is_contiguous(), "new_k/v must be contiguous")
-        T = int(new_k.shape[2])
+        if new_k is not None:
+            _need(new_k.dim() == 4 and new_k.shape[:2] == (B, Hkv) and new_k.shape[3] == Dh,
+                  "new_k [B][Hkv][T][Dh]")
+            _need(new_v.shape == new_k.shape and new_k.dtype == new_v.dtype == cme_k.dtype, "new_k/v must match")
+            _need(new_k.is_contiguous() and new_v.is_contiguous(), "new_k/v must be contiguous")
+            T = int(new_k.shape[2])
     if idx is not None:
         _need(idx.shape == (B, k) and idx.dtype == torch.int32 and idx.is_contiguous(), "idx [B][k] int32")
+    if k_len is not None:
+        _need(k_len.shape == (B,) and k_len.dtype == torch.int32 and k_len.is_contiguous(), "k_len [B] int32")
     if out is None:
         out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
     _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
     if workspace is None:
         workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
     ws_bytes = workspace.numel() * workspace.element_size()
-    rc = lib().cmc_decode_step(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k),
-                               _ptr(win_k) if W > 0 else None, _ptr(win_v) if W > 0 else None,
-                               _ptr(win_count) if W > 0 else None, int(W),
-                               _ptr(new_k) if W > 0 else None, _ptr(new_v) if W > 0 else None, T,
-                               _kv_dtype(cme_k), B, Hq, Hkv, Dh, N, float(scale), _ptr(out), _ptr(workspace),
-                               ws_bytes, _stream(stream))
+    win = ((_ptr(win_k), _ptr(win_v), _ptr(win_count)) if W > 0 else (None, None, None))
+    new = ((_ptr(new_k), _ptr(new_v)) if W > 0 and new_k is not None else (None, None))
+    return dict(B=B, Hq=Hq, Hkv=Hkv, Dh=Dh, N=N, W=int(W), T=T, win=win, new=new, out=out, workspace=workspace,
+                ws_bytes=ws_bytes, dtype=_kv_dtype(cme_k))
+
+
+def cmc_two_tier_decode(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, scale: float,
+                        out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """One decode step over [pool rows idx || ring slots].  q [B][Hq][Dh] fp32,
+    cme_* [B][Hkv][N][Dh], idx [B][k] int32 or None, win_* [B][Hkv][W][Dh] or
+    None (W = 0), win_count [B] int32.  Returns out [B][Hq][Dh] fp32."""
+    a = _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, None, None, out, workspace, W, None)
+    rc = lib().cmc_two_tier_decode(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k), *a["win"], a["W"],
+                                   a["dtype"], a["B"], a["Hq"], a["Hkv"], a["Dh"], a["N"], float(scale),
+                                   _ptr(a["out"]), _ptr(a["workspace"]), a["ws_bytes"], _stream(stream))
     _check(rc)
-    return out
+    return a["out"]
+
+
+def cmc_decode_step(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, new_k, new_v, scale: float,
+                    out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """Ring append of new_k/new_v [B][Hkv][T][Dh] followed by the two-tier
+    decode, in one launch.  Same arguments as cmc_two_tier_decode plus the
+    new rows.  Returns out [B][Hq][Dh] fp32."""
+    a = _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, workspace, W, None)
+    rc = lib().cmc_decode_step(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k), *a["win"], a["W"],
+                               *a["new"], a["T"], a["dtype"], a["B"], a["Hq"], a["Hkv"], a["Dh"], a["N"],
+                               float(scale), _ptr(a["out"]), _ptr(a["workspace"]), a["ws_bytes"], _stream(stream))
+    _check(rc)
+    return a["out"]
+
+
+def cmc_two_tier_decode_ragged(q, cme_k, cme_v, idx, k_len, k: int, win_k, win_v, win_count, scale: float,
+                               out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """cmc_two_tier_decode with per-sequence pool-row counts k_len [B] int32
+    (device); k is the row stride of idx."""
+    a = _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, None, None, out, workspace, W, k_len)
+    rc = lib().cmc_two_tier_decode_ragged(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), _ptr(k_len), int(k),
+                                          *a["win"], a["W"], a["dtype"], a["B"], a["Hq"], a["Hkv"], a["Dh"],
+                                          a["N"], float(scale), _ptr(a["out"]), _ptr(a["workspace"]),
+                                          a["ws_bytes"], _stream(stream))
+    _check(rc)
+    return a["out"]
+
+
+def cmc_decode_step_ragged(q, cme_k, cme_v, idx, k_len, k: int, win_k, win_v, win_count, new_k, new_v,
+                           scale: float, out=None, workspace=None, W: Optional[int] = None, stream=None):
+    """cmc_decode_step with per-sequence pool-row counts k_len [B] int32."""
+    a = _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, workspace, W, k_len)
+    rc = lib().cmc_decode_step_ragged(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), _ptr(k_len), int(k),
+                                      *a["win"], a["W"], *a["new"], a["T"], a["dtype"], a["B"], a["Hq"], a["Hkv"],
+                                      a["Dh"], a["N"], float(scale), _ptr(a["out"]), _ptr(a["workspace"]),
+                                      a["ws_bytes"], _stream(stream))
+    _check(rc)
+    return a["out"]

@@ -154,9 +154,43 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int
                         workspace ? workspace_bytes : (size_t)0);
         scores = static_cast<float *>(workspace);
     }
-    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k};
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, k, nullptr, nullptr, nullptr};
     hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select launch");
+    return ok();
+}
+
+cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, const int32_t *n_rows,
+                                  const int32_t *q_rows, int B, int N, int D, int k, int idx_stride,
+                                  int32_t *idx_out, int32_t *k_out, float *scores_out, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
+    if (B < 0 || N < 0 || k < 0 || D < 4)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: need B >= 0, N >= 0, k >= 0, D >= 4 (got B=%d N=%d k=%d D=%d)", B, N, k, D);
+    if (idx_stride < k)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: idx_stride=%d is below k=%d", idx_stride, k);
+    if (D % 4 != 0) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: D=%d must be a multiple of 4", D);
+    if (N > cmc::kSelectMaxN) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: N=%d exceeds %d", N, cmc::kSelectMaxN);
+    if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: B=%d exceeds 65535", B);
+    if (B == 0) return ok();
+    if (!n_rows) return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: n_rows must be non-null");
+    if (N > 0 && (!sel_keys || !q_vec))
+        return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: sel_keys and q_vec must be non-null");
+    if (idx_stride > 0 && !idx_out)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: idx_out must be non-null when idx_stride > 0");
+    if (misaligned(sel_keys) || misaligned(q_vec) || misaligned(n_rows) || misaligned(q_rows) ||
+        misaligned(idx_out) || misaligned(k_out) || misaligned(scores_out) || misaligned(workspace))
+        return fail(CMC_ERR_UNSUPPORTED, "select_ragged: every pointer must be 16-byte aligned");
+    float *scores = scores_out;
+    if (!scores && N > 0) {
+        const size_t need = cmc_select_workspace_bytes(B, N);
+        if (!workspace || workspace_bytes < need)
+            return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "select_ragged: workspace of %zu bytes needed, %zu given",
+                        need, workspace ? workspace_bytes : (size_t)0);
+        scores = static_cast<float *>(workspace);
+    }
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, idx_stride, n_rows, q_rows, k_out};
+    hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "select_ragged launch");
     return ok();
 }
 
@@ -197,7 +231,7 @@ size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W) 
 namespace {
 
 cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
-                       int k, void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
+                       const int32_t *k_len, int k, void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
                        const void *new_v, int T_new, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
                        float scale, float *out, void *workspace, size_t workspace_bytes, void *stream) {
     if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
@@ -223,7 +257,8 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     if (W > 0 && (!win_k || !win_v || !win_count))
         return fail(CMC_ERR_INVALID_ARGUMENT, "%s: null Tier-2 window", fn);
     if (T_new > 0 && (!new_k || !new_v)) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: null new rows", fn);
-    if (misaligned(q) || misaligned(cme_k) || misaligned(cme_v) || misaligned(idx) || misaligned(win_k) ||
+    if (misaligned(q) || misaligned(cme_k) || misaligned(cme_v) || misaligned(idx) || misaligned(k_len) ||
+        misaligned(win_k) ||
         misaligned(win_v) || misaligned(win_count) || misaligned(out) || misaligned(workspace) ||
         misaligned(new_k) || misaligned(new_v))
         return fail(CMC_ERR_UNSUPPORTED, "%s: every pointer must be 16-byte aligned", fn);
@@ -237,6 +272,7 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     p.cme_k = cme_k;
     p.cme_v = cme_v;
     p.idx = idx;
+    p.k_len = k_len;
     p.win_k = W > 0 ? win_k : nullptr;
     p.win_v = W > 0 ? win_v : nullptr;
     p.win_count = W > 0 ? win_count : nullptr;
@@ -273,7 +309,7 @@ cmc_status cmc_two_tier_decode(const float *q, const void *cme_k, const void *cm
                                float scale, float *out, void *workspace, size_t workspace_bytes,
                                void *stream) {
     // Nothing is appended (T_new = 0), so the window is only read.
-    return decode_impl("decode", q, cme_k, cme_v, idx, k, const_cast<void *>(win_k), const_cast<void *>(win_v),
+    return decode_impl("decode", q, cme_k, cme_v, idx, nullptr, k, const_cast<void *>(win_k), const_cast<void *>(win_v),
                        const_cast<int32_t *>(win_count), W, nullptr, nullptr, 0, kv_dtype, B, Hq, Hkv, Dh, N,
                        scale, out, workspace, workspace_bytes, stream);
 }
@@ -285,8 +321,32 @@ cmc_status cmc_decode_step(const float *q, const void *cme_k, const void *cme_v,
                            void *stream) {
     if (W > 0 && T_new < 1)
         return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step: need 1 <= T_new <= W (got T_new=%d W=%d)", T_new, W);
-    return decode_impl("decode_step", q, cme_k, cme_v, idx, k, win_k, win_v, win_count, W, new_k, new_v, T_new,
+    return decode_impl("decode_step", q, cme_k, cme_v, idx, nullptr, k, win_k, win_v, win_count, W, new_k, new_v, T_new,
                        kv_dtype, B, Hq, Hkv, Dh, N, scale, out, workspace, workspace_bytes, stream);
+}
+
+cmc_status cmc_two_tier_decode_ragged(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                                      const int32_t *k_len, int k, const void *win_k, const void *win_v,
+                                      const int32_t *win_count, int W, cmc_dtype kv_dtype, int B, int Hq,
+                                      int Hkv, int Dh, int N, float scale, float *out, void *workspace,
+                                      size_t workspace_bytes, void *stream) {
+    if (B > 0 && !k_len) return fail(CMC_ERR_INVALID_ARGUMENT, "decode_ragged: k_len must be non-null");
+    return decode_impl("decode_ragged", q, cme_k, cme_v, idx, k_len, k, const_cast<void *>(win_k),
+                       const_cast<void *>(win_v), const_cast<int32_t *>(win_count), W, nullptr, nullptr, 0,
+                       kv_dtype, B, Hq, Hkv, Dh, N, scale, out, workspace, workspace_bytes, stream);
+}
+
+cmc_status cmc_decode_step_ragged(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                                  const int32_t *k_len, int k, void *win_k, void *win_v, int32_t *win_count,
+                                  int W, const void *new_k, const void *new_v, int T_new, cmc_dtype kv_dtype,
+                                  int B, int Hq, int Hkv, int Dh, int N, float scale, float *out,
+                                  void *workspace, size_t workspace_bytes, void *stream) {
+    if (B > 0 && !k_len) return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step_ragged: k_len must be non-null");
+    if (W > 0 && T_new < 1)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step_ragged: need 1 <= T_new <= W (got T_new=%d W=%d)",
+                    T_new, W);
+    return decode_impl("decode_step_ragged", q, cme_k, cme_v, idx, k_len, k, win_k, win_v, win_count, W, new_k,
+                       new_v, T_new, kv_dtype, B, Hq, Hkv, Dh, N, scale, out, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

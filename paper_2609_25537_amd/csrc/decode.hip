@@ -129,7 +129,8 @@ __device__ __forceinline__ RowPtrs<T> row_ptrs(int row, int r, const T *poolK, c
 #define LOCATE(row) PTRS(row, FETCH(row))
 
 template <typename T>
-__device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, int kvh, int DH, int slot0) {
+__device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, int kvh, int DH, int kb,
+                                                 int slot0) {
     RowMap<T> m;
     const size_t head = (size_t)b * p.Hkv + kvh;
     m.poolK = static_cast<const T *>(p.cme_k) + head * (size_t)p.N * DH;
@@ -139,7 +140,7 @@ __device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, i
     m.newK = p.T_new > 0 ? static_cast<const T *>(p.new_k) + head * (size_t)p.T_new * DH : nullptr;
     m.newV = p.T_new > 0 ? static_cast<const T *>(p.new_v) + head * (size_t)p.T_new * DH : nullptr;
     m.idx = p.idx ? p.idx + (size_t)b * p.k : nullptr;
-    m.k = p.k;
+    m.k = kb;
     m.W = p.W;
     m.nmax = p.N > 0 ? p.N - 1 : 0;
     m.slot0 = slot0;
@@ -404,22 +405,22 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 }
 
 template <int NW, int DH, int G>
-__device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int c0, int c1, int cnt0,
-                                          int slot0, float *s_p, WaveState<G, DH / 16> &st) {
+__device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int kb, int c0, int c1,
+                                          int cnt0, int slot0, float *s_p, WaveState<G, DH / 16> &st) {
     bf16x8 qa_hi[DH / 32], qa_lo[DH / 32];
     load_q_operand<DH, G>(p, b, kvh, qa_hi, qa_lo);
     const size_t head = (size_t)b * p.Hkv + kvh;
     const int T_new = p.W > 0 ? p.T_new : 0;
     const int n_old = p.W > 0 ? min(cnt0, p.W - T_new) : 0;
-    const int pool_end = p.k, ring_end = p.k + n_old;
+    const int pool_end = kb, ring_end = kb + n_old;
 
     // pool rows
     {
         const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
-        // The list always holds all k pool rows, so this phase's end does not
-        // depend on the ring count: its loads need not wait for that load.
+        // The list holds all kb pool rows whatever the ring count, so this
+        // phase's loads need not wait for the count.
         mfma_phase<NW, DH, G, PoolRows, false>(c0, min(c0 + p.chunk, pool_end), rows, kb, vb, nullptr, nullptr,
                                            qa_hi, qa_lo, s_p, st);
     }
@@ -597,10 +598,15 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
         valid = cnt1 < p.W ? (int)cnt1 : p.W;
         slot0 = cnt0 % p.W;
     }
-    const int L = p.k + valid;
+    int kb = p.k;  // pool rows of this sequence
+    if (p.k_len) {
+        const int v = p.k_len[b];
+        kb = v < 0 ? 0 : (v > p.k ? p.k : v);
+    }
+    const int L = kb + valid;
     const int c0 = s * p.chunk;
     const int c1 = min(c0 + p.chunk, L);
-    const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, slot0);
+    const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0);
 
     // Ring count: every workgroup of the sequence arrives on a counter as
     // soon as it has read the count (the increment depends on the loaded
@@ -618,7 +624,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
     st.init();
     if constexpr (MF) {
         __shared__ float s_pw[NW][16 * G];
-        mfma_loop<NW, DH, G>(p, b, kvh, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
+        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);

@@ -20,6 +20,7 @@ struct DecodeParams {
     const void *cme_k;        // [B][Hkv][N][Dh]
     const void *cme_v;
     const int32_t *idx;       // [B][k] or nullptr
+    const int32_t *k_len;     // [B] pool rows used per sequence (clamped to [0, k]), or nullptr: all k
     void *win_k;              // [B][Hkv][W][Dh]; written only for rows appended this call
     void *win_v;
     int32_t *win_count;       // [B]; advanced by T_new when T_new > 0
@@ -61,8 +62,12 @@ struct SelectParams {
     const float *sel_keys;    // [B][N][D]
     const float *q_vec;       // [B][D]
     float *scores;            // [B][N]
-    int32_t *idx_out;         // [B][k]
+    int32_t *idx_out;         // [B][idx_stride]
     int B, N, D, k;
+    int idx_stride;           // >= k
+    const int32_t *n_rows;    // [B] candidate rows per sequence, or nullptr: all N
+    const int32_t *q_rows;    // [B] pinned question rows per sequence, or nullptr: none
+    int32_t *k_out;           // [B] entries written per sequence, or nullptr
 };
 constexpr int kSelectMaxN = 32768;
 hipError_t launch_select(const SelectParams &p, hipStream_t stream);

@@ -15,6 +15,11 @@
 // to T in index order (ties go to the earlier document position).  Two
 // block-wide exclusive scans over the threads' contiguous index ranges give
 // each selected row its output slot, so idx comes out ascending.
+//
+// Ragged batches: sequence b has its own candidate count n_b (rows past it
+// score -inf and are never selected), keeps k_b = min(k, n_b) rows, and may
+// pin q_b question rows after them (pool rows n_b .. n_b + q_b - 1, the
+// question's place in the assembled cache [M* || C_local || q]).
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -22,19 +27,28 @@ namespace cmc {
 
 namespace {
 
+__device__ __forceinline__ int clamp_count(int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
+
 template <int R>
 __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
     const int b = blockIdx.y;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int j0 = (blockIdx.x * 4 + wave) * R;
     if (j0 >= p.N) return;  // wave-uniform; no barriers below
+    // Rows past this sequence's count are not candidates: they score -inf
+    // and are not read.
+    const int nb = p.n_rows ? clamp_count(p.n_rows[b], p.N) : p.N;
+    if (j0 >= nb) {
+        if (lane < R && j0 + lane < p.N) p.scores[(size_t)b * p.N + j0 + lane] = -INFINITY;
+        return;
+    }
 
     const int D4 = p.D / 4;
     const float4 *q4 = reinterpret_cast<const float4 *>(p.q_vec + (size_t)b * p.D);
     const float4 *rows[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int j = min(j0 + r, p.N - 1);
+        const int j = min(j0 + r, nb - 1);
         rows[r] = reinterpret_cast<const float4 *>(p.sel_keys + ((size_t)b * p.N + j) * p.D);
     }
     float dot[R], nn[R], qq = 0.f;
@@ -68,7 +82,8 @@ __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
         const float d = lane_reduce<OpSum, 1, kWave>(dot[r]);
         const float n2 = lane_reduce<OpSum, 1, kWave>(nn[r]);
         const int j = j0 + r;
-        if (lane == 0 && j < p.N) p.scores[(size_t)b * p.N + j] = d / (fmaxf(sqrtf(n2), 1e-8f) * qn);
+        if (lane == 0 && j < p.N)
+            p.scores[(size_t)b * p.N + j] = j < nb ? d / (fmaxf(sqrtf(n2), 1e-8f) * qn) : -INFINITY;
     }
 }
 
@@ -117,10 +132,12 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *s_wave) {
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
-    const int N = p.N, k = p.k;
+    const int N = p.N;
+    const int nb = p.n_rows ? clamp_count(p.n_rows[b], N) : N;  // candidates: rows [0, nb)
+    const int k = min(p.k, nb);
     const int per = (N + kTopkThreads - 1) / kTopkThreads;  // <= kPerThread
     const int j0 = tid * per;
-    const int cnt = max(0, min(per, N - j0));
+    const int cnt = max(0, min(per, nb - j0));
 
     __shared__ float s_part[2][kTopkWaves];
     __shared__ int s_wave[kTopkWaves];
@@ -169,26 +186,34 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
         }
     }
     int pos = block_exclusive_scan(take, s_wave);
-    int32_t *out = p.idx_out + (size_t)b * k;
+    int32_t *out = p.idx_out + (size_t)b * p.idx_stride;
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i)
         if (mask & (1u << i)) out[pos++] = j0 + i;
+    // Pinned question rows (pool rows nb, nb+1, ...) follow the selection,
+    // then -1 up to the row stride.
+    const int qb = p.q_rows ? clamp_count(p.q_rows[b], p.idx_stride - k) : 0;
+    for (int t = tid; t < p.idx_stride - k; t += kTopkThreads) out[k + t] = t < qb ? nb + t : -1;
+    if (tid == 0 && p.k_out) p.k_out[b] = k + qb;
 }
 
 }  // namespace
 
 hipError_t launch_select(const SelectParams &p, hipStream_t stream) {
-    if (p.B == 0 || p.N == 0) return hipSuccess;
-    const long long rows = (long long)p.B * p.N;
-    if (rows >= 65536) {
-        dim3 grid((p.N + 15) / 16, p.B);
-        score_kernel<4><<<grid, 256, 0, stream>>>(p);
-    } else {
-        dim3 grid((p.N + 3) / 4, p.B);
-        score_kernel<1><<<grid, 256, 0, stream>>>(p);
+    if (p.B == 0) return hipSuccess;
+    hipError_t e = hipSuccess;
+    if (p.N > 0) {
+        const long long rows = (long long)p.B * p.N;
+        if (rows >= 65536) {
+            dim3 grid((p.N + 15) / 16, p.B);
+            score_kernel<4><<<grid, 256, 0, stream>>>(p);
+        } else {
+            dim3 grid((p.N + 3) / 4, p.B);
+            score_kernel<1><<<grid, 256, 0, stream>>>(p);
+        }
+        e = hipGetLastError();
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.k == 0) return e;
+    if (e != hipSuccess || (p.idx_stride == 0 && !p.k_out)) return e;
     topk_kernel<<<p.B, kTopkThreads, 0, stream>>>(p);
     return hipGetLastError();
 }

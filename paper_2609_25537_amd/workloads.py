@@ -38,6 +38,7 @@ ROLE = {
     "chan": 10,      # log-normal per-channel scale
     "full_k": 11,    # uncompressed-cache baseline keys
     "full_v": 12,    # uncompressed-cache baseline values
+    "ragged": 13,    # per-sequence sizes of a ragged batch
 }
 
 
@@ -54,6 +55,13 @@ class Workload:
     K and V by exp(N(0, chan_sigma^2)) per (kv head, channel).
     ``full_ctx`` > 0 describes an uncompressed-cache baseline of that many
     prefilled tokens.
+
+    Ragged batches (``ragged``): sequence b has a context of ctx_b tokens,
+    drawn log-uniform in [ctx_min, ctx_max]; it has n_b = ceil(ctx_b /
+    ratio) memory rows (N is the largest), keeps k_b = min(k, n_b) of them,
+    pins q_b question rows (uniform in [q_min, q_max]) stored in its pool
+    right after its memory rows, and starts with min(W, ctx_b) tokens in its
+    window.
     """
 
     name: str
@@ -73,6 +81,12 @@ class Workload:
     chan_sigma: float = 0.0
     full_ctx: int = 0
     gap_min: float = 1e-3
+    ragged: bool = False
+    ctx_min: int = 0
+    ctx_max: int = 0
+    ratio: int = 4
+    q_min: int = 0
+    q_max: int = 0
 
     @property
     def G(self) -> int:
@@ -85,6 +99,17 @@ class Workload:
     @property
     def kv_bytes(self) -> int:
         return 2 if self.kv_dtype == "bf16" else 4
+
+    @property
+    def pool_rows(self) -> int:
+        """Rows of each (sequence, kv head) pool: the memory rows plus room
+        for the pinned question rows."""
+        return self.N + self.q_max
+
+    @property
+    def idx_stride(self) -> int:
+        """Entries per index-list row: the selection plus the question rows."""
+        return self.k + self.q_max
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -107,6 +132,12 @@ WORKLOADS: Dict[str, Workload] = {
     "long_wide_d256": Workload("long_wide_d256", B=16, Hq=16, Hkv=16, Dh=256, N=16384,
                                D=3072, k=1024, W=2048, steps=3000, kv_dtype="bf16",
                                kv_std=1.0, seed=404, chan_sigma=1.0),
+    # Ragged Mistral-7B-shaped batch: contexts of 512..16384 tokens at ratio 4
+    # (128..4096 memory rows, some below k), 8..48 pinned question rows.
+    "ragged_batch64": Workload("ragged_batch64", B=64, Hq=32, Hkv=8, Dh=128, N=4096,
+                               D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",
+                               kv_std=1.0 / math.sqrt(128.0), seed=606, ragged=True,
+                               ctx_min=512, ctx_max=16384, ratio=4, q_min=8, q_max=48),
     # 32-layer Llama-shaped decode stack; baseline is a 32768-token full cache.
     "llama_stack32": Workload("llama_stack32", B=32, Hq=32, Hkv=8, Dh=128, N=8192,
                               D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",
@@ -193,14 +224,36 @@ def _kv_rows(w: Workload, role: str, layer: int, b: int, h: int, rows: int,
     return x
 
 
+def ragged_sizes(w: Workload) -> Dict[str, np.ndarray]:
+    """Per-sequence sizes of a ragged batch (int32 [B] each): ctx (context
+    tokens), n_rows (memory rows), q_rows (pinned question rows), fill
+    (initial window tokens).  A uniform workload gets ctx = N * ratio,
+    n_rows = N, q_rows = 0 and fill = W."""
+    if not w.ragged:
+        return {"ctx": np.full(w.B, w.N * w.ratio, np.int32), "n_rows": np.full(w.B, w.N, np.int32),
+                "q_rows": np.zeros(w.B, np.int32), "fill": np.full(w.B, w.W, np.int32)}
+    r = _rng(w.seed, "ragged")
+    u = r.random(w.B)
+    ctx = np.exp(math.log(w.ctx_min) + u * (math.log(w.ctx_max) - math.log(w.ctx_min)))
+    ctx = np.clip(np.round(ctx), w.ctx_min, w.ctx_max).astype(np.int64)
+    n_rows = np.minimum((ctx + w.ratio - 1) // w.ratio, w.N)
+    q_rows = r.integers(w.q_min, w.q_max + 1, size=w.B)
+    fill = np.minimum(ctx, w.W)
+    return {"ctx": ctx.astype(np.int32), "n_rows": n_rows.astype(np.int32),
+            "q_rows": q_rows.astype(np.int32), "fill": fill.astype(np.int32)}
+
+
 def pool_kv(w: Workload, layer: int = 0, b: Optional[int] = None,
             h: Optional[int] = None, rows: Optional[int] = None):
-    """Tier-1 pool K and V, [B][Hkv][N][Dh] (or one sequence / one head).
+    """Tier-1 pool K and V, [B][Hkv][pool_rows][Dh] (or one sequence / one
+    head): memory rows, then (ragged workloads) room for question rows, all
+    drawn from one stream per (sequence, head), so the first N rows do not
+    depend on the room added after them.
 
-    ``rows`` overrides N (the uncompressed baseline uses the same layout
+    ``rows`` overrides that (the uncompressed baseline uses the same layout
     with ``full_ctx`` rows and its own roles).
     """
-    n = w.N if rows is None else rows
+    n = w.pool_rows if rows is None else rows
     rk, rv = ("cme_k", "cme_v") if rows is None else ("full_k", "full_v")
     s = chan_scale(w, layer)
     bs = range(w.B) if b is None else [b]
@@ -214,22 +267,28 @@ def pool_kv(w: Workload, layer: int = 0, b: Optional[int] = None,
     return _kv_cast(w, K), _kv_cast(w, V)
 
 
-def window_kv(w: Workload, layer: int = 0, fill: Optional[int] = None):
+def window_kv(w: Workload, layer: int = 0, fill=None):
     """Initial Tier-2 ring [B][Hkv][W][Dh] and its count [B] (int32).
 
-    The ring starts holding ``fill`` prefilled tokens (default: full, W) in
-    slots 0..fill-1; unused slots are zero.
+    Sequence b's ring starts holding fill_b prefilled tokens in slots
+    0..fill_b-1 (unused slots are zero).  ``fill`` is one count for every
+    sequence or one per sequence; by default the ring is full (W), or, for
+    a ragged workload, holds min(W, ctx_b) tokens.
     """
-    f = w.W if fill is None else fill
+    if fill is None:
+        fills = ragged_sizes(w)["fill"]
+    else:
+        fills = np.broadcast_to(np.asarray(fill, np.int32), (w.B,))
     s = chan_scale(w, layer)
     K = np.zeros((w.B, w.Hkv, w.W, w.Dh), np.float32)
     V = np.zeros((w.B, w.Hkv, w.W, w.Dh), np.float32)
     for b in range(w.B):
+        f = int(fills[b])
         for h in range(w.Hkv):
             if f:
                 K[b, h, :f] = _kv_rows(w, "win_k", layer, b, h, f, s)
                 V[b, h, :f] = _kv_rows(w, "win_v", layer, b, h, f, s)
-    count = np.full((w.B,), f, np.int32)
+    count = np.array(fills, np.int32)
     return _kv_cast(w, K), _kv_cast(w, V), count
 
 
@@ -261,7 +320,7 @@ def kv_to_f32(w: Workload, x: np.ndarray) -> np.ndarray:
 # The 32-layer stack (tens of GB of K/V) is drawn directly on the GPU with
 # torch's counter-based generator, one stream per (seed, role, ids) as above.
 # These draws are not bit-identical to the numpy ones; they feed timing
-# runs only (parity for that shape runs a single layer from the numpy
+# runs only (parity for that shape runs one layer from the numpy
 # streams).
 
 def _device_seed(seed: int, role: str, ids: Sequence[int]) -> int:

@@ -397,6 +397,78 @@ def pin_empty_key_list(orc):
     assert not out.any()
 
 
+def pin_select_ragged_brute(orc):
+    """Ragged selection vs exact rational top-k on each sequence's own rows:
+    rows past n_b are made perfect matches (cosine 1) and must still never
+    be chosen; a duplicated row makes a tie inside a prefix; k_b = min(k,
+    n_b); question rows n_b.. follow; -1 pads the row; q_b is clamped to the
+    room left in the row."""
+    rng = np.random.default_rng(41)
+    B, N, D, k, stride = 5, 11, 6, 4, 7
+    keys = rng.standard_normal((B, N, D)).astype(np.float32)
+    q = rng.standard_normal((B, D)).astype(np.float32)
+    n_rows = np.array([11, 6, 0, 3, 8], np.int32)
+    q_rows = np.array([0, 2, 3, 1, 5], np.int32)
+    keys[1, 3] = keys[1, 1]
+    for b in range(B):
+        keys[b, n_rows[b]:] = 10.0 * q[b]
+    idx, k_out = orc.select_ragged(keys, q, n_rows, k, q_rows, stride)
+    for b in range(B):
+        nb = int(n_rows[b])
+        kb = min(k, nb)
+        qb = min(int(q_rows[b]), stride - kb)
+        want = brute.exact_topk(keys[b, :nb], q[b], kb) + list(range(nb, nb + qb))
+        want += [-1] * (stride - len(want))
+        assert idx[b].tolist() == want, (b, idx[b].tolist(), want)
+        assert int(k_out[b]) == kb + qb
+
+
+def pin_select_ragged_uniform(orc):
+    """Every sequence at full length, no question rows: the ragged selection
+    is the uniform one."""
+    rng = np.random.default_rng(42)
+    keys = rng.standard_normal((3, 40, 8)).astype(np.float32)
+    q = rng.standard_normal((3, 8)).astype(np.float32)
+    idx, k_out = orc.select_ragged(keys, q, np.full(3, 40, np.int32), 9)
+    ref, _, _ = orc.select(keys, q, 9)
+    assert (idx == ref).all() and (k_out == 9).all()
+
+
+def pin_decode_ragged_history(orc):
+    """Ragged decode over several steps vs list-history attention with each
+    sequence's own pool rows (k_len clamped into [0, k]) and its own window
+    fill."""
+    rng = np.random.default_rng(43)
+    B, Hq, Hkv, Dh, N, k, W = 3, 4, 2, 8, 10, 6, 4
+    f32 = lambda *sh: rng.standard_normal(sh).astype(np.float32)
+    pk, pv = f32(B, Hkv, N, Dh), f32(B, Hkv, N, Dh)
+    idx = np.stack([np.sort(rng.choice(N, size=k, replace=False)) for _ in range(B)]).astype(np.int32)
+    k_len = np.array([9, 2, -1], np.int32)
+    kb = [6, 2, 0]
+    fill = [4, 1, 0]
+    wk, wv = np.zeros((B, Hkv, W, Dh), np.float32), np.zeros((B, Hkv, W, Dh), np.float32)
+    for b in range(B):
+        wk[b, :, :fill[b]] = f32(Hkv, fill[b], Dh)
+        wv[b, :, :fill[b]] = f32(Hkv, fill[b], Dh)
+    cnt = np.array(fill, np.int32)
+    hist_k = [[[wk[b, h, s] for s in range(fill[b])] for h in range(Hkv)] for b in range(B)]
+    hist_v = [[[wv[b, h, s] for s in range(fill[b])] for h in range(Hkv)] for b in range(B)]
+    scale = 1.0 / math.sqrt(Dh)
+    for step in range(5):
+        nk, nv = f32(B, Hkv, 1, Dh), f32(B, Hkv, 1, Dh)
+        orc.window_append(wk, wv, cnt, nk, nv)
+        for b in range(B):
+            for h in range(Hkv):
+                hist_k[b][h].append(nk[b, h, 0])
+                hist_v[b][h].append(nv[b, h, 0])
+        q = f32(B, Hq, Dh)
+        out = orc.two_tier_decode_ragged(q, pk, pv, idx, k_len, k, wk, wv, cnt, W, scale)
+        for b in range(B):
+            ref = brute.history_attention(q[b], pk[b], pv[b], idx[b, :kb[b]].tolist(), hist_k[b], hist_v[b],
+                                          W, scale)
+            _close(out[b], ref, 1e-12, f"ragged history step {step} b {b}")
+
+
 ALL_PINS = [v for n, v in sorted(globals().items()) if n.startswith("pin_") and callable(v)]
 
 

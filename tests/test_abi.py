@@ -124,3 +124,56 @@ def test_append_validation(kw, code):
 
 def test_append_without_window_is_noop():
     assert _app(W=0, wk=None, wv=None, wc=None, T=5) == cmc.CMC_OK
+
+
+def _sel_r(**kw):
+    a = dict(keys=FAKE, qv=FAKE, n=FAKE, qr=None, B=2, N=64, D=8, k=4, stride=6, idx=FAKE, kout=FAKE,
+             sc=None, ws=FAKE, wsb=1 << 20, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_select_cmes_ragged(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=None), cmc.CMC_ERR_INVALID_ARGUMENT),             # n_rows is required
+    (dict(stride=3), cmc.CMC_ERR_INVALID_ARGUMENT),           # idx_stride < k
+    (dict(idx=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(D=6), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(N=40000), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(wsb=16), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    (dict(qr=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # alignment
+    (dict(kout=FAKE + 8), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(k=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
+])
+def test_select_ragged_validation(kw, code):
+    assert _sel_r(**kw) == code
+    assert cmc.last_error()
+
+
+def test_select_ragged_empty_batch_ok():
+    assert _sel_r(B=0, n=None) == cmc.CMC_OK
+
+
+def _dec_r(step=False, **kw):
+    a = dict(q=FAKE, ck=FAKE, cv=FAKE, idx=FAKE, kl=FAKE, k=4, wk=FAKE, wv=FAKE, wc=FAKE, W=8)
+    if step:
+        a.update(nk=FAKE, nv=FAKE, T=1)
+    a.update(dt=cmc.CMC_BF16, B=1, Hq=8, Hkv=2, Dh=128, N=16, scale=0.1, out=FAKE, ws=FAKE, wsb=1 << 30, s=None)
+    a.update(kw)
+    fn = cmc.lib().cmc_decode_step_ragged if step else cmc.lib().cmc_two_tier_decode_ragged
+    return fn(*a.values())
+
+
+@pytest.mark.parametrize("step", [False, True])
+@pytest.mark.parametrize("kw,code", [
+    (dict(kl=None), cmc.CMC_ERR_INVALID_ARGUMENT),            # k_len is required
+    (dict(kl=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # alignment
+    (dict(Hq=12, Hkv=4), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(k=0, W=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(wsb=64), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+])
+def test_decode_ragged_validation(step, kw, code):
+    assert _dec_r(step=step, **kw) == code
+
+
+def test_decode_step_ragged_needs_new_rows():
+    assert _dec_r(step=True, T=0) == cmc.CMC_ERR_INVALID_ARGUMENT

@@ -69,3 +69,11 @@ def test_full_mistral7b_batch64(orc):
 @pytest.mark.timeout(900)
 def test_full_long_wide_d256(orc):
     _run_full(orc, "long_wide_d256")
+
+
+@pytest.mark.timeout(900)
+def test_full_llama_stack32_layer(orc):
+    """One layer of the 32-layer stack's shape (B=32, 256 (sequence, kv
+    head) pairs: one 8-wave workgroup each) from the numpy streams; the
+    stack benchmark draws its 32 layers on the device instead."""
+    _run_full(orc, "llama_stack32")
