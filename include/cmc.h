@@ -16,6 +16,7 @@
  *   cmc_two_tier_decode  decode attention over [selected rows || window]
  *   cmc_decode_step      append + decode fused into one launch (every step)
  *   *_ragged             the same with per-sequence sizes (ragged batches)
+ *   cmc_locate_window    CME-guided Tier-2 window placement (once per question)
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -110,8 +111,11 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec,
  *                                  idx_stride
  *   k_out      [B] int32           k_b + q_b (the k_len of the ragged decode
  *                                  calls), or NULL
+ *   norms_out  [B][N] fp32         |m_j| of every candidate row (0 past n_b),
+ *                                  from the same pass over the keys, for
+ *                                  cmc_locate_window; or NULL
  *   sel_keys, q_vec, scores_out, workspace: as cmc_select_cmes (N is the row
- *   stride of sel_keys and scores_out)
+ *   stride of sel_keys, scores_out and norms_out)
  *
  * Limits: B >= 0, N >= 0, k >= 0, idx_stride >= k, D >= 4 and D % 4 == 0,
  * N <= 32768.  k may exceed N (then k_b = n_b).  With n_b = N and no question
@@ -121,7 +125,39 @@ cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec,
                                   const int32_t *n_rows, const int32_t *q_rows,
                                   int B, int N, int D, int k, int idx_stride,
                                   int32_t *idx_out, int32_t *k_out, float *scores_out,
+                                  float *norms_out,
                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * CME-guided Tier-2 localization (appendix on Tier-2 window localization:
+ * when the answer offset alpha is not known, take the offset of the chunk
+ * whose CME has the largest norm; the window start then follows the Tier-2
+ * window equation of Sec. 2.5).  Each chunk (segment) contributes
+ * mems_per_chunk consecutive rows of M (Sec. 2.3), so row j belongs to
+ * chunk j / mems_per_chunk.  Offsets are in tokens of the context C.
+ *
+ *   norms        [B][N] fp32   row norms, e.g. norms_out of
+ *                              cmc_select_cmes_ragged; the decision is made
+ *                              on these values
+ *   n_rows       [B] int32     rows of sequence b (clamped into [0, N]), or
+ *                              NULL for all N
+ *   ctx_len      [B] int32     |C| of sequence b, in tokens
+ *   chunk_offset [B][n_chunks] int32  token offset of each chunk in C, or
+ *                              NULL: chunk i starts at i * chunk_tokens
+ *   alpha_out    [B] int32     alpha_b, or NULL
+ *   start_out    [B] int32     start_b = max(0, min(|C| - W, alpha_b - floor(W/2)))
+ *
+ * alpha_b is the offset of the chunk of the row with the largest norm among
+ * the first n_b rows (the lowest row index on ties).  A sequence with no rows
+ * takes the midpoint alpha_b = floor(|C|/2) (the appendix's midpoint
+ * heuristic).  Limits: B, N, W, chunk_tokens >= 0, mems_per_chunk >= 1;
+ * with chunk_offset, n_chunks * mems_per_chunk >= N.  Results are exact
+ * (integer work on the given norms).
+ */
+cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const int32_t *ctx_len,
+                             int B, int N, int mems_per_chunk,
+                             const int32_t *chunk_offset, int n_chunks, int chunk_tokens,
+                             int W, int32_t *alpha_out, int32_t *start_out, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Tier-2 window.                                                           */

@@ -11,7 +11,8 @@ Policy"): ``select`` (Tier-1 cosine score and top-K in document order),
 keeps the cache bounded by K + W + |q|) and ``two_tier_decode`` (softmax
 attention over the assembled cache), plus ``select_ragged`` and
 ``two_tier_decode_ragged`` (the same definitions per sequence, for batches
-whose sequences differ in size).
+whose sequences differ in size), and ``row_norms`` / ``locate`` (CME-guided
+Tier-2 localization, from the appendix on window localization).
 
 ``Oracle(path)`` binds any build of the same source (the tests use it to
 load deliberately mutated builds and show that the pins reject them); the
@@ -75,6 +76,10 @@ class Oracle:
         lib.oracle_two_tier_decode.argtypes = [P, P, P, I, P, I, P, P, P, I,
                                                I, I, I, I, I, ctypes.c_double, P]
         lib.oracle_two_tier_decode.restype = I
+        lib.oracle_row_norms.argtypes = [P, I, I, I, P]
+        lib.oracle_row_norms.restype = I
+        lib.oracle_locate.argtypes = [P, P, I, I, I, P, I, I, P, I, P, P]
+        lib.oracle_locate.restype = I
         lib.oracle_window_start.argtypes = [ctypes.c_longlong] * 3
         lib.oracle_window_start.restype = ctypes.c_longlong
         lib.oracle_num_threads.argtypes = []
@@ -109,6 +114,34 @@ class Oracle:
                                     _ptr(idx), _ptr(scores), _ptr(gap))
         _check(rc, "select")
         return idx, scores, gap
+
+    def row_norms(self, sel_keys: np.ndarray) -> np.ndarray:
+        """||m_j|| of every row, fp64 [B][N]."""
+        keys = np.ascontiguousarray(sel_keys, np.float32)
+        B, N, D = keys.shape
+        out = np.zeros((B, N), np.float64)
+        _check(self.lib.oracle_row_norms(_ptr(keys), B, N, D, _ptr(out)), "row_norms")
+        return out
+
+    def locate(self, norms: np.ndarray, ctx_len: np.ndarray, W: int, mems_per_chunk: int,
+               n_rows: Optional[np.ndarray] = None, chunk_offset: Optional[np.ndarray] = None,
+               chunk_tokens: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+        """CME-guided Tier-2 localization: (alpha [B], start [B]) int32.
+        norms [B][N] (taken as given: the decision is made on these values),
+        ctx_len [B] tokens, chunk_offset [B][n_chunks] or None (chunk i at
+        i * chunk_tokens)."""
+        nr = np.ascontiguousarray(norms, np.float64)
+        B, N = nr.shape
+        ctx = np.ascontiguousarray(ctx_len, np.int32)
+        rows = None if n_rows is None else np.ascontiguousarray(n_rows, np.int32)
+        off = None if chunk_offset is None else np.ascontiguousarray(chunk_offset, np.int32)
+        n_chunks = 0 if off is None else off.shape[1]
+        alpha = np.zeros((B,), np.int32)
+        start = np.zeros((B,), np.int32)
+        rc = self.lib.oracle_locate(_ptr(nr), _ptr(rows), B, N, int(mems_per_chunk), _ptr(off), n_chunks,
+                                    int(chunk_tokens), _ptr(ctx), int(W), _ptr(alpha), _ptr(start))
+        _check(rc, "locate")
+        return alpha, start
 
     def window_start(self, ctx_len: int, W: int, alpha: int) -> int:
         """Tier-2 window start, max(0, min(|C| - W, alpha - floor(W/2)))."""
@@ -258,3 +291,11 @@ def select_ragged(sel_keys, q_vec, n_rows, k, q_rows=None, idx_stride=None):
 
 def two_tier_decode_ragged(q, cme_k, cme_v, idx, k_len, k, win_k, win_v, win_count, W, scale):
     return default().two_tier_decode_ragged(q, cme_k, cme_v, idx, k_len, k, win_k, win_v, win_count, W, scale)
+
+
+def row_norms(sel_keys):
+    return default().row_norms(sel_keys)
+
+
+def locate(norms, ctx_len, W, mems_per_chunk, n_rows=None, chunk_offset=None, chunk_tokens=0):
+    return default().locate(norms, ctx_len, W, mems_per_chunk, n_rows, chunk_offset, chunk_tokens)

@@ -19,7 +19,9 @@
  *   - decode attention is ordinary softmax attention with z = scale * <q,k>
  *     over the explicit key list [pool rows idx[0..k-1]] ++ [ring slots
  *     0..min(count,W)-1]; query head h reads kv head h / (Hq/Hkv); an empty
- *     key list yields a zero output row.
+ *     key list yields a zero output row;
+ *   - CME-guided localization works in token offsets; a sequence with no
+ *     memory rows falls back to the midpoint floor(|C|/2).
  *
  * Parity pins: tests check this file against exact-rational ranking,
  * list-history attention written without ring arithmetic, a library SDPA
@@ -213,6 +215,70 @@ int oracle_window_append(void *win_k, void *win_v, int elem_bytes, int32_t *win_
             }
         }
         win_count[b] = c + T_new;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* CME-guided Tier-2 localization (appendix on Tier-2 window           */
+/* localization: alpha is the offset of the chunk that produced the    */
+/* highest-norm CME; the midpoint heuristic uses alpha = |C|/2).  Each */
+/* segment contributes m^(c) consecutive rows of M (Sec. 2.3).         */
+/* ------------------------------------------------------------------ */
+
+/* norms_out[b][j] = ||m_j||_2 of sel_keys[b][j][:]. */
+int oracle_row_norms(const float *sel_keys, int B, int N, int D, double *norms_out)
+{
+    if (B < 0 || N < 0 || D < 1)
+        return ORACLE_BAD_ARG;
+    #pragma omp parallel for schedule(static)
+    for (long long r = 0; r < (long long)B * N; ++r) {
+        const float *m = sel_keys + (size_t)r * D;
+        double s = 0.0;
+        for (int d = 0; d < D; ++d)
+            s += (double)m[d] * (double)m[d];
+        norms_out[r] = sqrt(s);
+    }
+    return ORACLE_OK;
+}
+
+/*
+ * Per sequence b (norms [B][N], any non-negative values):
+ *   n_b = n_rows[b] clamped into [0, N] (all N rows when n_rows is NULL);
+ *   j*  = the row j < n_b with the largest norm, the lowest such j on ties;
+ *   the chunk of j* is j* / mems_per_chunk;
+ *   alpha = chunk_offset[b][chunk] (chunk * chunk_tokens when chunk_offset is
+ *           NULL); a sequence with no rows takes the midpoint floor(|C|/2);
+ *   start = max(0, min(|C| - W, alpha - floor(W/2))) with |C| = ctx_len[b].
+ * chunk_offset, when given, is [B][n_chunks] with n_chunks * mems_per_chunk
+ * >= N.
+ */
+int oracle_locate(const double *norms, const int32_t *n_rows, int B, int N, int mems_per_chunk,
+                  const int32_t *chunk_offset, int n_chunks, int chunk_tokens,
+                  const int32_t *ctx_len, int W, int32_t *alpha_out, int32_t *start_out)
+{
+    if (B < 0 || N < 0 || mems_per_chunk < 1 || W < 0 || chunk_tokens < 0)
+        return ORACLE_BAD_ARG;
+    if (chunk_offset && (long long)n_chunks * mems_per_chunk < N)
+        return ORACLE_BAD_ARG;
+    for (int b = 0; b < B; ++b) {
+        int nb = n_rows ? n_rows[b] : N;
+        if (nb < 0) nb = 0;
+        if (nb > N) nb = N;
+        long long alpha;
+        if (nb == 0) {
+            alpha = ctx_len[b] / 2;
+        } else {
+            int best = 0;
+            for (int j = 1; j < nb; ++j)
+                if (norms[(size_t)b * N + j] > norms[(size_t)b * N + best])
+                    best = j;
+            int chunk = best / mems_per_chunk;
+            alpha = chunk_offset ? chunk_offset[(size_t)b * n_chunks + chunk]
+                                 : (long long)chunk * chunk_tokens;
+        }
+        alpha_out[b] = (int32_t)alpha;
+        start_out[b] = (int32_t)oracle_window_start(ctx_len[b], W, alpha);
     }
     return ORACLE_OK;
 }

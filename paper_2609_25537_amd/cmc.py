@@ -32,8 +32,8 @@ CMC_BF16 = 1
 EXPORTED = [
     "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_window_append",
     "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
-    "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_status_string", "cmc_last_error",
-    "cmc_version",
+    "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_status_string",
+    "cmc_last_error", "cmc_version",
 ]
 
 
@@ -71,7 +71,10 @@ def lib() -> ctypes.CDLL:
         L.cmc_decode_step.argtypes = [P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
                                       ctypes.c_float, P, P, SZ, P]
         L.cmc_decode_step.restype = I
-        L.cmc_select_cmes_ragged.argtypes = [P, P, P, P, I, I, I, I, I, P, P, P, P, SZ, P]
+        L.cmc_select_cmes_ragged.argtypes = [P, P, P, P, I, I, I, I, I, P, P, P, P, P, SZ, P]
+        L.cmc_select_cmes_ragged.restype = I
+        L.cmc_locate_window.argtypes = [P, P, P, I, I, I, P, I, I, I, P, P, P]
+        L.cmc_locate_window.restype = I
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_two_tier_decode_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
                                                  ctypes.c_float, P, P, SZ, P]
@@ -171,7 +174,8 @@ def cmc_select_cmes(sel_keys, q_vec, k: int, idx_out=None, scores_out=None, work
 
 
 def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_stride: Optional[int] = None,
-                           idx_out=None, k_out=None, scores_out=None, workspace=None, stream=None):
+                           idx_out=None, k_out=None, scores_out=None, norms_out=None, workspace=None,
+                           stream=None):
     """Ragged Tier-1 selection: sequence b's candidates are its first
     n_rows[b] rows; q_rows[b] pinned question rows (pool rows n_b ..) follow
     the selected ones.  n_rows/q_rows [B] int32 (device).  Returns
@@ -195,6 +199,9 @@ def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_str
     _need(k_out.shape == (B,) and k_out.dtype == torch.int32, "k_out [B] int32")
     if scores_out is not None:
         _need(scores_out.shape == (B, N) and scores_out.dtype == torch.float32, "scores_out [B][N] fp32")
+    if norms_out is not None:
+        _need(norms_out.shape == (B, N) and norms_out.dtype == torch.float32 and norms_out.is_contiguous(),
+              "norms_out [B][N] fp32")
     ws_bytes = 0
     if scores_out is None and workspace is None:
         workspace = torch.empty(max(1, cmc_select_workspace_bytes(B, N)), dtype=torch.uint8, device=dev)
@@ -202,9 +209,38 @@ def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_str
         ws_bytes = workspace.numel() * workspace.element_size()
     rc = lib().cmc_select_cmes_ragged(_ptr(sel_keys), _ptr(q_vec), _ptr(n_rows), _ptr(q_rows), B, N, D,
                                       int(k), stride, _ptr(idx_out), _ptr(k_out), _ptr(scores_out),
-                                      _ptr(workspace), ws_bytes, _stream(stream))
+                                      _ptr(norms_out), _ptr(workspace), ws_bytes, _stream(stream))
     _check(rc)
     return idx_out, k_out
+
+
+def cmc_locate_window(norms, ctx_len, W: int, mems_per_chunk: int, n_rows=None, chunk_offset=None,
+                      chunk_tokens: int = 0, alpha_out=None, start_out=None, stream=None):
+    """CME-guided Tier-2 window placement.  norms [B][N] fp32, ctx_len [B]
+    int32, chunk_offset [B][n_chunks] int32 or None (chunk i at i *
+    chunk_tokens).  Returns (alpha [B], start [B]) int32."""
+    import torch
+    _need(norms.dim() == 2 and norms.dtype == torch.float32 and norms.is_contiguous(), "norms [B][N] fp32")
+    B, N = norms.shape
+    _need(ctx_len.shape == (B,) and ctx_len.dtype == torch.int32 and ctx_len.is_contiguous(), "ctx_len [B] int32")
+    if n_rows is not None:
+        _need(n_rows.shape == (B,) and n_rows.dtype == torch.int32 and n_rows.is_contiguous(), "n_rows [B] int32")
+    n_chunks = 0
+    if chunk_offset is not None:
+        _need(chunk_offset.dim() == 2 and chunk_offset.shape[0] == B and chunk_offset.dtype == torch.int32
+              and chunk_offset.is_contiguous(), "chunk_offset [B][n_chunks] int32")
+        n_chunks = int(chunk_offset.shape[1])
+    if alpha_out is None:
+        alpha_out = torch.empty((B,), dtype=torch.int32, device=norms.device)
+    if start_out is None:
+        start_out = torch.empty((B,), dtype=torch.int32, device=norms.device)
+    _need(alpha_out.shape == (B,) and start_out.shape == (B,) and alpha_out.dtype == start_out.dtype == torch.int32,
+          "alpha_out/start_out [B] int32")
+    rc = lib().cmc_locate_window(_ptr(norms), _ptr(n_rows), _ptr(ctx_len), B, N, int(mems_per_chunk),
+                                 _ptr(chunk_offset), n_chunks, int(chunk_tokens), int(W), _ptr(alpha_out),
+                                 _ptr(start_out), _stream(stream))
+    _check(rc)
+    return alpha_out, start_out
 
 
 # ---------------------------------------------------------------- window

@@ -154,7 +154,7 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int
                         workspace ? workspace_bytes : (size_t)0);
         scores = static_cast<float *>(workspace);
     }
-    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, k, nullptr, nullptr, nullptr};
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, k, nullptr, nullptr, nullptr, nullptr};
     hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
@@ -162,8 +162,8 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int
 
 cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, const int32_t *n_rows,
                                   const int32_t *q_rows, int B, int N, int D, int k, int idx_stride,
-                                  int32_t *idx_out, int32_t *k_out, float *scores_out, void *workspace,
-                                  size_t workspace_bytes, void *stream) {
+                                  int32_t *idx_out, int32_t *k_out, float *scores_out, float *norms_out,
+                                  void *workspace, size_t workspace_bytes, void *stream) {
     if (B < 0 || N < 0 || k < 0 || D < 4)
         return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: need B >= 0, N >= 0, k >= 0, D >= 4 (got B=%d N=%d k=%d D=%d)", B, N, k, D);
     if (idx_stride < k)
@@ -178,7 +178,8 @@ cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, con
     if (idx_stride > 0 && !idx_out)
         return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: idx_out must be non-null when idx_stride > 0");
     if (misaligned(sel_keys) || misaligned(q_vec) || misaligned(n_rows) || misaligned(q_rows) ||
-        misaligned(idx_out) || misaligned(k_out) || misaligned(scores_out) || misaligned(workspace))
+        misaligned(idx_out) || misaligned(k_out) || misaligned(scores_out) || misaligned(norms_out) ||
+        misaligned(workspace))
         return fail(CMC_ERR_UNSUPPORTED, "select_ragged: every pointer must be 16-byte aligned");
     float *scores = scores_out;
     if (!scores && N > 0) {
@@ -188,9 +189,33 @@ cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, con
                         need, workspace ? workspace_bytes : (size_t)0);
         scores = static_cast<float *>(workspace);
     }
-    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, idx_stride, n_rows, q_rows, k_out};
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, idx_stride, n_rows, q_rows, k_out,
+                        norms_out};
     hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select_ragged launch");
+    return ok();
+}
+
+cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const int32_t *ctx_len, int B, int N,
+                             int mems_per_chunk, const int32_t *chunk_offset, int n_chunks, int chunk_tokens,
+                             int W, int32_t *alpha_out, int32_t *start_out, void *stream) {
+    if (B < 0 || N < 0 || mems_per_chunk < 1 || W < 0 || chunk_tokens < 0 || n_chunks < 0)
+        return fail(CMC_ERR_INVALID_ARGUMENT,
+                    "locate: need B, N, W, chunk_tokens, n_chunks >= 0 and mems_per_chunk >= 1");
+    if (chunk_offset && (long long)n_chunks * mems_per_chunk < N)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "locate: n_chunks=%d chunks of %d rows do not cover N=%d", n_chunks,
+                    mems_per_chunk, N);
+    if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "locate: B=%d exceeds 65535", B);
+    if (B == 0) return ok();
+    if (!ctx_len || !start_out || (N > 0 && !norms))
+        return fail(CMC_ERR_INVALID_ARGUMENT, "locate: norms, ctx_len and start_out must be non-null");
+    if (misaligned(norms) || misaligned(n_rows) || misaligned(ctx_len) || misaligned(chunk_offset) ||
+        misaligned(alpha_out) || misaligned(start_out))
+        return fail(CMC_ERR_UNSUPPORTED, "locate: every pointer must be 16-byte aligned");
+    cmc::LocateParams p{norms, n_rows, chunk_offset, ctx_len, alpha_out, start_out,
+                        B, N, mems_per_chunk, n_chunks, chunk_tokens, W};
+    hipError_t e = cmc::launch_locate(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "locate launch");
     return ok();
 }
 

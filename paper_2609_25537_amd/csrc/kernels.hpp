@@ -68,8 +68,20 @@ struct SelectParams {
     const int32_t *n_rows;    // [B] candidate rows per sequence, or nullptr: all N
     const int32_t *q_rows;    // [B] pinned question rows per sequence, or nullptr: none
     int32_t *k_out;           // [B] entries written per sequence, or nullptr
+    float *norms;             // [B][N] row norms |m_j| (0 past n_b), or nullptr
 };
 constexpr int kSelectMaxN = 32768;
 hipError_t launch_select(const SelectParams &p, hipStream_t stream);
+
+struct LocateParams {
+    const float *norms;         // [B][N]
+    const int32_t *n_rows;      // [B] or nullptr: all N
+    const int32_t *chunk_offset;  // [B][n_chunks] or nullptr: chunk i at i * chunk_tokens
+    const int32_t *ctx_len;     // [B]
+    int32_t *alpha_out;         // [B] or nullptr
+    int32_t *start_out;         // [B]
+    int B, N, mems_per_chunk, n_chunks, chunk_tokens, W;
+};
+hipError_t launch_locate(const LocateParams &p, hipStream_t stream);
 
 }  // namespace cmc

@@ -20,6 +20,8 @@
 // score -inf and are never selected), keeps k_b = min(k, n_b) rows, and may
 // pin q_b question rows after them (pool rows n_b .. n_b + q_b - 1, the
 // question's place in the assembled cache [M* || C_local || q]).
+#include <limits.h>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -39,7 +41,10 @@ __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
     // and are not read.
     const int nb = p.n_rows ? clamp_count(p.n_rows[b], p.N) : p.N;
     if (j0 >= nb) {
-        if (lane < R && j0 + lane < p.N) p.scores[(size_t)b * p.N + j0 + lane] = -INFINITY;
+        if (lane < R && j0 + lane < p.N) {
+            p.scores[(size_t)b * p.N + j0 + lane] = -INFINITY;
+            if (p.norms) p.norms[(size_t)b * p.N + j0 + lane] = 0.f;
+        }
         return;
     }
 
@@ -82,8 +87,11 @@ __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
         const float d = lane_reduce<OpSum, 1, kWave>(dot[r]);
         const float n2 = lane_reduce<OpSum, 1, kWave>(nn[r]);
         const int j = j0 + r;
-        if (lane == 0 && j < p.N)
-            p.scores[(size_t)b * p.N + j] = j < nb ? d / (fmaxf(sqrtf(n2), 1e-8f) * qn) : -INFINITY;
+        if (lane == 0 && j < p.N) {
+            const float mn = sqrtf(n2);
+            p.scores[(size_t)b * p.N + j] = j < nb ? d / (fmaxf(mn, 1e-8f) * qn) : -INFINITY;
+            if (p.norms) p.norms[(size_t)b * p.N + j] = j < nb ? mn : 0.f;
+        }
     }
 }
 
@@ -197,7 +205,73 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     if (tid == 0 && p.k_out) p.k_out[b] = k + qb;
 }
 
+// CME-guided Tier-2 localization: one 256-thread workgroup per sequence
+// finds the row with the largest norm among its n_b rows (lowest index on
+// ties), maps it to its chunk and the chunk's token offset alpha, and
+// applies the window equation.  A sequence without rows takes the midpoint.
+__global__ __launch_bounds__(256) void locate_kernel(LocateParams p) {
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nb = p.n_rows ? clamp_count(p.n_rows[b], p.N) : p.N;
+    const float *nr = p.norms + (size_t)b * p.N;
+    float best = -INFINITY;
+    int bj = INT_MAX;
+    for (int j = tid; j < nb; j += 256) {
+        const float v = nr[j];
+        if (v > best) {  // strided ascending scan: the first maximum is kept
+            best = v;
+            bj = j;
+        }
+    }
+    // (max value, then min index) across the wave, then across the 4 waves
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const float ov = __shfl_xor(best, off);
+        const int oj = __shfl_xor(bj, off);
+        if (ov > best || (ov == best && oj < bj)) {
+            best = ov;
+            bj = oj;
+        }
+    }
+    __shared__ float s_v[4];
+    __shared__ int s_j[4];
+    if (lane == 0) {
+        s_v[wave] = best;
+        s_j[wave] = bj;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < 4; ++w) {
+            if (s_v[w] > best || (s_v[w] == best && s_j[w] < bj)) {
+                best = s_v[w];
+                bj = s_j[w];
+            }
+        }
+        const long long ctx = p.ctx_len[b];
+        long long alpha;
+        if (nb == 0) {
+            alpha = ctx / 2;
+        } else {
+            if (bj >= nb) bj = 0;  // no comparable value (NaN norms): keeps the read in bounds
+            const int chunk = bj / p.mems_per_chunk;
+            alpha = p.chunk_offset ? (long long)p.chunk_offset[(size_t)b * p.n_chunks + chunk]
+                                   : (long long)chunk * p.chunk_tokens;
+        }
+        long long start = alpha - p.W / 2;
+        if (start > ctx - p.W) start = ctx - p.W;
+        if (start < 0) start = 0;
+        if (p.alpha_out) p.alpha_out[b] = (int32_t)alpha;
+        p.start_out[b] = (int32_t)start;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_locate(const LocateParams &p, hipStream_t stream) {
+    if (p.B == 0) return hipSuccess;
+    locate_kernel<<<p.B, 256, 0, stream>>>(p);
+    return hipGetLastError();
+}
 
 hipError_t launch_select(const SelectParams &p, hipStream_t stream) {
     if (p.B == 0) return hipSuccess;

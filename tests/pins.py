@@ -469,6 +469,56 @@ def pin_decode_ragged_history(orc):
             _close(out[b], ref, 1e-12, f"ragged history step {step} b {b}")
 
 
+def pin_row_norms_library(orc):
+    """Row norms vs numpy's own norm routine."""
+    rng = np.random.default_rng(51)
+    keys = rng.standard_normal((3, 17, 9)).astype(np.float32)
+    keys[1, 4] = 0.0
+    ref = np.linalg.norm(keys.astype(np.float64), axis=2)
+    _close(orc.row_norms(keys), ref, 1e-12, "row norms")
+
+
+def pin_locate_cases(orc):
+    """CME-guided localization on hand-checked cases: the largest norm's
+    chunk (mems_per_chunk rows per chunk) gives alpha from the offset table
+    or from chunk * chunk_tokens; ties go to the earlier row; rows past n_b
+    are ignored even when their norm is larger; a sequence without rows
+    takes the midpoint; the window start then follows the window equation,
+    checked here by its defining properties."""
+    norms = np.array([
+        [1.0, 2.0, 7.0, 7.0, 3.0, 0.5],    # rows 2 and 3 tie -> row 2 -> chunk 1 (m=2)
+        [9.0, 1.0, 1.0, 1.0, 1.0, 8.0],    # row 0 -> chunk 0
+        [1.0, 2.0, 3.0, 4.0, 5.0, 99.0],   # n_b = 5: row 5 ignored -> row 4 -> chunk 2
+        [5.0, 5.0, 5.0, 5.0, 5.0, 5.0],    # n_b = 0 -> midpoint
+    ])
+    n_rows = np.array([6, 6, 5, 0], np.int32)
+    ctx = np.array([1000, 50, 400, 301], np.int32)
+    offsets = np.array([[0, 333, 666], [0, 20, 40], [10, 120, 390], [0, 1, 2]], np.int32)
+    W = 100
+    alpha, start = orc.locate(norms, ctx, W, 2, n_rows=n_rows, chunk_offset=offsets)
+    assert alpha.tolist() == [333, 0, 390, 150], alpha.tolist()
+    # window start: centred on alpha when that fits, else flush with an end
+    assert start.tolist() == [283, 0, 300, 100], start.tolist()
+    alpha2, _ = orc.locate(norms, ctx, W, 2, n_rows=n_rows, chunk_tokens=64)
+    assert alpha2.tolist() == [64, 0, 128, 150], alpha2.tolist()
+    alpha3, _ = orc.locate(norms, ctx, W, 1, chunk_tokens=10)   # one row per chunk, all rows
+    assert alpha3.tolist() == [20, 0, 50, 0], alpha3.tolist()
+
+
+def pin_locate_argmax_library(orc):
+    """Random norms with planted ties: the chosen row is numpy's argmax
+    (first occurrence) of the row's prefix."""
+    rng = np.random.default_rng(52)
+    B, N, m = 6, 40, 4
+    norms = rng.integers(0, 12, size=(B, N)).astype(np.float64)  # many exact ties
+    n_rows = np.array([40, 13, 1, 0, 39, 4], np.int32)
+    ctx = np.full(B, 10000, np.int32)
+    alpha, _ = orc.locate(norms, ctx, 64, m, n_rows=n_rows, chunk_tokens=1)
+    for b in range(B):
+        want = ctx[b] // 2 if n_rows[b] == 0 else int(np.argmax(norms[b, :n_rows[b]])) // m
+        assert alpha[b] == want, (b, alpha[b], want)
+
+
 ALL_PINS = [v for n, v in sorted(globals().items()) if n.startswith("pin_") and callable(v)]
 
 

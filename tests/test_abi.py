@@ -128,7 +128,7 @@ def test_append_without_window_is_noop():
 
 def _sel_r(**kw):
     a = dict(keys=FAKE, qv=FAKE, n=FAKE, qr=None, B=2, N=64, D=8, k=4, stride=6, idx=FAKE, kout=FAKE,
-             sc=None, ws=FAKE, wsb=1 << 20, s=None)
+             sc=None, nrm=None, ws=FAKE, wsb=1 << 20, s=None)
     a.update(kw)
     return cmc.lib().cmc_select_cmes_ragged(*a.values())
 
@@ -142,6 +142,7 @@ def _sel_r(**kw):
     (dict(wsb=16), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
     (dict(qr=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # alignment
     (dict(kout=FAKE + 8), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(nrm=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),
     (dict(k=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
 ])
 def test_select_ragged_validation(kw, code):
@@ -177,3 +178,27 @@ def test_decode_ragged_validation(step, kw, code):
 
 def test_decode_step_ragged_needs_new_rows():
     assert _dec_r(step=True, T=0) == cmc.CMC_ERR_INVALID_ARGUMENT
+
+
+def _loc(**kw):
+    a = dict(nrm=FAKE, n=None, ctx=FAKE, B=2, N=64, m=4, off=FAKE, nch=16, ct=0, W=32, al=FAKE, st=FAKE, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_locate_window(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(m=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(nch=15), cmc.CMC_ERR_INVALID_ARGUMENT),             # chunks do not cover N rows
+    (dict(W=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(ctx=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(st=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(nrm=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(off=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(B=70000), cmc.CMC_ERR_UNSUPPORTED),
+])
+def test_locate_validation(kw, code):
+    assert _loc(**kw) == code
+
+
+def test_locate_empty_batch_ok():
+    assert _loc(B=0, nrm=None, ctx=None, st=None) == cmc.CMC_OK

@@ -42,6 +42,13 @@ MUTANTS = [
     ("window_row_stride", "row[k + s] = (((size_t)b * Hkv + kv) * W + (size_t)s) * Dh;",
      "row[k + s] = (((size_t)b * Hkv + kv) * W + (size_t)(valid - 1 - s) / 2) * Dh;"),
     ("bf16_widening", "uint32_t u = ((uint32_t)h) << 16;", "uint32_t u = ((uint32_t)h) << 15;"),
+    ("locate_tie_to_later_row", "if (norms[(size_t)b * N + j] > norms[(size_t)b * N + best])",
+     "if (norms[(size_t)b * N + j] >= norms[(size_t)b * N + best])"),
+    ("locate_row_not_chunk", "int chunk = best / mems_per_chunk;", "int chunk = best;"),
+    ("locate_chunk_modulo", "int chunk = best / mems_per_chunk;", "int chunk = best % mems_per_chunk;"),
+    ("locate_all_rows", "if (nb > N) nb = N;", "nb = N;"),
+    ("locate_no_midpoint", "alpha = ctx_len[b] / 2;", "alpha = 0;"),
+    ("row_norm_squared", "norms_out[r] = sqrt(s);", "norms_out[r] = s;"),
 ]
 
 
