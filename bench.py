@@ -464,6 +464,8 @@ def main():
 
     cmc.lib()  # fail loudly before any work if the HIP library is missing
     dev = torch.device("cuda:0")
+    if args.workload in wl.DENOISE_WORKLOADS:
+        return main_denoise(args, wl.DENOISE_WORKLOADS[args.workload], dev)
     w = wl.get(args.workload)
     if w.layers != 1:
         return main_stack(args, w, dev)
@@ -535,6 +537,97 @@ def main():
                    **({"ragged": {"ctx_tokens": [w.ctx_min, w.ctx_max], "ratio": w.ratio,
                                   "question_rows": [w.q_min, w.q_max]}} if w.ragged else {})},
         "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    txt = json.dumps(line)
+    print(txt, flush=True)
+    if args.out:
+        with open(args.out, "a") as f:
+            f.write(txt + "\n")
+
+
+def denoise_bytes(w, n_tokens) -> int:
+    """Algorithmic bytes of one cmc_denoise call: every embedding row of
+    every sequence read once, the Eq. 3 byte written and read back, the kept
+    positions written (4 bytes per position of the [B][n] list)."""
+    tok = int(np.sum(n_tokens))
+    return tok * w.H * w.elem_bytes + 2 * w.B * w.n + 4 * w.B * w.n
+
+
+def denoise_cpu_baseline(w, n_tokens, budget_s: float):
+    """The oracle on whole sequences until the budget is spent; tokens/s."""
+    import oracle
+    from paper_2609_25537_amd import workloads as wl
+    orc = oracle.default()
+    done_tok, t = 0, 0.0
+    b = 0
+    while b < w.B and (b < 1 or t < budget_s):
+        e = wl.denoise_emb(w, b)[None]
+        nt = n_tokens[b:b + 1]
+        t0 = time.perf_counter()
+        mc = orc.denoise_scores(e, w.g, nt)
+        orc.denoise_select(mc, w.tau, w.keep_min_every, nt, w.chunk_tokens)
+        t += time.perf_counter() - t0
+        done_tok += int(nt[0])
+        b += 1
+    return {"value": done_tok / t, "unit": "tokens/s", "cores": orc.num_threads(), "kind": "oracle",
+            "sample": f"{b} of {w.B} contexts ({done_tok} tokens, {t:.2f} s)"}
+
+
+def main_denoise(args, w, dev):
+    """Graph-based context denoising of a batch of contexts: one step is one
+    cmc_denoise call (statistic + Eq. 3 + floor + compaction + chunk
+    offsets) over all B contexts, inputs resident in HBM."""
+    import torch
+    from paper_2609_25537_amd import cmc
+    from paper_2609_25537_amd import workloads as wl
+    n_tokens = wl.denoise_tokens(w)
+    emb = to_dev(wl.denoise_emb(w), dev)
+    nt = to_dev(n_tokens, dev)
+    kept_idx = torch.empty((w.B, w.n), dtype=torch.int32, device=dev)
+    kept_count = torch.empty((w.B,), dtype=torch.int32, device=dev)
+    nch = -(-w.n // w.chunk_tokens)
+    chunk_offset = torch.empty((w.B, nch), dtype=torch.int32, device=dev)
+    n_chunks = torch.empty((w.B,), dtype=torch.int32, device=dev)
+    ws = torch.empty(max(1, cmc.cmc_denoise_workspace_bytes(w.B, w.n)), dtype=torch.uint8, device=dev)
+
+    def call():
+        cmc.cmc_denoise(emb, g=w.g, tau=w.tau, keep_min_every=w.keep_min_every, n_tokens=nt,
+                        chunk_tokens=w.chunk_tokens, kept_idx=kept_idx, kept_count=kept_count,
+                        chunk_offset=chunk_offset, n_chunks_out=n_chunks, workspace=ws)
+
+    reps = max(1, args.launch_reps // 10)
+    g = capture(lambda: [call() for _ in range(reps)])
+    for _ in range(args.warmup):
+        g.replay()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(args.steps):
+        g.replay()
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    calls = args.steps * reps
+    t_call = ms * 1e-3 / calls
+    tok = int(n_tokens.sum())
+    nbytes = denoise_bytes(w, n_tokens)
+    achieved = nbytes / t_call / 1e9
+    kept = int(kept_count.sum().item())
+    cpu = None if args.no_cpu_baseline else denoise_cpu_baseline(w, n_tokens, args.cpu_seconds)
+    line = {
+        "metric": "denoised context tokens/s and achieved HBM GB/s (% of MI355X peak)",
+        "value": round(tok * calls / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": calls,
+        "warmup": args.warmup, "ms_per_step": round(ms / calls, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "n_max": w.n, "tokens": tok, "H": w.H, "g": w.g, "tau": w.tau,
+                   "keep_min_every": w.keep_min_every, "chunk_tokens": w.chunk_tokens, "graph": True,
+                   "retention": round(kept / tok, 4)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "denoise_score_kernel + denoise_select_kernel (one cmc_denoise call)",
+                     "bytes_per_launch": nbytes, "launch_us": round(t_call * 1e6, 3)},
         "cpu_baseline": cpu,
     }
     txt = json.dumps(line)

@@ -17,6 +17,8 @@
  *   cmc_decode_step      append + decode fused into one launch (every step)
  *   *_ragged             the same with per-sequence sizes (ragged batches)
  *   cmc_locate_window    CME-guided Tier-2 window placement (once per question)
+ *   cmc_denoise          graph-based context denoising before compression
+ *                        (Sec. 2.1, once per context)
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -158,6 +160,51 @@ cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const in
                              int B, int N, int mems_per_chunk,
                              const int32_t *chunk_offset, int n_chunks, int chunk_tokens,
                              int W, int32_t *alpha_out, int32_t *start_out, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Context denoising.                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of workspace cmc_denoise needs (one byte per token); 0 for invalid
+ * sizes or B*n == 0. */
+size_t cmc_denoise_workspace_bytes(int B, int n);
+
+/*
+ * Graph-based context denoising (Sec. 2.1, Eq. 3, with the minimum keep
+ * interval of the hyper-parameter table): token i of sequence b is kept when
+ *   max over j = i+1 .. min(i+g, n_b-1) of e_i.e_j / (max(|e_i|,1e-8) max(|e_j|,1e-8))
+ * is >= tau (the last token has no neighbour and fails), or when
+ * keep_min_every = m > 0 and the m-1 positions before it hold no kept token
+ * (so any m consecutive positions hold one).  The kept tokens, in order, are
+ * the denoised context C', cut into chunks of chunk_tokens tokens.
+ *
+ *   emb          [B][n][H] fp32 or bf16 (dtype)  token embeddings
+ *   n_tokens     [B] int32   tokens of sequence b (clamped into [0, n]), or
+ *                            NULL for all n
+ *   g, tau       neighbourhood (1..4; the paper uses 3) and threshold (0.05)
+ *   keep_min_every  m (0: no floor; the paper uses 16)
+ *   max_cos_out  [B][n] fp32  the statistic (-inf where a token has no
+ *                            neighbour or lies past n_b), or NULL
+ *   keep_out     [B][n] uint8 1 = kept, or NULL
+ *   kept_idx     [B][n] int32 kept positions ascending, then -1
+ *   kept_count   [B] int32    |C'_b|
+ *   chunk_offset [B][ceil(n / chunk_tokens)] int32  position in C of the
+ *                            first token of each chunk of C' (the offsets of
+ *                            cmc_locate_window), then -1; NULL, or ignored
+ *                            when chunk_tokens == 0
+ *   n_chunks_out [B] int32    ceil(|C'_b| / chunk_tokens), or NULL
+ *   workspace    >= cmc_denoise_workspace_bytes(B, n) bytes, any content
+ *
+ * Limits: B, n >= 0, H >= 1 with H % 8 == 0 (bf16) or H % 4 == 0 (fp32),
+ * 1 <= g <= 4, tau not NaN.  Arithmetic: fp32 with a fixed order; the
+ * threshold decision is taken on the fp32 statistic that max_cos_out
+ * returns.
+ */
+cmc_status cmc_denoise(const void *emb, cmc_dtype dtype, const int32_t *n_tokens,
+                       int B, int n, int H, int g, float tau, int keep_min_every, int chunk_tokens,
+                       float *max_cos_out, uint8_t *keep_out, int32_t *kept_idx, int32_t *kept_count,
+                       int32_t *chunk_offset, int32_t *n_chunks_out,
+                       void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Tier-2 window.                                                           */

@@ -12,7 +12,9 @@ keeps the cache bounded by K + W + |q|) and ``two_tier_decode`` (softmax
 attention over the assembled cache), plus ``select_ragged`` and
 ``two_tier_decode_ragged`` (the same definitions per sequence, for batches
 whose sequences differ in size), and ``row_norms`` / ``locate`` (CME-guided
-Tier-2 localization, from the appendix on window localization).
+Tier-2 localization, from the appendix on window localization), and
+``denoise_scores`` / ``denoise_select`` (graph-based context denoising,
+Sec. 2.1 Eq. 3 with the minimum keep interval).
 
 ``Oracle(path)`` binds any build of the same source (the tests use it to
 load deliberately mutated builds and show that the pins reject them); the
@@ -80,6 +82,10 @@ class Oracle:
         lib.oracle_row_norms.restype = I
         lib.oracle_locate.argtypes = [P, P, I, I, I, P, I, I, P, I, P, P]
         lib.oracle_locate.restype = I
+        lib.oracle_denoise_scores.argtypes = [P, I, P, I, I, I, I, P]
+        lib.oracle_denoise_scores.restype = I
+        lib.oracle_denoise_select.argtypes = [P, P, I, I, ctypes.c_double, I, I, P, P, P, P, P]
+        lib.oracle_denoise_select.restype = I
         lib.oracle_window_start.argtypes = [ctypes.c_longlong] * 3
         lib.oracle_window_start.restype = ctypes.c_longlong
         lib.oracle_num_threads.argtypes = []
@@ -114,6 +120,44 @@ class Oracle:
                                     _ptr(idx), _ptr(scores), _ptr(gap))
         _check(rc, "select")
         return idx, scores, gap
+
+    def denoise_scores(self, emb: np.ndarray, g: int, n_tokens: Optional[np.ndarray] = None) -> np.ndarray:
+        """Eq. 3's statistic: the largest cosine similarity of each token to
+        its next g tokens, fp64 [B][n] (-inf where there is none).  emb
+        [B][n][H] fp32 or bf16 bits (uint16)."""
+        e = np.ascontiguousarray(emb)
+        B, n, H = e.shape
+        nt = None if n_tokens is None else np.ascontiguousarray(n_tokens, np.int32)
+        out = np.zeros((B, n), np.float64)
+        rc = self.lib.oracle_denoise_scores(_ptr(e), 1 if e.dtype == np.uint16 else 0, _ptr(nt), B, n, H,
+                                            int(g), _ptr(out))
+        _check(rc, "denoise_scores")
+        return out
+
+    def denoise_select(self, max_cos: np.ndarray, tau: float, keep_min_every: int,
+                       n_tokens: Optional[np.ndarray] = None, chunk_tokens: int = 0):
+        """Threshold, minimum keep interval and compaction on the given
+        max_cos [B][n].  Returns dict(keep [B][n] uint8, kept_idx [B][n],
+        kept_count [B], chunk_offset [B][ceil(n/chunk_tokens)], n_chunks
+        [B]) (the last two only with chunk_tokens > 0)."""
+        mc = np.ascontiguousarray(max_cos, np.float64)
+        B, n = mc.shape
+        nt = None if n_tokens is None else np.ascontiguousarray(n_tokens, np.int32)
+        keep = np.zeros((B, n), np.uint8)
+        idx = np.zeros((B, n), np.int32)
+        cnt = np.zeros((B,), np.int32)
+        nch = -(-n // chunk_tokens) if chunk_tokens > 0 else 0
+        off = np.zeros((B, max(nch, 1)), np.int32)
+        ncs = np.zeros((B,), np.int32)
+        rc = self.lib.oracle_denoise_select(_ptr(mc), _ptr(nt), B, n, float(tau), int(keep_min_every),
+                                            int(chunk_tokens), _ptr(keep), _ptr(idx), _ptr(cnt), _ptr(off),
+                                            _ptr(ncs))
+        _check(rc, "denoise_select")
+        r = {"keep": keep, "kept_idx": idx, "kept_count": cnt}
+        if chunk_tokens > 0:
+            r["chunk_offset"] = off[:, :nch]
+            r["n_chunks"] = ncs
+        return r
 
     def row_norms(self, sel_keys: np.ndarray) -> np.ndarray:
         """||m_j|| of every row, fp64 [B][N]."""
@@ -299,3 +343,11 @@ def row_norms(sel_keys):
 
 def locate(norms, ctx_len, W, mems_per_chunk, n_rows=None, chunk_offset=None, chunk_tokens=0):
     return default().locate(norms, ctx_len, W, mems_per_chunk, n_rows, chunk_offset, chunk_tokens)
+
+
+def denoise_scores(emb, g, n_tokens=None):
+    return default().denoise_scores(emb, g, n_tokens)
+
+
+def denoise_select(max_cos, tau, keep_min_every, n_tokens=None, chunk_tokens=0):
+    return default().denoise_select(max_cos, tau, keep_min_every, n_tokens, chunk_tokens)

@@ -21,7 +21,12 @@
  *     0..min(count,W)-1]; query head h reads kv head h / (Hq/Hkv); an empty
  *     key list yields a zero output row;
  *   - CME-guided localization works in token offsets; a sequence with no
- *     memory rows falls back to the midpoint floor(|C|/2).
+ *     memory rows falls back to the midpoint floor(|C|/2);
+ *   - denoising (Eq. 3): the neighbourhood is the g tokens after i inside
+ *     the sequence, so the last token has none and is discarded by Eq. 3;
+ *     zero norms are clamped to 1e-8 as in the selection score; the
+ *     minimum keep interval m means any m consecutive positions hold a kept
+ *     token (a token is kept when the m - 1 positions before it hold none).
  *
  * Parity pins: tests check this file against exact-rational ranking,
  * list-history attention written without ring arithmetic, a library SDPA
@@ -215,6 +220,114 @@ int oracle_window_append(void *win_k, void *win_v, int elem_bytes, int32_t *win_
             }
         }
         win_count[b] = c + T_new;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Graph-based context denoising (Sec. 2.1, Eq. 3; the minimum keep    */
+/* interval of the hyper-parameter table and of the appendix on the    */
+/* denoising threshold).                                               */
+/* ------------------------------------------------------------------ */
+
+/*
+ * max_cos_out[b][i] = max over j = i+1 .. min(i+g, n_b-1) of
+ *   e_i.e_j / (max(|e_i|, 1e-8) max(|e_j|, 1e-8)),
+ * and -inf where that range is empty (the last token of a sequence, and
+ * every position at or past n_b).  emb [B][n][H], fp32 or bf16 bits;
+ * n_b = n_tokens[b] clamped into [0, n] (all n when n_tokens is NULL).
+ */
+int oracle_denoise_scores(const void *emb, int is_bf16, const int32_t *n_tokens, int B, int n, int H, int g,
+                          double *max_cos_out)
+{
+    if (B < 0 || n < 0 || H < 1 || g < 1)
+        return ORACLE_BAD_ARG;
+    for (int b = 0; b < B; ++b) {
+        int nb = n_tokens ? n_tokens[b] : n;
+        if (nb < 0) nb = 0;
+        if (nb > n) nb = n;
+        #pragma omp parallel for schedule(static)
+        for (int i = 0; i < n; ++i) {
+            double best = -INFINITY;
+            if (i < nb) {
+                size_t ri = ((size_t)b * n + i) * H;
+                double ni = 0.0;
+                for (int h = 0; h < H; ++h) {
+                    double x = load_elem(emb, is_bf16, ri + h);
+                    ni += x * x;
+                }
+                ni = sqrt(ni);
+                for (int j = i + 1; j <= i + g && j < nb; ++j) {
+                    size_t rj = ((size_t)b * n + j) * H;
+                    double dot = 0.0, nj = 0.0;
+                    for (int h = 0; h < H; ++h) {
+                        double y = load_elem(emb, is_bf16, rj + h);
+                        dot += load_elem(emb, is_bf16, ri + h) * y;
+                        nj += y * y;
+                    }
+                    double c = dot / (fmax(ni, 1e-8) * fmax(sqrt(nj), 1e-8));
+                    if (c > best) best = c;
+                }
+            }
+            max_cos_out[(size_t)b * n + i] = best;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/*
+ * Which tokens survive, given max_cos [B][n] (the decision is taken on
+ * these values): token i < n_b passes Eq. 3 when max_cos >= tau.  Scanning
+ * left to right, a token is kept when it passes, or when keep_min_every > 0
+ * and the keep_min_every - 1 positions before it (counting from a virtual
+ * kept token at -1) hold no kept token, so that any keep_min_every
+ * consecutive positions hold at least one kept token.
+ * Outputs: keep_out [B][n] 0/1 (or NULL); kept_idx [B][n] = the kept
+ * positions ascending, then -1; kept_count [B]; with chunk_tokens > 0,
+ * chunk_offset [B][ceil(n / chunk_tokens)] = the position of the first kept
+ * token of each chunk of chunk_tokens kept tokens, then -1, and
+ * n_chunks_out [B] = ceil(kept_count / chunk_tokens) (either may be NULL).
+ */
+int oracle_denoise_select(const double *max_cos, const int32_t *n_tokens, int B, int n, double tau,
+                          int keep_min_every, int chunk_tokens, uint8_t *keep_out, int32_t *kept_idx,
+                          int32_t *kept_count, int32_t *chunk_offset, int32_t *n_chunks_out)
+{
+    if (B < 0 || n < 0 || keep_min_every < 0 || chunk_tokens < 0)
+        return ORACLE_BAD_ARG;
+    int max_chunks = chunk_tokens > 0 ? (n + chunk_tokens - 1) / chunk_tokens : 0;
+    for (int b = 0; b < B; ++b) {
+        int nb = n_tokens ? n_tokens[b] : n;
+        if (nb < 0) nb = 0;
+        if (nb > n) nb = n;
+        int last = -1, count = 0;
+        for (int i = 0; i < n; ++i) {
+            int keep = 0;
+            if (i < nb) {
+                keep = max_cos[(size_t)b * n + i] >= tau;
+                if (keep_min_every > 0 && i - last >= keep_min_every)
+                    keep = 1;
+            }
+            if (keep) {
+                last = i;
+                kept_idx[(size_t)b * n + count] = i;
+                ++count;
+            }
+            if (keep_out)
+                keep_out[(size_t)b * n + i] = (uint8_t)keep;
+        }
+        for (int c = count; c < n; ++c)
+            kept_idx[(size_t)b * n + c] = -1;
+        kept_count[b] = count;
+        if (chunk_tokens > 0) {
+            int nc = (count + chunk_tokens - 1) / chunk_tokens;
+            for (int c = 0; c < max_chunks; ++c) {
+                int v = c < nc ? kept_idx[(size_t)b * n + (size_t)c * chunk_tokens] : -1;
+                if (chunk_offset)
+                    chunk_offset[(size_t)b * max_chunks + c] = v;
+            }
+            if (n_chunks_out)
+                n_chunks_out[b] = nc;
+        }
     }
     return ORACLE_OK;
 }

@@ -32,8 +32,8 @@ CMC_BF16 = 1
 EXPORTED = [
     "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_window_append",
     "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
-    "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_status_string",
-    "cmc_last_error", "cmc_version",
+    "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_denoise_workspace_bytes",
+    "cmc_denoise", "cmc_status_string", "cmc_last_error", "cmc_version",
 ]
 
 
@@ -75,6 +75,10 @@ def lib() -> ctypes.CDLL:
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_locate_window.argtypes = [P, P, P, I, I, I, P, I, I, I, P, P, P]
         L.cmc_locate_window.restype = I
+        L.cmc_denoise_workspace_bytes.argtypes = [I, I]
+        L.cmc_denoise_workspace_bytes.restype = SZ
+        L.cmc_denoise.argtypes = [P, I, P, I, I, I, I, ctypes.c_float, I, I, P, P, P, P, P, P, P, SZ, P]
+        L.cmc_denoise.restype = I
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_two_tier_decode_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
                                                  ctypes.c_float, P, P, SZ, P]
@@ -241,6 +245,63 @@ def cmc_locate_window(norms, ctx_len, W: int, mems_per_chunk: int, n_rows=None, 
                                  _ptr(start_out), _stream(stream))
     _check(rc)
     return alpha_out, start_out
+
+
+# ------------------------------------------------------------- denoising
+
+def cmc_denoise_workspace_bytes(B: int, n: int) -> int:
+    return int(lib().cmc_denoise_workspace_bytes(int(B), int(n)))
+
+
+def cmc_denoise(emb, g: int = 3, tau: float = 0.05, keep_min_every: int = 16, n_tokens=None,
+                chunk_tokens: int = 0, max_cos_out=None, keep_out=None, kept_idx=None, kept_count=None,
+                chunk_offset=None, n_chunks_out=None, workspace=None, stream=None):
+    """Graph-based context denoising.  emb [B][n][H] fp32 or bf16 (device).
+    Returns dict(kept_idx [B][n] int32, kept_count [B] int32, and when asked
+    for (a tensor passed, or chunk_tokens > 0) max_cos, keep, chunk_offset,
+    n_chunks)."""
+    import torch
+    _need(emb.dim() == 3 and emb.is_contiguous(), "emb must be contiguous [B][n][H]")
+    B, n, H = emb.shape
+    dev = emb.device
+    dtype = _kv_dtype(emb)
+    if n_tokens is not None:
+        _need(n_tokens.shape == (B,) and n_tokens.dtype == torch.int32 and n_tokens.is_contiguous(),
+              "n_tokens [B] int32")
+    if kept_idx is None:
+        kept_idx = torch.empty((B, n), dtype=torch.int32, device=dev)
+    if kept_count is None:
+        kept_count = torch.empty((B,), dtype=torch.int32, device=dev)
+    _need(kept_idx.shape == (B, n) and kept_idx.dtype == torch.int32, "kept_idx [B][n] int32")
+    _need(kept_count.shape == (B,) and kept_count.dtype == torch.int32, "kept_count [B] int32")
+    if max_cos_out is not None:
+        _need(max_cos_out.shape == (B, n) and max_cos_out.dtype == torch.float32, "max_cos_out [B][n] fp32")
+    if keep_out is not None:
+        _need(keep_out.shape == (B, n) and keep_out.dtype == torch.uint8, "keep_out [B][n] uint8")
+    nch = -(-n // chunk_tokens) if chunk_tokens > 0 else 0
+    if chunk_tokens > 0:
+        if chunk_offset is None:
+            chunk_offset = torch.empty((B, max(nch, 1)), dtype=torch.int32, device=dev)
+        if n_chunks_out is None:
+            n_chunks_out = torch.empty((B,), dtype=torch.int32, device=dev)
+        _need(chunk_offset.dtype == torch.int32 and chunk_offset.shape[0] == B and chunk_offset.shape[1] >= nch,
+              "chunk_offset [B][ceil(n/chunk_tokens)] int32")
+    if workspace is None:
+        workspace = torch.empty(max(1, cmc_denoise_workspace_bytes(B, n)), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_denoise(_ptr(emb), dtype, _ptr(n_tokens), B, n, H, int(g), float(tau), int(keep_min_every),
+                           int(chunk_tokens), _ptr(max_cos_out), _ptr(keep_out), _ptr(kept_idx), _ptr(kept_count),
+                           _ptr(chunk_offset), _ptr(n_chunks_out), _ptr(workspace), ws_bytes, _stream(stream))
+    _check(rc)
+    r = {"kept_idx": kept_idx, "kept_count": kept_count}
+    if max_cos_out is not None:
+        r["max_cos"] = max_cos_out
+    if keep_out is not None:
+        r["keep"] = keep_out
+    if chunk_tokens > 0:
+        r["chunk_offset"] = chunk_offset[:, :nch]
+        r["n_chunks"] = n_chunks_out
+    return r
 
 
 # ---------------------------------------------------------------- window

@@ -219,6 +219,61 @@ cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const in
     return ok();
 }
 
+// ------------------------------------------------------------- denoising
+
+size_t cmc_denoise_workspace_bytes(int B, int n) {
+    if (B < 0 || n < 0) return 0;
+    return align256((size_t)B * (size_t)n);
+}
+
+cmc_status cmc_denoise(const void *emb, cmc_dtype dtype, const int32_t *n_tokens, int B, int n, int H, int g,
+                       float tau, int keep_min_every, int chunk_tokens, float *max_cos_out, uint8_t *keep_out,
+                       int32_t *kept_idx, int32_t *kept_count, int32_t *chunk_offset, int32_t *n_chunks_out,
+                       void *workspace, size_t workspace_bytes, void *stream) {
+    if (dtype != CMC_F32 && dtype != CMC_BF16)
+        return fail(CMC_ERR_UNSUPPORTED, "denoise: unknown dtype %d", (int)dtype);
+    if (B < 0 || n < 0 || H < 1 || g < 1 || keep_min_every < 0 || chunk_tokens < 0)
+        return fail(CMC_ERR_INVALID_ARGUMENT,
+                    "denoise: need B, n, keep_min_every, chunk_tokens >= 0 and H, g >= 1");
+    if (!(tau == tau)) return fail(CMC_ERR_INVALID_ARGUMENT, "denoise: tau is NaN");
+    if (g > cmc::kDenoiseMaxG) return fail(CMC_ERR_UNSUPPORTED, "denoise: g=%d exceeds %d", g, cmc::kDenoiseMaxG);
+    const int vec = dtype == CMC_BF16 ? 8 : 4;
+    if (H % vec != 0) return fail(CMC_ERR_UNSUPPORTED, "denoise: H=%d must be a multiple of %d", H, vec);
+    if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "denoise: B=%d exceeds 65535", B);
+    if (B == 0) return ok();
+    if ((n > 0 && (!emb || !kept_idx)) || !kept_count)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "denoise: emb, kept_idx and kept_count must be non-null");
+    if (misaligned(emb) || misaligned(n_tokens) || misaligned(max_cos_out) || misaligned(keep_out) ||
+        misaligned(kept_idx) || misaligned(kept_count) || misaligned(chunk_offset) || misaligned(n_chunks_out) ||
+        misaligned(workspace))
+        return fail(CMC_ERR_UNSUPPORTED, "denoise: every pointer must be 16-byte aligned");
+    const size_t need = cmc_denoise_workspace_bytes(B, n);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "denoise: workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    cmc::DenoiseParams p{};
+    p.emb = emb;
+    p.n_tokens = n_tokens;
+    p.pass = static_cast<uint8_t *>(workspace);
+    p.max_cos = max_cos_out;
+    p.keep_out = keep_out;
+    p.kept_idx = kept_idx;
+    p.kept_count = kept_count;
+    p.chunk_offset = chunk_tokens > 0 ? chunk_offset : nullptr;
+    p.n_chunks = chunk_tokens > 0 ? n_chunks_out : nullptr;
+    p.B = B;
+    p.n = n;
+    p.H = H;
+    p.g = g;
+    p.tau = tau;
+    p.keep_min_every = keep_min_every;
+    p.chunk_tokens = chunk_tokens;
+    p.max_chunks = chunk_tokens > 0 ? (n + chunk_tokens - 1) / chunk_tokens : 0;
+    hipError_t e = cmc::launch_denoise(p, dtype == CMC_BF16, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "denoise launch");
+    return ok();
+}
+
 // ---------------------------------------------------------------- window
 
 cmc_status cmc_window_append(void *win_k, void *win_v, cmc_dtype kv_dtype, int32_t *win_count,

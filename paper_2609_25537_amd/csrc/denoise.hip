@@ -1,0 +1,291 @@
+// Graph-based context denoising (Sec. 2.1, Eq. 3): token i of a context is
+// kept when its cosine similarity to one of its next g tokens reaches tau;
+// the minimum keep interval m (hyper-parameter table; appendix on the
+// denoising threshold) makes any m consecutive positions hold a kept token.
+// The survivors, in order, form the denoised context C' that is cut into
+// chunks of t tokens; the position of each chunk's first token in C is the
+// offset CME-guided localization needs.
+//
+// denoise_score_kernel: one wave per 16 consecutive tokens.  Lanes split
+// the hidden dimension (16-byte loads); the wave streams the 16 + g rows it
+// needs once, keeping the last g rows in registers, and accumulates the 16
+// + g squared norms and the 16 x g neighbour dot products per lane, then
+// reduces them across the wave.  The halo of g rows is the next wave's
+// first rows, so it is mostly served by L2.  Output: the fp32 statistic
+// max_cos (-inf where a token has no neighbour) and the Eq. 3 bit.
+//
+// denoise_select_kernel: one 1024-thread workgroup per sequence scans the
+// Eq. 3 bits.  With a(i) the last passing position before i (-1 if none),
+// the floor keeps exactly the positions a(i) + m, a(i) + 2m, ... before the
+// next passing one, so kept(i) = pass(i) or (i - a(i)) mod m == 0.  a(i) is
+// a block-wide max-scan, the output slots a sum-scan; 8 positions per
+// thread per round, carried across rounds.
+#include <limits.h>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace cmc {
+
+namespace {
+
+constexpr int kTokensPerWave = 16;
+
+__device__ __forceinline__ int clamp_tokens(int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
+
+template <typename T>
+struct Lane16;  // one 16-byte lane load widened to fp32
+template <>
+struct Lane16<float> {
+    static constexpr int N = 4;
+    __device__ __forceinline__ static void widen(const uint4 &u, float (&f)[4]) {
+        f[0] = __uint_as_float(u.x);
+        f[1] = __uint_as_float(u.y);
+        f[2] = __uint_as_float(u.z);
+        f[3] = __uint_as_float(u.w);
+    }
+};
+template <>
+struct Lane16<uint16_t> {
+    static constexpr int N = 8;
+    __device__ __forceinline__ static void widen(const uint4 &u, float (&f)[8]) {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            f[2 * i] = __uint_as_float(w[i] << 16);
+            f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+};
+
+template <typename T, int G>
+__global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
+    constexpr int TT = kTokensPerWave, R = TT + G, VEC = Lane16<T>::N;
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i0 = (blockIdx.x * 4 + wave) * TT;
+    if (i0 >= p.n) return;  // wave-uniform; no barriers below
+    const int nb = p.n_tokens ? clamp_tokens(p.n_tokens[b], p.n) : p.n;
+    const char *base = static_cast<const char *>(p.emb) + (size_t)b * p.n * p.H * sizeof(T);
+    const size_t row_bytes = (size_t)p.H * sizeof(T);
+
+    float nn[R], dd[TT][G];
+#pragma unroll
+    for (int r = 0; r < R; ++r) nn[r] = 0.f;
+#pragma unroll
+    for (int t = 0; t < TT; ++t)
+#pragma unroll
+        for (int d = 0; d < G; ++d) dd[t][d] = 0.f;
+
+    if (i0 < nb) {
+        for (int e0 = lane * VEC; e0 < p.H; e0 += kWave * VEC) {
+            // All R rows of this slice are loaded up front: rows past the
+            // sequence are clamped to its last row (in bounds) and zeroed
+            // after the load, so no load sits behind a branch.
+            uint4 raw[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                raw[r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
+                                                          (size_t)e0 * sizeof(T));
+            float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float x[VEC];
+                Lane16<T>::widen(raw[r], x);
+                if (i0 + r >= nb) {
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) x[v] = 0.f;
+                }
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
+#pragma unroll
+                for (int d = 1; d <= G; ++d) {
+                    if (r - d >= 0 && r - d < TT) {
+                        const float(&y)[VEC] = win[(r - d) % (G + 1)];
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                    }
+                }
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
+            }
+        }
+    }
+    // Wave sums, staged in LDS private to the wave so that lane t < 16 can
+    // finish token i0 + t from its own registers.
+    __shared__ float s_nn[4][R], s_dd[4][TT][G];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float v = lane_reduce<OpSum, 1, kWave>(nn[r]);
+        if (lane == 0) s_nn[wave][r] = v;
+    }
+#pragma unroll
+    for (int t = 0; t < TT; ++t)
+#pragma unroll
+        for (int d = 0; d < G; ++d) {
+            const float v = lane_reduce<OpSum, 1, kWave>(dd[t][d]);
+            if (lane == 0) s_dd[wave][t][d] = v;
+        }
+    asm volatile("" ::: "memory");  // one wave's LDS accesses execute in order
+    const int i = i0 + lane;
+    float best = -INFINITY;
+    if (lane < TT && i < nb) {
+        const float ni = fmaxf(sqrtf(s_nn[wave][lane]), 1e-8f);
+#pragma unroll
+        for (int d = 1; d <= G; ++d) {
+            if (i + d < nb)
+                best = fmaxf(best, s_dd[wave][lane][d - 1] / (ni * fmaxf(sqrtf(s_nn[wave][lane + d]), 1e-8f)));
+        }
+    }
+    if (lane < TT && i < p.n) {
+        const size_t o = (size_t)b * p.n + i;
+        if (p.max_cos) p.max_cos[o] = best;
+        p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
+    }
+}
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kPerThread = 8;
+
+// Block-wide exclusive scans over thread order (sum and max), with the
+// block total / maximum returned through `total`.
+__device__ __forceinline__ int block_excl_sum(int v, int *s_w, int &total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+    }
+    if (lane == kWave - 1) s_w[wave] = x;
+    __syncthreads();
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        base += w < wave ? s_w[w] : 0;
+        tot += s_w[w];
+    }
+    __syncthreads();
+    total = tot;
+    return base + x - v;
+}
+
+__device__ __forceinline__ int block_excl_max(int v, int *s_w, int &total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x = max(x, y);
+    }
+    const int prev_in_wave = __shfl_up(x, 1);
+    if (lane == kWave - 1) s_w[wave] = x;
+    __syncthreads();
+    int base = INT_MIN, tot = INT_MIN;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        base = w < wave ? max(base, s_w[w]) : base;
+        tot = max(tot, s_w[w]);
+    }
+    __syncthreads();
+    total = tot;
+    return lane > 0 ? max(base, prev_in_wave) : base;
+}
+
+__global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoiseParams p) {
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int nb = p.n_tokens ? clamp_tokens(p.n_tokens[b], p.n) : p.n;
+    const int m = p.keep_min_every;
+    const uint8_t *pass = p.pass + (size_t)b * p.n;
+    int32_t *idx = p.kept_idx + (size_t)b * p.n;
+    __shared__ int s_w[kSelWaves];
+
+    int carry_last = -1, carry_count = 0;
+    for (int r0 = 0; r0 < nb; r0 += kSelThreads * kPerThread) {
+        const int j0 = r0 + tid * kPerThread;
+        uint32_t bits = 0;
+        int last = -1;
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int i = j0 + u;
+            if (i < nb && pass[i]) {
+                bits |= 1u << u;
+                last = i;
+            }
+        }
+        int block_last;
+        const int before = block_excl_max(last, s_w, block_last);
+        int a = max(carry_last, before);
+        uint32_t keep = 0;
+        int cnt = 0;
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int i = j0 + u;
+            if (i < nb) {
+                const bool ps = (bits >> u) & 1u;
+                const bool k = ps || (m > 0 && (i - a) % m == 0);
+                if (ps) a = i;
+                if (k) {
+                    keep |= 1u << u;
+                    ++cnt;
+                }
+            }
+        }
+        int block_cnt;
+        int o = carry_count + block_excl_sum(cnt, s_w, block_cnt);
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int i = j0 + u;
+            if ((keep >> u) & 1u) {
+                idx[o] = i;
+                if (p.chunk_offset && p.chunk_tokens > 0 && o % p.chunk_tokens == 0)
+                    p.chunk_offset[(size_t)b * p.max_chunks + o / p.chunk_tokens] = i;
+                ++o;
+            }
+            if (p.keep_out && i < nb) p.keep_out[(size_t)b * p.n + i] = (uint8_t)((keep >> u) & 1u);
+        }
+        carry_last = max(carry_last, block_last);
+        carry_count += block_cnt;
+    }
+    const int count = carry_count;
+    for (int i = count + tid; i < p.n; i += kSelThreads) idx[i] = -1;
+    if (p.keep_out)
+        for (int i = nb + tid; i < p.n; i += kSelThreads) p.keep_out[(size_t)b * p.n + i] = 0;
+    if (p.chunk_tokens > 0) {
+        const int nc = (count + p.chunk_tokens - 1) / p.chunk_tokens;
+        if (p.chunk_offset)
+            for (int c = nc + tid; c < p.max_chunks; c += kSelThreads)
+                p.chunk_offset[(size_t)b * p.max_chunks + c] = -1;
+        if (tid == 0 && p.n_chunks) p.n_chunks[b] = nc;
+    }
+    if (tid == 0) p.kept_count[b] = count;
+}
+
+template <typename T>
+hipError_t launch_scores(const DenoiseParams &p, hipStream_t stream) {
+    dim3 grid((p.n + 4 * kTokensPerWave - 1) / (4 * kTokensPerWave), p.B);
+    switch (p.g) {
+        case 1: denoise_score_kernel<T, 1><<<grid, 256, 0, stream>>>(p); break;
+        case 2: denoise_score_kernel<T, 2><<<grid, 256, 0, stream>>>(p); break;
+        case 3: denoise_score_kernel<T, 3><<<grid, 256, 0, stream>>>(p); break;
+        case 4: denoise_score_kernel<T, 4><<<grid, 256, 0, stream>>>(p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_denoise(const DenoiseParams &p, bool bf16, hipStream_t stream) {
+    if (p.B == 0) return hipSuccess;
+    if (p.n > 0) {
+        const hipError_t e = bf16 ? launch_scores<uint16_t>(p, stream) : launch_scores<float>(p, stream);
+        if (e != hipSuccess) return e;
+    }
+    denoise_select_kernel<<<p.B, kSelThreads, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace cmc

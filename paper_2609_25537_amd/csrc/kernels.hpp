@@ -84,4 +84,21 @@ struct LocateParams {
 };
 hipError_t launch_locate(const LocateParams &p, hipStream_t stream);
 
+struct DenoiseParams {
+    const void *emb;            // [B][n][H] fp32 or bf16
+    const int32_t *n_tokens;    // [B] or nullptr: all n
+    uint8_t *pass;              // [B][n] Eq. 3 bits (workspace)
+    float *max_cos;             // [B][n] or nullptr
+    uint8_t *keep_out;          // [B][n] or nullptr
+    int32_t *kept_idx;          // [B][n]
+    int32_t *kept_count;        // [B]
+    int32_t *chunk_offset;      // [B][max_chunks] or nullptr
+    int32_t *n_chunks;          // [B] or nullptr
+    int B, n, H, g;
+    float tau;
+    int keep_min_every, chunk_tokens, max_chunks;
+};
+constexpr int kDenoiseMaxG = 4;
+hipError_t launch_denoise(const DenoiseParams &p, bool bf16, hipStream_t stream);
+
 }  // namespace cmc

@@ -39,6 +39,7 @@ ROLE = {
     "full_k": 11,    # uncompressed-cache baseline keys
     "full_v": 12,    # uncompressed-cache baseline values
     "ragged": 13,    # per-sequence sizes of a ragged batch
+    "emb": 14,       # token embeddings of the denoising workloads
 }
 
 
@@ -337,3 +338,67 @@ def device_normal(seed: int, role: str, ids: Sequence[int], shape, std: float, d
     if std != 1.0:
         x.mul_(std)
     return x.to(dtype)
+
+
+# ------------------------------------------------------------- denoising
+
+@dataclasses.dataclass(frozen=True)
+class DenoiseWorkload:
+    """Token embeddings for graph-based context denoising (Sec. 2.1, Eq. 3).
+
+    B contexts of up to n tokens (lengths uniform in [n_min, n]) with
+    hidden size H.  Token i links to token i-1 with probability p_link:
+    e_i = 0.6 e_{i-1} + 0.8 z_i, else e_i = z_i, z ~ N(0, I).  Linked runs
+    stand in for coherent phrases (neighbour cosine about 0.6, 0.36, ...),
+    unlinked tokens for isolated ones (cosine about N(0, 1/H)); p_link is
+    set so that about 14% of the tokens survive tau = 0.05 with g = 3 and
+    the keep-every-16 floor, the retention the paper reports.
+    """
+
+    name: str
+    B: int
+    n: int
+    H: int
+    dtype: str
+    seed: int
+    n_min: int = 0
+    p_link: float = 0.02
+    g: int = 3
+    tau: float = 0.05
+    keep_min_every: int = 16
+    chunk_tokens: int = 256
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
+
+    def replace(self, **kw) -> "DenoiseWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+DENOISE_WORKLOADS: Dict[str, DenoiseWorkload] = {
+    # GPT2-Large-sized encoder inputs at the paper's maximum input length.
+    "denoise_gpt2l_batch64": DenoiseWorkload("denoise_gpt2l_batch64", B=64, n=3072, H=1280, dtype="bf16",
+                                             seed=707, n_min=1024),
+}
+
+
+def denoise_tokens(w: DenoiseWorkload) -> np.ndarray:
+    """Context lengths [B] int32."""
+    if w.n_min >= w.n:
+        return np.full(w.B, w.n, np.int32)
+    return _rng(w.seed, "ragged", 1).integers(w.n_min, w.n + 1, size=w.B).astype(np.int32)
+
+
+def denoise_emb(w: DenoiseWorkload, b: Optional[int] = None) -> np.ndarray:
+    """Embeddings [B][n][H] (or [n][H] for one context): fp32, or bf16 bits."""
+    if b is None:
+        return np.stack([denoise_emb(w, i) for i in range(w.B)])
+    r = _rng(w.seed, "emb", b)
+    z = r.standard_normal(size=(w.n, w.H), dtype=np.float32)
+    link = r.random(w.n) < w.p_link
+    e = np.empty_like(z)
+    e[0] = z[0]
+    for i in range(1, w.n):
+        e[i] = np.float32(0.6) * e[i - 1] + np.float32(0.8) * z[i] if link[i] else z[i]
+    return f32_to_bf16_bits(e) if w.dtype == "bf16" else e

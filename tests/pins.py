@@ -519,6 +519,96 @@ def pin_locate_argmax_library(orc):
         assert alpha[b] == want, (b, alpha[b], want)
 
 
+def _onehot(classes, H=8):
+    return np.eye(H, dtype=np.float32)[np.asarray(classes)]
+
+
+def pin_denoise_onehot_cases(orc):
+    """Eq. 3 on one-hot tokens, where a cosine is exactly 1 (same class) or
+    0 (different class), so every decision can be read off the class
+    sequence by eye:
+        position  0 1 2 3 4 5 6 7 8 9 10 11
+        class     0 1 0 2 3 3 1 1 4 5 6  7
+    With g = 3, a token passes when one of its next three tokens has its
+    class: positions 0 (2), 4 (5), 6 (7).  Position 11 has no neighbour.
+    With no floor (m = 0) the kept set is {0, 4, 6}.  With m = 4, position
+    10 (= 6 + 4) is forced as well (4 = 0 + 4 passes anyway); with m = 3,
+    3 (= 0 + 3) and 9 (= 6 + 3) are forced and nothing else (11 - 9 = 2).  tau = 1 keeps exact-1 cosines
+    (Eq. 3 is '>='); tau just above 1 keeps nothing by Eq. 3, so only the
+    floor remains: m = 5 keeps 4 and 9 (first at -1 + 5).  A second
+    sequence of 7 tokens (n_b = 7) must ignore tokens past its end: its
+    position 6 has class 1 like position 7 of the first row's pattern, but
+    position 7 is outside it."""
+    classes = [0, 1, 0, 2, 3, 3, 1, 1, 4, 5, 6, 7]
+    e = np.stack([_onehot(classes), _onehot(classes)])
+    n_tok = np.array([12, 7], np.int32)
+    mc = orc.denoise_scores(e, 3, n_tok)
+    assert mc[0].tolist()[:11] == [1, 0, 0, 0, 1, 0, 1, 0, 0, 0, 0] and np.isneginf(mc[0, 11])
+    assert mc[1].tolist()[:6] == [1, 0, 0, 0, 1, 0] and np.isneginf(mc[1, 6:]).all()
+    kept = lambda r: r["kept_idx"][0, :r["kept_count"][0]].tolist()
+    assert kept(orc.denoise_select(mc, 0.05, 0, n_tok)) == [0, 4, 6]
+    assert kept(orc.denoise_select(mc, 0.05, 4, n_tok)) == [0, 4, 6, 10]
+    assert kept(orc.denoise_select(mc, 0.05, 3, n_tok)) == [0, 3, 4, 6, 9]
+    assert kept(orc.denoise_select(mc, 1.0, 0, n_tok)) == [0, 4, 6]
+    assert kept(orc.denoise_select(mc, 1.0 + 1e-12, 5, n_tok)) == [4, 9]
+    r = orc.denoise_select(mc, 0.05, 4, n_tok, chunk_tokens=3)
+    assert r["kept_idx"][1].tolist() == [0, 4, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1]
+    assert r["kept_count"].tolist() == [4, 2]
+    assert r["chunk_offset"].tolist() == [[0, 10, -1, -1], [0, -1, -1, -1]]
+    assert r["n_chunks"].tolist() == [2, 1]
+    assert r["keep"][0].tolist() == [1, 0, 0, 0, 1, 0, 1, 0, 0, 0, 1, 0]
+
+
+def pin_denoise_scores_library(orc):
+    """The Eq. 3 statistic against torch's cosine_similarity, offset by
+    offset, in fp64; bf16 inputs are widened exactly first."""
+    import torch
+    rng = np.random.default_rng(61)
+    B, n, H, g = 2, 30, 16, 3
+    e = rng.standard_normal((B, n, H)).astype(np.float32)
+    e[:, ::4] += e[:, 1::4]  # some strongly aligned neighbours
+    for dtype in ("f32", "bf16"):
+        arr = e if dtype == "f32" else _bf16(e)
+        vals = torch.from_numpy(e.astype(np.float64) if dtype == "f32" else
+                                (arr.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+        ref = np.full((B, n), -np.inf)
+        for d in range(1, g + 1):
+            c = torch.nn.functional.cosine_similarity(vals[:, :-d], vals[:, d:], dim=2).numpy()
+            ref[:, :-d] = np.maximum(ref[:, :-d], c)
+        got = orc.denoise_scores(arr, g)
+        assert np.isneginf(got[:, -1]).all()
+        _close(got[:, :-1], ref[:, :-1], 1e-12, f"denoise scores {dtype}")
+
+
+def pin_denoise_floor_properties(orc):
+    """On random statistics and thresholds the kept set is characterised by:
+    every token passing Eq. 3 is kept; any m consecutive positions of the
+    sequence hold a kept token; a kept token that does not pass sits exactly
+    m after the previous kept one (virtual -1); nothing past n_b is kept."""
+    rng = np.random.default_rng(62)
+    B, n = 6, 200
+    mc = rng.uniform(-1, 1, size=(B, n))
+    mc[:, -1] = -np.inf
+    n_tok = np.array([200, 150, 1, 0, 37, 199], np.int32)
+    for tau in (-2.0, 0.3, 0.9, 2.0):
+        for m in (0, 1, 5, 16):
+            r = orc.denoise_select(mc, tau, m, n_tok)
+            for b in range(B):
+                nb = int(n_tok[b])
+                kept = r["kept_idx"][b, :r["kept_count"][b]].tolist()
+                assert kept == sorted(set(kept)) and all(0 <= i < nb for i in kept)
+                assert r["keep"][b].tolist() == [1 if i in set(kept) else 0 for i in range(n)]
+                passing = {i for i in range(nb) if mc[b, i] >= tau}
+                assert passing <= set(kept)
+                if m > 0:
+                    marks = [-1] + kept
+                    for a, c in zip(marks, marks[1:]):
+                        assert c in passing or c - a == m
+                    assert all(any(j in set(kept) for j in range(s, s + m)) for s in range(0, nb - m + 1))
+                else:
+                    assert set(kept) == passing
+
+
 ALL_PINS = [v for n, v in sorted(globals().items()) if n.startswith("pin_") and callable(v)]
 
 

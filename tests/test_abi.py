@@ -202,3 +202,33 @@ def test_locate_validation(kw, code):
 
 def test_locate_empty_batch_ok():
     assert _loc(B=0, nrm=None, ctx=None, st=None) == cmc.CMC_OK
+
+
+def _den(**kw):
+    a = dict(emb=FAKE, dt=cmc.CMC_BF16, nt=None, B=2, n=64, H=128, g=3, tau=0.05, m=16, t=0, mc=None, keep=None,
+             idx=FAKE, cnt=FAKE, off=None, nch=None, ws=FAKE, wsb=1 << 20, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_denoise(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(g=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(g=5), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(H=12), cmc.CMC_ERR_UNSUPPORTED),                    # bf16 rows need H % 8 == 0
+    (dict(dt=cmc.CMC_F32, H=6), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(tau=float("nan")), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(m=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(idx=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(cnt=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(wsb=64), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    (dict(emb=FAKE + 2), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(dt=5), cmc.CMC_ERR_UNSUPPORTED),
+])
+def test_denoise_validation(kw, code):
+    assert _den(**kw) == code
+
+
+def test_denoise_workspace_query():
+    assert cmc.cmc_denoise_workspace_bytes(3, 1000) >= 3000
+    assert cmc.cmc_denoise_workspace_bytes(-1, 10) == 0
+    assert _den(B=0) == cmc.CMC_OK

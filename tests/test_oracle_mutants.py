@@ -49,6 +49,19 @@ MUTANTS = [
     ("locate_all_rows", "if (nb > N) nb = N;", "nb = N;"),
     ("locate_no_midpoint", "alpha = ctx_len[b] / 2;", "alpha = 0;"),
     ("row_norm_squared", "norms_out[r] = sqrt(s);", "norms_out[r] = s;"),
+    ("denoise_strict_threshold", "keep = max_cos[(size_t)b * n + i] >= tau;",
+     "keep = max_cos[(size_t)b * n + i] > tau;"),
+    ("denoise_neighbourhood_short", "for (int j = i + 1; j <= i + g && j < nb; ++j) {",
+     "for (int j = i + 1; j < i + g && j < nb; ++j) {"),
+    ("denoise_past_sequence_end", "for (int j = i + 1; j <= i + g && j < nb; ++j) {",
+     "for (int j = i + 1; j <= i + g && j < n; ++j) {"),
+    ("denoise_floor_off_by_one", "if (keep_min_every > 0 && i - last >= keep_min_every)",
+     "if (keep_min_every > 0 && i - last > keep_min_every)"),
+    ("denoise_floor_start", "int last = -1, count = 0;", "int last = 0, count = 0;"),
+    ("denoise_upstream_norm", "double c = dot / (fmax(ni, 1e-8) * fmax(sqrt(nj), 1e-8));",
+     "double c = dot / (fmax(ni, 1e-8) * fmax(ni, 1e-8));"),
+    ("denoise_chunk_first_token", "int v = c < nc ? kept_idx[(size_t)b * n + (size_t)c * chunk_tokens] : -1;",
+     "int v = c < nc ? kept_idx[(size_t)b * n + (size_t)c] : -1;"),
 ]
 
 
