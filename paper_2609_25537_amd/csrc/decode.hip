@@ -21,10 +21,10 @@
 //     holding the G query heads repeated (row m = head m % G), so every lane
 //     ends with all G scores of key (lane % 16).  q is split into bf16
 //     hi + lo parts (two MFMAs per slice), which keeps the logit error at the
-//     level of fp32 accumulation.  P V runs on the VALU in fp32: the block is
-//     split into two halves of 8 keys, lane l owning key (l & 7) and Dh/8
-//     dims; its p values come from its own lane or lane l ^ 8 (one DPP row
-//     rotate).
+//     level of fp32 accumulation.  P V runs on the VALU in fp32 in four
+//     quarters of 4 keys: lane l owns key (l & 3) of each quarter and Dh/16
+//     dims; the p values reach that layout through 16 x G floats of LDS
+//     private to the wave.
 //   VALU (fp32 K/V, or G = 8): 16-byte lane loads, LPR lanes per row, dot
 //     products reduced by a DPP butterfly.
 // Both keep an online softmax per wave (running max in log2 units, q
