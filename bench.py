@@ -475,6 +475,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.workload in wl.DENOISE_WORKLOADS:
         return main_denoise(args, wl.DENOISE_WORKLOADS[args.workload], dev)
+    if args.workload in wl.BRIDGE_WORKLOADS:
+        return main_bridge(args, wl.BRIDGE_WORKLOADS[args.workload], dev)
     w = wl.get(args.workload)
     if w.layers != 1:
         return main_stack(args, w, dev)
@@ -637,6 +639,84 @@ def main_denoise(args, w, dev):
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "denoise_score_kernel + denoise_select_kernel (one cmc_denoise call)",
                      "bytes_per_launch": nbytes, "launch_us": round(t_call * 1e6, 3)},
+        "cpu_baseline": cpu,
+    }
+    txt = json.dumps(line)
+    print(txt, flush=True)
+    if args.out:
+        with open(args.out, "a") as f:
+            f.write(txt + "\n")
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bridge_cpu_baseline(w, budget_s: float):
+    """The fp64 oracle on rows of the workload until the budget is spent."""
+    import oracle
+    from paper_2609_25537_amd import workloads as wl
+    orc = oracle.default()
+    p = wl.bridge_params(w)
+    done, t, r0 = 0, 0.0, 0
+    while done < 16 or t < budget_s:
+        rows = list(range(r0, min(r0 + 16, w.M)))
+        h = wl.bridge_h(w, rows)
+        t0 = time.perf_counter()
+        orc.memory_bridge(h, p["w1"], p["b1"], p["w2"], p["b2"], p["gamma"], p["beta"], w.nu, w.eps)
+        t += time.perf_counter() - t0
+        done += len(rows)
+        r0 = (r0 + 16) % w.M
+        if done >= w.M:
+            break
+    return {"value": done / t, "unit": "CME rows/s", "cores": orc.num_threads(), "kind": "oracle",
+            "sample": f"{done} of {w.M} rows ({t:.2f} s)"}
+
+
+def main_bridge(args, w, dev):
+    """MemoryBridge projection of a batch of CME vectors: one step is one
+    cmc_memory_bridge call (two MFMA GEMMs, LayerNorm, tanh, cap), inputs
+    resident in HBM."""
+    import torch
+    from paper_2609_25537_amd import cmc
+    from paper_2609_25537_amd import workloads as wl
+    p = wl.bridge_params(w)
+    h = to_dev(wl.bridge_h(w), dev)
+    d = {k: to_dev(v, dev) for k, v in p.items()}
+    out = torch.empty((w.M, w.Hd), dtype=torch.float32, device=dev)
+    ws = torch.empty(cmc.cmc_bridge_workspace_bytes(w.M, w.F), dtype=torch.uint8, device=dev)
+
+    def call():
+        cmc.cmc_memory_bridge(h, d["w1"], d["b1"], d["w2"], d["b2"], d["gamma"], d["beta"], w.nu, w.eps, out=out,
+                              workspace=ws)
+
+    reps = max(1, args.launch_reps // 50)
+    g = capture(lambda: [call() for _ in range(reps)])
+    for _ in range(args.warmup):
+        g.replay()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(args.steps):
+        g.replay()
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    calls = args.steps * reps
+    t_call = ms * 1e-3 / calls
+    flops = 2.0 * w.M * (w.Hc * w.F + w.F * w.Hd)
+    achieved = flops / t_call / 1e12
+    cpu = None if args.no_cpu_baseline else bridge_cpu_baseline(w, args.cpu_seconds)
+    line = {
+        "metric": "MemoryBridge CME rows/s and achieved TFLOP/s (% of MI355X dense bf16 MFMA peak)",
+        "value": round(w.M * calls / (ms * 1e-3), 1), "unit": "CME rows/s", "n_gpus": 1, "steps": calls,
+        "warmup": args.warmup, "ms_per_step": round(ms / calls, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "M": w.M, "Hc": w.Hc, "F": w.F, "Hd": w.Hd, "nu": w.nu, "graph": True},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_nt_kernel x2 + bridge_norm_kernel (one cmc_memory_bridge call)",
+                     "flops_per_launch": flops, "launch_us": round(t_call * 1e6, 3)},
         "cpu_baseline": cpu,
     }
     txt = json.dumps(line)

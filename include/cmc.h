@@ -19,6 +19,8 @@
  *   cmc_locate_window    CME-guided Tier-2 window placement (once per question)
  *   cmc_denoise          graph-based context denoising before compression
  *                        (Sec. 2.1, once per context)
+ *   cmc_memory_bridge    MemoryBridge projection of CME vectors into selection
+ *                        keys (Sec. 2.2, once per context)
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -160,6 +162,47 @@ cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const in
                              int B, int N, int mems_per_chunk,
                              const int32_t *chunk_offset, int n_chunks, int chunk_tokens,
                              int W, int32_t *alpha_out, int32_t *start_out, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* MemoryBridge.                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of workspace cmc_memory_bridge needs: the hidden activations,
+ * M * F bf16. */
+size_t cmc_bridge_workspace_bytes(int M, int F);
+
+/*
+ * MemoryBridge projection (Sec. 2.2): each CME vector h (encoder width Hc)
+ * becomes a decoder-ready memory row of width Hd,
+ *   hidden = GELU(h W1^T + b1)                      (exact erf GELU)
+ *   m_hat  = LayerNorm(hidden W2^T + b2)            (gamma, beta, biased variance,
+ *                                                    eps inside the square root:
+ *                                                    the appendix's nn.LayerNorm)
+ *   t      = nu tanh(m_hat)
+ *   out    = t * min(1, 2 nu / ||t||_2)             (the section's norm cap:
+ *                                                    |out_i| <= nu, ||out|| <= 2 nu)
+ * with nu = s * (mean l2 norm of the decoder's token embeddings), computed
+ * by the caller.  The rows of out are the selection keys of cmc_select_cmes.
+ *
+ *   h        [M][Hc] bf16     CME vectors
+ *   w1       [F][Hc] bf16     first layer (nn.Linear layout: [out][in]); b1 [F] fp32
+ *   w2       [Hd][F] bf16     second layer; b2 [Hd] fp32
+ *   ln_gamma, ln_beta [Hd] fp32
+ *   out      [M][Hd] fp32
+ *   workspace >= cmc_bridge_workspace_bytes(M, F) bytes, any content; after
+ *            the call it holds the hidden activations, [M][F] bf16 (rounded
+ *            to nearest even from fp32)
+ *
+ * Limits: M >= 0; Hc % 64 == 0, F % 128 == 0, Hd % 128 == 0 (the GEMM tile);
+ * nu > 0 and eps >= 0 finite.  Arithmetic: bf16 operands, fp32 accumulation
+ * (MFMA), the second layer reads the bf16 hidden activations; LayerNorm,
+ * tanh and the cap in fp32.
+ */
+cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1,
+                             const void *w2, const float *b2,
+                             const float *ln_gamma, const float *ln_beta,
+                             float nu, float ln_eps, int M, int Hc, int F, int Hd,
+                             float *out, void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Context denoising.                                                       */

@@ -14,7 +14,9 @@ attention over the assembled cache), plus ``select_ragged`` and
 whose sequences differ in size), and ``row_norms`` / ``locate`` (CME-guided
 Tier-2 localization, from the appendix on window localization), and
 ``denoise_scores`` / ``denoise_select`` (graph-based context denoising,
-Sec. 2.1 Eq. 3 with the minimum keep interval).
+Sec. 2.1 Eq. 3 with the minimum keep interval), and ``bridge_hidden`` /
+``bridge_out`` (the MemoryBridge projection and its norm-calibrated tanh
+cap, Sec. 2.2).
 
 ``Oracle(path)`` binds any build of the same source (the tests use it to
 load deliberately mutated builds and show that the pins reject them); the
@@ -86,6 +88,10 @@ class Oracle:
         lib.oracle_denoise_scores.restype = I
         lib.oracle_denoise_select.argtypes = [P, P, I, I, ctypes.c_double, I, I, P, P, P, P, P]
         lib.oracle_denoise_select.restype = I
+        lib.oracle_bridge_hidden.argtypes = [P, P, P, I, I, I, P]
+        lib.oracle_bridge_hidden.restype = I
+        lib.oracle_bridge_out.argtypes = [P, P, P, P, P, ctypes.c_double, ctypes.c_double, I, I, I, P]
+        lib.oracle_bridge_out.restype = I
         lib.oracle_window_start.argtypes = [ctypes.c_longlong] * 3
         lib.oracle_window_start.restype = ctypes.c_longlong
         lib.oracle_num_threads.argtypes = []
@@ -158,6 +164,40 @@ class Oracle:
             r["chunk_offset"] = off[:, :nch]
             r["n_chunks"] = ncs
         return r
+
+    def bridge_hidden(self, h: np.ndarray, w1: np.ndarray, b1: np.ndarray) -> np.ndarray:
+        """MemoryBridge hidden layer GELU(h w1^T + b1), fp64 [M][F]; h [M][Hc]
+        and w1 [F][Hc] bf16 bits (uint16), b1 [F] fp32."""
+        hh = np.ascontiguousarray(h, np.uint16)
+        ww = np.ascontiguousarray(w1, np.uint16)
+        bb = np.ascontiguousarray(b1, np.float32)
+        M, Hc = hh.shape
+        F = ww.shape[0]
+        assert ww.shape == (F, Hc) and bb.shape == (F,)
+        out = np.zeros((M, F), np.float64)
+        _check(self.lib.oracle_bridge_hidden(_ptr(hh), _ptr(ww), _ptr(bb), M, Hc, F, _ptr(out)), "bridge_hidden")
+        return out
+
+    def bridge_out(self, hidden: np.ndarray, w2: np.ndarray, b2: np.ndarray, gamma: np.ndarray,
+                   beta: np.ndarray, nu: float, eps: float = 1e-5) -> np.ndarray:
+        """MemoryBridge output layer, LayerNorm and norm-calibrated tanh cap
+        from the given hidden activations [M][F] (any float values); w2 [Hd][F]
+        bf16 bits; b2, gamma, beta [Hd] fp32.  Returns fp64 [M][Hd]."""
+        hd = np.ascontiguousarray(hidden, np.float64)
+        ww = np.ascontiguousarray(w2, np.uint16)
+        M, F = hd.shape
+        Hd = ww.shape[0]
+        vec = [np.ascontiguousarray(v, np.float32) for v in (b2, gamma, beta)]
+        assert ww.shape == (Hd, F) and all(v.shape == (Hd,) for v in vec)
+        out = np.zeros((M, Hd), np.float64)
+        rc = self.lib.oracle_bridge_out(_ptr(hd), _ptr(ww), *[_ptr(v) for v in vec], float(nu), float(eps), M, F,
+                                        Hd, _ptr(out))
+        _check(rc, "bridge_out")
+        return out
+
+    def memory_bridge(self, h, w1, b1, w2, b2, gamma, beta, nu, eps=1e-5):
+        """The whole MemoryBridge in fp64 (hidden layer not rounded)."""
+        return self.bridge_out(self.bridge_hidden(h, w1, b1), w2, b2, gamma, beta, nu, eps)
 
     def row_norms(self, sel_keys: np.ndarray) -> np.ndarray:
         """||m_j|| of every row, fp64 [B][N]."""
@@ -351,3 +391,11 @@ def denoise_scores(emb, g, n_tokens=None):
 
 def denoise_select(max_cos, tau, keep_min_every, n_tokens=None, chunk_tokens=0):
     return default().denoise_select(max_cos, tau, keep_min_every, n_tokens, chunk_tokens)
+
+
+def bridge_hidden(h, w1, b1):
+    return default().bridge_hidden(h, w1, b1)
+
+
+def bridge_out(hidden, w2, b2, gamma, beta, nu, eps=1e-5):
+    return default().bridge_out(hidden, w2, b2, gamma, beta, nu, eps)

@@ -26,7 +26,10 @@
  *     the sequence, so the last token has none and is discarded by Eq. 3;
  *     zero norms are clamped to 1e-8 as in the selection score; the
  *     minimum keep interval m means any m consecutive positions hold a kept
- *     token (a token is kept when the m - 1 positions before it hold none).
+ *     token (a token is kept when the m - 1 positions before it hold none);
+ *   - MemoryBridge: Linear -> exact (erf) GELU -> Linear -> LayerNorm (biased
+ *     variance, eps inside the square root) -> norm-calibrated tanh cap; the
+ *     hidden width F is a parameter (the paper does not state it).
  *
  * Parity pins: tests check this file against exact-rational ranking,
  * list-history attention written without ring arithmetic, a library SDPA
@@ -220,6 +223,84 @@ int oracle_window_append(void *win_k, void *win_v, int elem_bytes, int32_t *win_
             }
         }
         win_count[b] = c + T_new;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* MemoryBridge (Sec. 2.2): a two-layer MLP with GELU, LayerNorm on its */
+/* output (the appendix's nn.LayerNorm formula), then the norm-         */
+/* calibrated tanh cap of the section's equation.                      */
+/* ------------------------------------------------------------------ */
+
+/* GELU, the exact (erf) form. */
+static double gelu(double x)
+{
+    return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));
+}
+
+/*
+ * Hidden layer: hidden[r][f] = GELU(sum_c h[r][c] * w1[f][c] + b1[f]).
+ * h [M][Hc] and w1 [F][Hc] are bf16 bit patterns, b1 [F] fp32.
+ */
+int oracle_bridge_hidden(const uint16_t *h, const uint16_t *w1, const float *b1, int M, int Hc, int F,
+                         double *hidden_out)
+{
+    if (M < 0 || Hc < 1 || F < 1)
+        return ORACLE_BAD_ARG;
+    #pragma omp parallel for schedule(static)
+    for (int r = 0; r < M; ++r) {
+        for (int f = 0; f < F; ++f) {
+            double u = (double)b1[f];
+            for (int c = 0; c < Hc; ++c)
+                u += widen_bf16(h[(size_t)r * Hc + c]) * widen_bf16(w1[(size_t)f * Hc + c]);
+            hidden_out[(size_t)r * F + f] = gelu(u);
+        }
+    }
+    return ORACLE_OK;
+}
+
+/*
+ * Output layer, LayerNorm and cap, from given hidden activations [M][F]:
+ *   y = hidden . w2^T + b2                        (w2 [Hd][F] bf16, b2 [Hd])
+ *   m_hat = gamma * (y - mean) / sqrt(var + eps) + beta   (biased variance)
+ *   t = nu * tanh(m_hat)
+ *   out = t * min(1, 2 nu / ||t||_2)
+ */
+int oracle_bridge_out(const double *hidden, const uint16_t *w2, const float *b2, const float *gamma,
+                      const float *beta, double nu, double eps, int M, int F, int Hd, double *out)
+{
+    if (M < 0 || F < 1 || Hd < 1 || !(nu > 0.0) || eps < 0.0)
+        return ORACLE_BAD_ARG;
+    #pragma omp parallel
+    {
+        double *y = (double *)malloc(sizeof(double) * (size_t)Hd);
+        #pragma omp for schedule(static)
+        for (int r = 0; r < M; ++r) {
+            double mean = 0.0, var = 0.0, nrm = 0.0;
+            for (int j = 0; j < Hd; ++j) {
+                double acc = (double)b2[j];
+                for (int f = 0; f < F; ++f)
+                    acc += hidden[(size_t)r * F + f] * widen_bf16(w2[(size_t)j * F + f]);
+                y[j] = acc;
+                mean += acc;
+            }
+            mean /= Hd;
+            for (int j = 0; j < Hd; ++j)
+                var += (y[j] - mean) * (y[j] - mean);
+            var /= Hd;
+            double inv = 1.0 / sqrt(var + eps);
+            for (int j = 0; j < Hd; ++j) {
+                double m_hat = (double)gamma[j] * (y[j] - mean) * inv + (double)beta[j];
+                y[j] = nu * tanh(m_hat);
+                nrm += y[j] * y[j];
+            }
+            nrm = sqrt(nrm);
+            double c = (nrm > 0.0 && 2.0 * nu / nrm < 1.0) ? 2.0 * nu / nrm : 1.0;
+            for (int j = 0; j < Hd; ++j)
+                out[(size_t)r * Hd + j] = y[j] * c;
+        }
+        free(y);
     }
     return ORACLE_OK;
 }

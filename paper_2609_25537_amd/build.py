@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libcmc.so")
 OBJDIR = os.path.join(PKG, "_build")
-SOURCES = ["cmc_api.hip", "decode.hip", "select.hip", "window.hip", "denoise.hip"]
+SOURCES = ["cmc_api.hip", "decode.hip", "select.hip", "window.hip", "denoise.hip", "bridge.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",

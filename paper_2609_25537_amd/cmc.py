@@ -33,7 +33,8 @@ EXPORTED = [
     "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_window_append",
     "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
     "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_denoise_workspace_bytes",
-    "cmc_denoise", "cmc_status_string", "cmc_last_error", "cmc_version",
+    "cmc_denoise", "cmc_bridge_workspace_bytes", "cmc_memory_bridge", "cmc_status_string", "cmc_last_error",
+    "cmc_version",
 ]
 
 
@@ -79,6 +80,11 @@ def lib() -> ctypes.CDLL:
         L.cmc_denoise_workspace_bytes.restype = SZ
         L.cmc_denoise.argtypes = [P, I, P, I, I, I, I, ctypes.c_float, I, I, P, P, P, P, P, P, P, SZ, P]
         L.cmc_denoise.restype = I
+        L.cmc_bridge_workspace_bytes.argtypes = [I, I]
+        L.cmc_bridge_workspace_bytes.restype = SZ
+        L.cmc_memory_bridge.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, ctypes.c_float, I, I, I, I, P, P, SZ,
+                                        P]
+        L.cmc_memory_bridge.restype = I
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_two_tier_decode_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
                                                  ctypes.c_float, P, P, SZ, P]
@@ -245,6 +251,41 @@ def cmc_locate_window(norms, ctx_len, W: int, mems_per_chunk: int, n_rows=None, 
                                  _ptr(start_out), _stream(stream))
     _check(rc)
     return alpha_out, start_out
+
+
+# ----------------------------------------------------------- MemoryBridge
+
+def cmc_bridge_workspace_bytes(M: int, F: int) -> int:
+    return int(lib().cmc_bridge_workspace_bytes(int(M), int(F)))
+
+
+def cmc_memory_bridge(h, w1, b1, w2, b2, ln_gamma, ln_beta, nu: float, ln_eps: float = 1e-5, out=None,
+                      workspace=None, stream=None):
+    """MemoryBridge projection.  h [M][Hc] bf16, w1 [F][Hc] bf16, b1 [F] fp32,
+    w2 [Hd][F] bf16, b2/ln_gamma/ln_beta [Hd] fp32 (device).  Returns out
+    [M][Hd] fp32; the workspace (if given) then holds the hidden activations
+    [M][F] bf16."""
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    _need(h.dim() == 2 and h.dtype == bf and h.is_contiguous(), "h must be contiguous bf16 [M][Hc]")
+    M, Hc = h.shape
+    _need(w1.dim() == 2 and w1.shape[1] == Hc and w1.dtype == bf and w1.is_contiguous(), "w1 [F][Hc] bf16")
+    F = w1.shape[0]
+    _need(w2.dim() == 2 and w2.shape[1] == F and w2.dtype == bf and w2.is_contiguous(), "w2 [Hd][F] bf16")
+    Hd = w2.shape[0]
+    for name, v, n in (("b1", b1, F), ("b2", b2, Hd), ("ln_gamma", ln_gamma, Hd), ("ln_beta", ln_beta, Hd)):
+        _need(v.shape == (n,) and v.dtype == f32 and v.is_contiguous(), f"{name} [{n}] fp32")
+    if out is None:
+        out = torch.empty((M, Hd), dtype=f32, device=h.device)
+    _need(out.shape == (M, Hd) and out.dtype == f32 and out.is_contiguous(), "out [M][Hd] fp32")
+    if workspace is None:
+        workspace = torch.empty(max(1, cmc_bridge_workspace_bytes(M, F)), dtype=torch.uint8, device=h.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = lib().cmc_memory_bridge(_ptr(h), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(ln_gamma), _ptr(ln_beta),
+                                 float(nu), float(ln_eps), M, Hc, F, Hd, _ptr(out), _ptr(workspace), ws_bytes,
+                                 _stream(stream))
+    _check(rc)
+    return out
 
 
 # ------------------------------------------------------------- denoising

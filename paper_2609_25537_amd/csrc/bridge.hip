@@ -1,0 +1,226 @@
+// MemoryBridge (Sec. 2.2): each CME vector h (encoder width Hc) becomes a
+// decoder-ready memory row
+//   m_hat = LayerNorm(W2 GELU(W1 h + b1) + b2)          (LayerNorm per the appendix)
+//   m     = nu tanh(m_hat) * min(1, 2 nu / |nu tanh(m_hat)|)   (the section's cap)
+// -- the selection keys of Tier-1.
+//
+// gemm_nt_kernel: C[M][N] = A[M][K] . B[N][K]^T on MFMA, bf16 operands, fp32
+// accumulation.  A 256-thread workgroup computes a 128 x 128 tile, each wave
+// 64 x 64 as 4 x 4 v_mfma_f32_16x16x32_bf16 tiles.  K advances 64 at a time
+// through two LDS buffers: the next slice is loaded into registers while
+// the current one feeds the MFMAs, then stored to the other buffer.  LDS
+// rows are padded to 72 bf16 (144 bytes) so that the 16-byte fragment reads
+// of 8 consecutive rows hit 8 disjoint groups of 4 banks.  Tiles are handed
+// out so that each XCD (workgroups are dealt round-robin to the 8 XCDs)
+// runs a contiguous run of them, N fastest: the tiles resident on one XCD
+// share their A rows in that XCD's L2.
+//   Epilogue 0 (first layer): + b1, exact GELU, rounded to bf16 (the hidden
+//   activations, kept in the workspace).  Epilogue 1 (second layer): + b2,
+//   fp32 into the output.
+//
+// bridge_norm_kernel: one wave per output row, in place: mean and biased
+// variance (two passes), LayerNorm with gamma/beta, nu tanh, the row norm,
+// and the cap.  The row (Hd fp32) is re-read from cache between passes.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace cmc {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
+constexpr int kGemmThreads = 256;
+constexpr int kChunks = BM * BK / 8 / kGemmThreads;  // 16-byte loads per thread per matrix per slice
+
+struct GemmParams {
+    const uint16_t *A;  // [M][K]
+    const uint16_t *B;  // [N][K]
+    const float *bias;  // [N]
+    void *C;            // [M][N]: bf16 (epilogue 0) or fp32 (epilogue 1)
+    int M, N, K;
+};
+
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+
+__device__ __forceinline__ uint16_t to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDK];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // Tile order: physical workgroup b runs on XCD b % 8; give each XCD a
+    // contiguous run of logical tiles (N fastest).
+    const int tiles_n = p.N / BN;
+    const int tiles = gridDim.x;
+    const int per_xcd = (tiles + 7) / 8;
+    const int bid = blockIdx.x;
+    int t = (bid % 8) * per_xcd + bid / 8;
+    if ((tiles % 8) != 0) t = bid;  // uneven split: plain order
+    const int tm = t / tiles_n, tn = t % tiles_n;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    // Global -> register -> LDS staging: chunk c = tid + 256 i is row c / 8,
+    // 16-byte column group c % 8 of the 128 x 64 slice.
+    uint4 ra[kChunks], rb[kChunks];
+    const int crow0 = tid >> 3, ccol = (tid & 7) * 8;  // row of chunk i: crow0 + 32 i
+    const uint16_t *Ag = p.A + (size_t)ccol, *Bg = p.B + (size_t)n0 * p.K + (size_t)ccol;
+#define CMC_GLOAD(K0_)                                                                                   \
+    do {                                                                                                 \
+        _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
+            const int ar = min(m0 + crow0 + 32 * i, p.M - 1); /* rows past M: clamped, discarded */      \
+            ra[i] = *reinterpret_cast<const uint4 *>(Ag + (size_t)ar * p.K + (K0_));                    \
+            rb[i] = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + 32 * i) * p.K + (K0_));      \
+        }                                                                                                \
+    } while (0)
+#define CMC_SSTORE(BUF_)                                                                                 \
+    do {                                                                                                 \
+        _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
+            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + 32 * i) * LDK + ccol]) = ra[i];               \
+            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + 32 * i) * LDK + ccol]) = rb[i];               \
+        }                                                                                                \
+    } while (0)
+
+    floatx4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    const int KT = p.K / BK;
+    CMC_GLOAD(0);
+    CMC_SSTORE(0);
+    __syncthreads();
+    const int fr = lane & 15, fk = 8 * (lane >> 4);
+    for (int kt = 0; kt < KT; ++kt) {
+        const int buf = kt & 1;
+        // The last slice reloads itself (branch-free; the copy is never read).
+        CMC_GLOAD(min(kt + 1, KT - 1) * BK);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 32) {
+            bf16x8 a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm * 64 + i * 16 + fr) * LDK + kk + fk]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                b[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][(wn * 64 + j * 16 + fr) * LDK + kk + fk]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        CMC_SSTORE(buf ^ 1);
+        __syncthreads();
+    }
+
+#undef CMC_GLOAD
+#undef CMC_SSTORE
+
+    // C fragment: lane l, element r -> row 4 (l / 16) + r, column l % 16.
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int col = n0 + wn * 64 + j * 16 + fr;
+        const float bias = p.bias[col];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + r;
+                if (row < p.M) {
+                    const float v = acc[i][j][r] + bias;
+                    if constexpr (EPI == 0)
+                        static_cast<uint16_t *>(p.C)[(size_t)row * p.N + col] = to_bf16_rne(gelu_erf(v));
+                    else
+                        static_cast<float *>(p.C)[(size_t)row * p.N + col] = v;
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void bridge_norm_kernel(BridgeParams p) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= p.M) return;  // wave-uniform; no barriers
+    float *y = p.out + (size_t)row * p.Hd;
+    const int n4 = p.Hd / 4;
+    const float4 *y4 = reinterpret_cast<const float4 *>(y);
+    const float4 *g4 = reinterpret_cast<const float4 *>(p.ln_gamma);
+    const float4 *b4 = reinterpret_cast<const float4 *>(p.ln_beta);
+
+    float s = 0.f;
+    for (int c = lane; c < n4; c += kWave) {
+        const float4 v = y4[c];
+        s += (v.x + v.y) + (v.z + v.w);
+    }
+    const float mean = lane_reduce<OpSum, 1, kWave>(s) / (float)p.Hd;
+    float q = 0.f;
+    for (int c = lane; c < n4; c += kWave) {
+        const float4 v = y4[c];
+        const float a = v.x - mean, b = v.y - mean, d = v.z - mean, e = v.w - mean;
+        q = fmaf(a, a, q);
+        q = fmaf(b, b, q);
+        q = fmaf(d, d, q);
+        q = fmaf(e, e, q);
+    }
+    const float var = lane_reduce<OpSum, 1, kWave>(q) / (float)p.Hd;
+    const float inv = 1.f / sqrtf(var + p.eps);
+    auto capped = [&](int c) {
+        const float4 v = y4[c], g = g4[c], b = b4[c];
+        return float4{p.nu * tanhf(fmaf(g.x * (v.x - mean), inv, b.x)),
+                      p.nu * tanhf(fmaf(g.y * (v.y - mean), inv, b.y)),
+                      p.nu * tanhf(fmaf(g.z * (v.z - mean), inv, b.z)),
+                      p.nu * tanhf(fmaf(g.w * (v.w - mean), inv, b.w))};
+    };
+    float nn = 0.f;
+    for (int c = lane; c < n4; c += kWave) {
+        const float4 t = capped(c);
+        nn = fmaf(t.x, t.x, nn);
+        nn = fmaf(t.y, t.y, nn);
+        nn = fmaf(t.z, t.z, nn);
+        nn = fmaf(t.w, t.w, nn);
+    }
+    const float nrm = sqrtf(lane_reduce<OpSum, 1, kWave>(nn));
+    const float scale = (nrm > 0.f && 2.f * p.nu < nrm) ? 2.f * p.nu / nrm : 1.f;
+    // Each lane rewrites only the elements it reads.
+    for (int c = lane; c < n4; c += kWave) {
+        const float4 t = capped(c);
+        reinterpret_cast<float4 *>(y)[c] = float4{t.x * scale, t.y * scale, t.z * scale, t.w * scale};
+    }
+}
+
+hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
+    const long long tiles = (long long)((g.M + BM - 1) / BM) * (g.N / BN);
+    if (tiles == 0) return hipSuccess;
+    if (epi == 0)
+        gemm_nt_kernel<0><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+    else
+        gemm_nt_kernel<1><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_memory_bridge(const BridgeParams &p, hipStream_t stream) {
+    if (p.M == 0) return hipSuccess;
+    GemmParams g1{p.h, p.w1, p.b1, p.hidden, p.M, p.F, p.Hc};
+    hipError_t e = launch_gemm(0, g1, stream);
+    if (e != hipSuccess) return e;
+    GemmParams g2{p.hidden, p.w2, p.b2, p.out, p.M, p.Hd, p.F};
+    e = launch_gemm(1, g2, stream);
+    if (e != hipSuccess) return e;
+    bridge_norm_kernel<<<(p.M + 3) / 4, 256, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace cmc

@@ -219,6 +219,44 @@ cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const in
     return ok();
 }
 
+// ----------------------------------------------------------- MemoryBridge
+
+size_t cmc_bridge_workspace_bytes(int M, int F) {
+    if (M < 0 || F < 0) return 0;
+    return align256((size_t)M * (size_t)F * sizeof(uint16_t));
+}
+
+cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1, const void *w2, const float *b2,
+                             const float *ln_gamma, const float *ln_beta, float nu, float ln_eps, int M, int Hc,
+                             int F, int Hd, float *out, void *workspace, size_t workspace_bytes, void *stream) {
+    if (M < 0 || Hc < 1 || F < 1 || Hd < 1)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "bridge: need M >= 0 and Hc, F, Hd >= 1");
+    if (!(nu > 0.f) || isinf(nu) || !(ln_eps >= 0.f) || isinf(ln_eps))
+        return fail(CMC_ERR_INVALID_ARGUMENT, "bridge: need a finite nu > 0 and a finite eps >= 0");
+    if (Hc % cmc::kBridgeK != 0 || F % cmc::kBridgeN != 0 || Hd % cmc::kBridgeN != 0)
+        return fail(CMC_ERR_UNSUPPORTED, "bridge: need Hc %% %d == 0 and F, Hd %% %d == 0 (got Hc=%d F=%d Hd=%d)",
+                    cmc::kBridgeK, cmc::kBridgeN, Hc, F, Hd);
+    if ((long long)((M + 127) / 128) * (F / cmc::kBridgeN) > 0x7fffffffLL ||
+        (long long)((M + 127) / 128) * (Hd / cmc::kBridgeN) > 0x7fffffffLL)
+        return fail(CMC_ERR_UNSUPPORTED, "bridge: M=%d too large", M);
+    if (M == 0) return ok();
+    if (!h || !w1 || !b1 || !w2 || !b2 || !ln_gamma || !ln_beta || !out)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "bridge: null pointer");
+    if (misaligned(h) || misaligned(w1) || misaligned(b1) || misaligned(w2) || misaligned(b2) ||
+        misaligned(ln_gamma) || misaligned(ln_beta) || misaligned(out) || misaligned(workspace))
+        return fail(CMC_ERR_UNSUPPORTED, "bridge: every pointer must be 16-byte aligned");
+    const size_t need = cmc_bridge_workspace_bytes(M, F);
+    if (!workspace || workspace_bytes < need)
+        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "bridge: workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    cmc::BridgeParams p{static_cast<const uint16_t *>(h), static_cast<const uint16_t *>(w1), b1,
+                        static_cast<const uint16_t *>(w2), b2, ln_gamma, ln_beta, static_cast<uint16_t *>(workspace),
+                        out, M, Hc, F, Hd, nu, ln_eps};
+    hipError_t e = cmc::launch_memory_bridge(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "bridge launch");
+    return ok();
+}
+
 // ------------------------------------------------------------- denoising
 
 size_t cmc_denoise_workspace_bytes(int B, int n) {

@@ -99,6 +99,24 @@ struct DenoiseParams {
     int keep_min_every, chunk_tokens, max_chunks;
 };
 constexpr int kDenoiseMaxG = 4;
+
+struct BridgeParams {
+    const uint16_t *h;          // [M][Hc] bf16 CME vectors
+    const uint16_t *w1;         // [F][Hc] bf16
+    const float *b1;            // [F]
+    const uint16_t *w2;         // [Hd][F] bf16
+    const float *b2;            // [Hd]
+    const float *ln_gamma;      // [Hd]
+    const float *ln_beta;       // [Hd]
+    uint16_t *hidden;           // [M][F] bf16 (workspace)
+    float *out;                 // [M][Hd]
+    int M, Hc, F, Hd;
+    float nu, eps;
+};
+// Tile multiples of the MemoryBridge GEMMs: Hc (K of the first) a multiple of
+// kBridgeK, F and Hd (N of both, K of the second) multiples of kBridgeN.
+constexpr int kBridgeK = 64, kBridgeN = 128;
+hipError_t launch_memory_bridge(const BridgeParams &p, hipStream_t stream);
 hipError_t launch_denoise(const DenoiseParams &p, bool bf16, hipStream_t stream);
 
 }  // namespace cmc

@@ -402,3 +402,62 @@ def denoise_emb(w: DenoiseWorkload, b: Optional[int] = None) -> np.ndarray:
     for i in range(1, w.n):
         e[i] = np.float32(0.6) * e[i - 1] + np.float32(0.8) * z[i] if link[i] else z[i]
     return f32_to_bf16_bits(e) if w.dtype == "bf16" else e
+
+
+# ----------------------------------------------------------- MemoryBridge
+
+@dataclasses.dataclass(frozen=True)
+class BridgeWorkload:
+    """MemoryBridge inputs (Sec. 2.2): M CME vectors of the encoder width Hc
+    projected through hidden width F to the decoder width Hd.  Weights are
+    nn.Linear-scaled draws (N(0, 1/fan_in)), biases N(0, 0.02^2), LayerNorm
+    gamma 1 + N(0, 0.1^2) and beta N(0, 0.1^2), all rounded to bf16 where
+    the kernel reads bf16; nu = s * nu_bar."""
+
+    name: str
+    M: int
+    Hc: int
+    F: int
+    Hd: int
+    seed: int
+    nu: float = 1.0
+    eps: float = 1e-5
+
+    def replace(self, **kw) -> "BridgeWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+BRIDGE_WORKLOADS: Dict[str, BridgeWorkload] = {
+    # 64 GPT2-Large contexts of 3072 tokens: 12 chunks of 256 tokens at ratio 4
+    # -> 64 CMEs per chunk, 768 per context; projected into Llama-3-8B's width.
+    "bridge_gpt2l_llama3_batch64": BridgeWorkload("bridge_gpt2l_llama3_batch64", M=64 * 768, Hc=1280, F=4096,
+                                                  Hd=4096, seed=808),
+}
+
+
+def bridge_params(w: BridgeWorkload) -> Dict[str, np.ndarray]:
+    """Weights: w1 [F][Hc], w2 [Hd][F] (bf16 bits), b1 [F], b2, gamma, beta [Hd] (fp32)."""
+    return {
+        "w1": f32_to_bf16_bits(normal_f32(w.seed, "cme_k", (1,), (w.F, w.Hc), 1.0 / math.sqrt(w.Hc))),
+        "w2": f32_to_bf16_bits(normal_f32(w.seed, "cme_v", (1,), (w.Hd, w.F), 1.0 / math.sqrt(w.F))),
+        "b1": normal_f32(w.seed, "cme_k", (2,), (w.F,), 0.02),
+        "b2": normal_f32(w.seed, "cme_v", (2,), (w.Hd,), 0.02),
+        "gamma": (1.0 + normal_f32(w.seed, "chan", (1,), (w.Hd,), 0.1)).astype(np.float32),
+        "beta": normal_f32(w.seed, "chan", (2,), (w.Hd,), 0.1),
+    }
+
+
+def bridge_h(w: BridgeWorkload, rows: Optional[Sequence[int]] = None) -> np.ndarray:
+    """CME vectors [M][Hc] (bf16 bits), N(0, 1), drawn in blocks of 1024 rows
+    so that any row can be regenerated alone (rows=None: all)."""
+    blk = 1024
+    if rows is None:
+        out = np.empty((w.M, w.Hc), np.uint16)
+        for b0 in range(0, w.M, blk):
+            n = min(blk, w.M - b0)
+            out[b0:b0 + n] = f32_to_bf16_bits(normal_f32(w.seed, "emb", (b0 // blk,), (blk, w.Hc))[:n])
+        return out
+    out = np.empty((len(rows), w.Hc), np.uint16)
+    for i, r in enumerate(rows):
+        out[i] = f32_to_bf16_bits(normal_f32(w.seed, "emb", (r // blk,), (blk, w.Hc))[r % blk])
+    return out

@@ -609,6 +609,83 @@ def pin_denoise_floor_properties(orc):
                     assert set(kept) == passing
 
 
+def _bf16_vals(bits):
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def pin_bridge_library(orc):
+    """MemoryBridge's MLP and LayerNorm against torch's Linear / exact GELU /
+    Linear / layer_norm in fp64 on the same bf16 weights; the cap is then
+    applied to torch's LayerNorm output (the cap itself is pinned by
+    pin_bridge_cap_cases)."""
+    import torch
+    rng = np.random.default_rng(71)
+    M, Hc, F, Hd, nu = 5, 24, 40, 16, 0.7
+    h = _bf16(rng.standard_normal((M, Hc)).astype(np.float32))
+    w1 = _bf16((rng.standard_normal((F, Hc)) / np.sqrt(Hc)).astype(np.float32))
+    w2 = _bf16((rng.standard_normal((Hd, F)) / np.sqrt(F)).astype(np.float32))
+    b1, b2 = rng.standard_normal(F).astype(np.float32), rng.standard_normal(Hd).astype(np.float32)
+    gamma, beta = rng.uniform(0.5, 2, Hd).astype(np.float32), rng.standard_normal(Hd).astype(np.float32)
+    T = lambda x: torch.from_numpy(np.asarray(x, np.float64))
+    hid = torch.nn.functional.gelu(T(_bf16_vals(h)) @ T(_bf16_vals(w1)).T + T(b1), approximate="none")
+    _close(orc.bridge_hidden(h, w1, b1), hid.numpy(), 1e-12, "bridge hidden")
+    y = hid @ T(_bf16_vals(w2)).T + T(b2)
+    m_hat = torch.nn.functional.layer_norm(y, (Hd,), T(gamma), T(beta), eps=1e-5)
+    t = nu * torch.tanh(m_hat)
+    ref = t * torch.clamp(2 * nu / t.norm(dim=1, keepdim=True), max=1.0)
+    _close(orc.bridge_out(hid.numpy(), w2, b2, gamma, beta, nu), ref.numpy(), 1e-12, "bridge out")
+
+
+def pin_bridge_cap_cases(orc):
+    """Hand-checked cases of LayerNorm + cap (output weights zero, so y is
+    the bias vector):
+      * constant y: LayerNorm gives beta; small beta stays below the cap, so
+        the output is exactly nu * tanh(beta);
+      * y = (1, 2, 3, 4), gamma = 1, beta = 0, eps = 0: mean 2.5, biased
+        variance 1.25, m_hat = (y - 2.5) / sqrt(1.25); the norm of
+        tanh(m_hat) is below 2, so the output is tanh(m_hat) (nu = 1);
+      * saturated: beta = +-30 in 16 coordinates: tanh = +-1, the norm is
+        4 nu > 2 nu, so every coordinate becomes +-nu / 2."""
+    def run(b2, gamma, beta, nu, eps):
+        Hd = len(b2)
+        zero_w2 = np.zeros((Hd, 3), np.uint16)
+        return orc.bridge_out(np.ones((1, 3)), zero_w2, np.asarray(b2, np.float32), np.asarray(gamma, np.float32),
+                              np.asarray(beta, np.float32), nu, eps)[0]
+    beta = np.array([0.1, -0.2, 0.05, 0.0, 0.3], np.float32)
+    out = run([2.0] * 5, [3.0] * 5, beta, 0.8, 1e-5)
+    assert np.allclose(out, [0.8 * math.tanh(float(b)) for b in beta], rtol=0, atol=1e-15), out
+    out = run([1.0, 2.0, 3.0, 4.0], [1.0] * 4, [0.0] * 4, 1.0, 0.0)
+    want = [math.tanh((v - 2.5) / math.sqrt(1.25)) for v in (1.0, 2.0, 3.0, 4.0)]
+    assert np.allclose(out, want, rtol=0, atol=1e-15), (out, want)
+    sgn = np.array([1 if i % 3 else -1 for i in range(16)], np.float32)
+    out = run([0.0] * 16, [1.0] * 16, 30.0 * sgn, 0.6, 1e-5)
+    assert np.allclose(out, 0.3 * sgn.astype(np.float64), rtol=0, atol=1e-15), out
+
+
+def pin_bridge_bounds(orc):
+    """The cap's guarantees on random large activations: every coordinate
+    within nu, every row's norm within 2 nu, and rows whose nu*tanh norm is
+    below 2 nu untouched (checked by scaling nu up until no row is capped)."""
+    rng = np.random.default_rng(72)
+    M, F, Hd = 20, 12, 64
+    hid = rng.standard_normal((M, F)) * 5
+    w2 = _bf16(rng.standard_normal((Hd, F)).astype(np.float32))
+    b2 = rng.standard_normal(Hd).astype(np.float32)
+    gamma = rng.uniform(1, 10, Hd).astype(np.float32)
+    beta = rng.standard_normal(Hd).astype(np.float32)
+    for nu in (0.1, 1.0, 7.5):
+        out = orc.bridge_out(hid, w2, b2, gamma, beta, nu)
+        assert (np.abs(out) <= nu * (1 + 1e-12)).all()
+        assert (np.linalg.norm(out, axis=1) <= 2 * nu * (1 + 1e-12)).all()
+        assert (np.linalg.norm(out, axis=1) >= 2 * nu * (1 - 1e-12)).any() or nu > 1
+    # nu * tanh(x) has norm <= nu * sqrt(Hd) = 8 nu: with Hd = 64 every row is capped unless small;
+    # with Hd = 3 the norm is at most nu * sqrt(3) < 2 nu, so the cap never acts.
+    w3 = _bf16(rng.standard_normal((3, F)).astype(np.float32))
+    out3 = orc.bridge_out(hid, w3, b2[:3], gamma[:3], beta[:3], 0.5)
+    ref3 = orc.bridge_out(hid, w3, b2[:3], gamma[:3], beta[:3], 0.5)
+    assert (np.linalg.norm(out3, axis=1) < 1.0).all() and np.array_equal(out3, ref3)
+
+
 ALL_PINS = [v for n, v in sorted(globals().items()) if n.startswith("pin_") and callable(v)]
 
 

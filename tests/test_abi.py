@@ -232,3 +232,31 @@ def test_denoise_workspace_query():
     assert cmc.cmc_denoise_workspace_bytes(3, 1000) >= 3000
     assert cmc.cmc_denoise_workspace_bytes(-1, 10) == 0
     assert _den(B=0) == cmc.CMC_OK
+
+
+def _bridge(**kw):
+    a = dict(h=FAKE, w1=FAKE, b1=FAKE, w2=FAKE, b2=FAKE, g=FAKE, be=FAKE, nu=1.0, eps=1e-5, M=10, Hc=64, F=128,
+             Hd=128, out=FAKE, ws=FAKE, wsb=1 << 20, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_memory_bridge(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hc=96), cmc.CMC_ERR_UNSUPPORTED),                   # Hc % 64
+    (dict(F=192), cmc.CMC_ERR_UNSUPPORTED),                   # F % 128
+    (dict(Hd=64), cmc.CMC_ERR_UNSUPPORTED),                   # Hd % 128
+    (dict(nu=0.0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(nu=float("inf")), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(eps=-1.0), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(M=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(b2=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(w1=FAKE + 2), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(wsb=100), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+])
+def test_bridge_validation(kw, code):
+    assert _bridge(**kw) == code
+
+
+def test_bridge_empty_and_workspace():
+    assert _bridge(M=0, h=None) == cmc.CMC_OK
+    assert cmc.cmc_bridge_workspace_bytes(10, 128) >= 10 * 128 * 2

@@ -60,6 +60,20 @@ MUTANTS = [
     ("denoise_floor_start", "int last = -1, count = 0;", "int last = 0, count = 0;"),
     ("denoise_upstream_norm", "double c = dot / (fmax(ni, 1e-8) * fmax(sqrt(nj), 1e-8));",
      "double c = dot / (fmax(ni, 1e-8) * fmax(ni, 1e-8));"),
+    ("bridge_gelu_tanh_form", "return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+     "return 0.5 * x * (1.0 + tanh(0.7978845608028654 * (x + 0.044715 * x * x * x)));"),
+    ("bridge_no_hidden_bias", "double u = (double)b1[f];", "double u = 0.0;"),
+    ("bridge_no_output_bias", "double acc = (double)b2[j];", "double acc = 0.0;"),
+    ("bridge_w2_transposed", "acc += hidden[(size_t)r * F + f] * widen_bf16(w2[(size_t)j * F + f]);",
+     "acc += hidden[(size_t)r * F + f] * widen_bf16(w2[((size_t)f * Hd + j) % ((size_t)Hd * F)]);"),
+    ("bridge_unbiased_variance", "var /= Hd;", "var /= (Hd > 1 ? Hd - 1 : 1);"),
+    ("bridge_eps_outside_sqrt", "double inv = 1.0 / sqrt(var + eps);", "double inv = 1.0 / (sqrt(var) + eps);"),
+    ("bridge_cap_at_nu", "double c = (nrm > 0.0 && 2.0 * nu / nrm < 1.0) ? 2.0 * nu / nrm : 1.0;",
+     "double c = (nrm > 0.0 && nu / nrm < 1.0) ? nu / nrm : 1.0;"),
+    ("bridge_gamma_beta_swapped",
+     "double m_hat = (double)gamma[j] * (y[j] - mean) * inv + (double)beta[j];",
+     "double m_hat = (double)beta[j] * (y[j] - mean) * inv + (double)gamma[j];"),
+    ("bridge_no_tanh", "y[j] = nu * tanh(m_hat);", "y[j] = nu * m_hat;"),
     ("denoise_chunk_first_token", "int v = c < nc ? kept_idx[(size_t)b * n + (size_t)c * chunk_tokens] : -1;",
      "int v = c < nc ? kept_idx[(size_t)b * n + (size_t)c] : -1;"),
 ]
