@@ -5,12 +5,14 @@
 // -- the selection keys of Tier-1.
 //
 // gemm_nt_kernel: C[M][N] = A[M][K] . B[N][K]^T on MFMA, bf16 operands, fp32
-// accumulation.  A 256-thread workgroup computes a 128 x 128 tile, each wave
-// 64 x 64 as 4 x 4 v_mfma_f32_16x16x32_bf16 tiles.  K advances 64 at a time
+// accumulation.  A 256-thread workgroup of 2 x 2 waves computes a 2WT x 2WT
+// tile, each wave WT x WT as (WT/16)^2 v_mfma_f32_16x16x32_bf16 tiles (WT =
+// 64 by default; WT = 128 halves the LDS reads per MFMA flop but leaves one
+// workgroup per CU, and measured no faster).  K advances BK at a time
 // through two LDS buffers: the next slice is loaded into registers while
 // the current one feeds the MFMAs, then stored to the other buffer.  LDS
-// rows are padded to 72 bf16 (144 bytes) so that the 16-byte fragment reads
-// of 8 consecutive rows hit 8 disjoint groups of 4 banks.  Tiles are handed
+// rows are padded by 8 bf16 (80 or 144 bytes) so that the 16-byte fragment
+// reads of 8 consecutive rows hit 8 disjoint groups of 4 banks.  Tiles are handed
 // out so that each XCD (workgroups are dealt round-robin to the 8 XCDs)
 // runs a contiguous run of them, N fastest: the tiles resident on one XCD
 // share their A rows in that XCD's L2.
@@ -18,9 +20,9 @@
 //   activations, kept in the workspace).  Epilogue 1 (second layer): + b2,
 //   fp32 into the output.
 //
-// bridge_norm_kernel: one wave per output row, in place: mean and biased
-// variance (two passes), LayerNorm with gamma/beta, nu tanh, the row norm,
-// and the cap.  The row (Hd fp32) is re-read from cache between passes.
+// bridge_norm_kernel: one wave per output row, in place, the row held in
+// registers: mean and biased variance (two passes over the registers),
+// LayerNorm with gamma/beta, nu tanh, the row norm, and the cap.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -31,9 +33,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
-constexpr int kGemmThreads = 256;
-constexpr int kChunks = BM * BK / 8 / kGemmThreads;  // 16-byte loads per thread per matrix per slice
+constexpr int kGemmThreads = 256;  // 2 x 2 waves
 
 struct GemmParams {
     const uint16_t *A;  // [M][K]
@@ -50,8 +50,14 @@ __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-template <int EPI>
+// WT x WT per wave (4 x 4 or 8 x 8 MFMA tiles of 16 x 16), BK of K per LDS
+// slice; the workgroup tile is 2 WT x 2 WT.
+template <int EPI, int WT, int BK>
 __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
+    constexpr int BM = 2 * WT, BN = 2 * WT, LDK = BK + 8, T = WT / 16;
+    constexpr int kRowChunks = BK / 8;                            // 16-byte chunks per tile row
+    constexpr int kChunks = BM * kRowChunks / kGemmThreads;       // per thread per matrix per slice
+    constexpr int kRowsPerPass = kGemmThreads / kRowChunks;
     __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDK];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -68,74 +74,76 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
     const int tm = t / tiles_n, tn = t % tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // Global -> register -> LDS staging: chunk c = tid + 256 i is row c / 8,
-    // 16-byte column group c % 8 of the 128 x 64 slice.
+    // Global -> register -> LDS staging: chunk c = tid + 256 i is row
+    // c / kRowChunks, 16-byte column group c % kRowChunks of the BM x BK slice.
+    // One register stage: slice j + 1 is loaded while slice j feeds the MFMAs.
     uint4 ra[kChunks], rb[kChunks];
-    const int crow0 = tid >> 3, ccol = (tid & 7) * 8;  // row of chunk i: crow0 + 32 i
+    const int crow0 = tid / kRowChunks, ccol = (tid % kRowChunks) * 8;
     const uint16_t *Ag = p.A + (size_t)ccol, *Bg = p.B + (size_t)n0 * p.K + (size_t)ccol;
 #define CMC_GLOAD(K0_)                                                                                   \
     do {                                                                                                 \
         _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
-            const int ar = min(m0 + crow0 + 32 * i, p.M - 1); /* rows past M: clamped, discarded */      \
+            const int ar = min(m0 + crow0 + kRowsPerPass * i, p.M - 1); /* past M: clamped, discarded */ \
             ra[i] = *reinterpret_cast<const uint4 *>(Ag + (size_t)ar * p.K + (K0_));                    \
-            rb[i] = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + 32 * i) * p.K + (K0_));      \
+            rb[i] = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + kRowsPerPass * i) * p.K + (K0_)); \
         }                                                                                                \
     } while (0)
 #define CMC_SSTORE(BUF_)                                                                                 \
     do {                                                                                                 \
         _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
-            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + 32 * i) * LDK + ccol]) = ra[i];               \
-            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + 32 * i) * LDK + ccol]) = rb[i];               \
+            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = ra[i];     \
+            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = rb[i];     \
         }                                                                                                \
     } while (0)
 
-    floatx4 acc[4][4];
+    floatx4 acc[T][T];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < T; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < T; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const int KT = p.K / BK;
+    const int fr = lane & 15, fk = 8 * (lane >> 4);
     CMC_GLOAD(0);
     CMC_SSTORE(0);
     __syncthreads();
-    const int fr = lane & 15, fk = 8 * (lane >> 4);
-    for (int kt = 0; kt < KT; ++kt) {
-        const int buf = kt & 1;
-        // The last slice reloads itself (branch-free; the copy is never read).
-        CMC_GLOAD(min(kt + 1, KT - 1) * BK);
+    for (int j = 0; j < KT; ++j) {
+        const int buf = j & 1;
+        // The last slice reloads itself: no load sits behind a branch (a
+        // conditional load here made the compiler keep the staging registers
+        // in scratch memory); the copy is never read.
+        CMC_GLOAD(min(j + 1, KT - 1) * BK);
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 32) {
-            bf16x8 a[4], b[4];
+            bf16x8 a[T], b[T];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm * 64 + i * 16 + fr) * LDK + kk + fk]);
+            for (int i = 0; i < T; ++i)
+                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm * WT + i * 16 + fr) * LDK + kk + fk]);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                b[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][(wn * 64 + j * 16 + fr) * LDK + kk + fk]);
+            for (int jj = 0; jj < T; ++jj)
+                b[jj] = *reinterpret_cast<const bf16x8 *>(&sB[buf][(wn * WT + jj * 16 + fr) * LDK + kk + fk]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < T; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                for (int jj = 0; jj < T; ++jj)
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
         }
         CMC_SSTORE(buf ^ 1);
         __syncthreads();
     }
-
 #undef CMC_GLOAD
 #undef CMC_SSTORE
 
     // C fragment: lane l, element r -> row 4 (l / 16) + r, column l % 16.
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int col = n0 + wn * 64 + j * 16 + fr;
+    for (int j = 0; j < T; ++j) {
+        const int col = n0 + wn * WT + j * 16 + fr;
         const float bias = p.bias[col];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < T; ++i) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + r;
+                const int row = m0 + wm * WT + i * 16 + 4 * (lane >> 4) + r;
                 if (row < p.M) {
                     const float v = acc[i][j][r] + bias;
                     if constexpr (EPI == 0)
@@ -148,7 +156,66 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
     }
 }
 
+// One wave per row; the row stays in registers (NV float4 per lane, Hd <=
+// 256 NV): one read and one write of the row.
+template <int NV>
 __global__ __launch_bounds__(256) void bridge_norm_kernel(BridgeParams p) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= p.M) return;  // wave-uniform; no barriers
+    float4 *y4 = reinterpret_cast<float4 *>(p.out + (size_t)row * p.Hd);
+    const float4 *g4 = reinterpret_cast<const float4 *>(p.ln_gamma);
+    const float4 *b4 = reinterpret_cast<const float4 *>(p.ln_beta);
+    const int n4 = p.Hd / 4;
+    float4 v[NV];
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        const int c = lane + u * kWave;
+        v[u] = c < n4 ? y4[c] : float4{0.f, 0.f, 0.f, 0.f};
+        s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+    }
+    const float mean = lane_reduce<OpSum, 1, kWave>(s) / (float)p.Hd;
+    float q = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        if (lane + u * kWave < n4) {
+            const float a = v[u].x - mean, b = v[u].y - mean, d = v[u].z - mean, e = v[u].w - mean;
+            q = fmaf(a, a, q);
+            q = fmaf(b, b, q);
+            q = fmaf(d, d, q);
+            q = fmaf(e, e, q);
+        }
+    }
+    const float var = lane_reduce<OpSum, 1, kWave>(q) / (float)p.Hd;
+    const float inv = 1.f / sqrtf(var + p.eps);
+    float nn = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        const int c = lane + u * kWave;
+        if (c < n4) {
+            const float4 g = g4[c], b = b4[c];
+            v[u] = float4{p.nu * tanhf(fmaf(g.x * (v[u].x - mean), inv, b.x)),
+                          p.nu * tanhf(fmaf(g.y * (v[u].y - mean), inv, b.y)),
+                          p.nu * tanhf(fmaf(g.z * (v[u].z - mean), inv, b.z)),
+                          p.nu * tanhf(fmaf(g.w * (v[u].w - mean), inv, b.w))};
+            nn = fmaf(v[u].x, v[u].x, nn);
+            nn = fmaf(v[u].y, v[u].y, nn);
+            nn = fmaf(v[u].z, v[u].z, nn);
+            nn = fmaf(v[u].w, v[u].w, nn);
+        }
+    }
+    const float nrm = sqrtf(lane_reduce<OpSum, 1, kWave>(nn));
+    const float scale = (nrm > 0.f && 2.f * p.nu < nrm) ? 2.f * p.nu / nrm : 1.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+        const int c = lane + u * kWave;
+        if (c < n4) y4[c] = float4{v[u].x * scale, v[u].y * scale, v[u].z * scale, v[u].w * scale};
+    }
+}
+
+// Rows wider than 256 * 16: the same steps re-reading the row from cache.
+__global__ __launch_bounds__(256) void bridge_norm_wide_kernel(BridgeParams p) {
     const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= p.M) return;  // wave-uniform; no barriers
@@ -157,7 +224,6 @@ __global__ __launch_bounds__(256) void bridge_norm_kernel(BridgeParams p) {
     const float4 *y4 = reinterpret_cast<const float4 *>(y);
     const float4 *g4 = reinterpret_cast<const float4 *>(p.ln_gamma);
     const float4 *b4 = reinterpret_cast<const float4 *>(p.ln_beta);
-
     float s = 0.f;
     for (int c = lane; c < n4; c += kWave) {
         const float4 v = y4[c];
@@ -199,14 +265,44 @@ __global__ __launch_bounds__(256) void bridge_norm_kernel(BridgeParams p) {
     }
 }
 
-hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
+hipError_t launch_norm(const BridgeParams &p, hipStream_t stream) {
+    const unsigned grid = (unsigned)((p.M + 3) / 4);
+    if (p.Hd <= 256 * 4)
+        bridge_norm_kernel<4><<<grid, 256, 0, stream>>>(p);
+    else if (p.Hd <= 256 * 8)
+        bridge_norm_kernel<8><<<grid, 256, 0, stream>>>(p);
+    else if (p.Hd <= 256 * 16)
+        bridge_norm_kernel<16><<<grid, 256, 0, stream>>>(p);
+    else
+        bridge_norm_wide_kernel<<<grid, 256, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
+// Build-time tuning knob: wave tile of the bridge GEMMs, 64 (128 x 128 per
+// workgroup, two workgroups per CU) or 128 (256 x 256, one per CU; for N a
+// multiple of 256).  Measured on the 49152 x 1280 -> 4096 -> 4096 workload:
+// 64 is slightly faster; both are held back by global-load latency with one
+// slice in flight.
+#ifndef CMC_BRIDGE_WAVE_TILE
+#define CMC_BRIDGE_WAVE_TILE 64
+#endif
+
+template <int WT, int BK>
+hipError_t launch_gemm_t(int epi, const GemmParams &g, hipStream_t stream) {
+    constexpr int BM = 2 * WT, BN = 2 * WT;
+    if (g.N % BN != 0 || g.K % BK != 0) return hipErrorInvalidValue;
     const long long tiles = (long long)((g.M + BM - 1) / BM) * (g.N / BN);
     if (tiles == 0) return hipSuccess;
     if (epi == 0)
-        gemm_nt_kernel<0><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<0, WT, BK><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
     else
-        gemm_nt_kernel<1><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<1, WT, BK><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
     return hipGetLastError();
+}
+
+hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
+    if (CMC_BRIDGE_WAVE_TILE == 128 && g.N % 256 == 0) return launch_gemm_t<128, 32>(epi, g, stream);
+    return launch_gemm_t<64, 64>(epi, g, stream);
 }
 
 }  // namespace
@@ -219,8 +315,7 @@ hipError_t launch_memory_bridge(const BridgeParams &p, hipStream_t stream) {
     GemmParams g2{p.hidden, p.w2, p.b2, p.out, p.M, p.Hd, p.F};
     e = launch_gemm(1, g2, stream);
     if (e != hipSuccess) return e;
-    bridge_norm_kernel<<<(p.M + 3) / 4, 256, 0, stream>>>(p);
-    return hipGetLastError();
+    return launch_norm(p, stream);
 }
 
 }  // namespace cmc
