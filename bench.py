@@ -122,6 +122,9 @@ class Inputs:
         from paper_2609_25537_amd import cmc
         self.sel_ws = torch.empty(max(1, cmc.cmc_select_workspace_bytes(w.B, w.N)), dtype=torch.uint8, device=dev)
         self.dec_ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.idx_stride, w.W, dev)
+        # Tier-1 rows gathered once per question into contiguous blocks.
+        self.gk = torch.empty((w.B, w.Hkv, w.idx_stride, w.Dh), dtype=self.pk.dtype, device=dev)
+        self.gv = torch.empty_like(self.gk)
 
     def select(self):
         from paper_2609_25537_amd import cmc
@@ -132,21 +135,24 @@ class Inputs:
                                        workspace=self.sel_ws)
         else:
             cmc.cmc_select_cmes(self.keys, self.qv, w.k, idx_out=self.idx, workspace=self.sel_ws)
+        cmc.cmc_gather_tier1(self.pk, self.pv, self.idx, w.idx_stride, k_len=self.k_out if w.ragged else None,
+                             out_k=self.gk, out_v=self.gv)
 
     def decode_step(self, j):
         from paper_2609_25537_amd import cmc
         w = self.w
         if w.ragged:
-            cmc.cmc_decode_step_ragged(self.q[j], self.pk, self.pv, self.idx, self.k_out, w.idx_stride, self.wk,
+            cmc.cmc_decode_step_ragged(self.q[j], self.gk, self.gv, None, self.k_out, w.idx_stride, self.wk,
                                        self.wv, self.wc, self.nk[j], self.nv[j], w.scale, out=self.out,
                                        workspace=self.dec_ws)
         else:
-            cmc.cmc_decode_step(self.q[j], self.pk, self.pv, self.idx, w.k, self.wk, self.wv, self.wc, self.nk[j],
+            cmc.cmc_decode_step(self.q[j], self.gk, self.gv, None, w.k, self.wk, self.wv, self.wc, self.nk[j],
                                 self.nv[j], w.scale, out=self.out, workspace=self.dec_ws)
 
 
 def run_pass(inp: Inputs, steps: int):
-    """One pass of the hot path: select once, then `steps` decode iterations."""
+    """One pass of the hot path: select (and gather the selected rows) once,
+    then `steps` decode iterations."""
     inp.select()
     for t in range(steps):
         inp.decode_step(t % inp.P)
@@ -155,8 +161,9 @@ def run_pass(inp: Inputs, steps: int):
 def decode_bytes(w) -> int:
     """Algorithmic bytes of one decode-step launch with the ring full: K and
     V of the k + W keys of each sequence (the newest row read from the
-    appended input; a ragged sequence has its own k_b + q_b pool rows), the
-    appended row written into the ring, q, out and the index entries."""
+    appended input; a ragged sequence has its own k_b + q_b pool rows, read
+    from the gathered Tier-1 block), the appended row written into the ring,
+    q and out."""
     from paper_2609_25537_amd import workloads as wl
     if w.ragged:
         rs = wl.ragged_sizes(w)
@@ -166,7 +173,7 @@ def decode_bytes(w) -> int:
     row = w.Dh * w.kv_bytes * 2
     kv = w.Hkv * (pool + w.B * w.W) * row
     ring_write = w.B * w.Hkv * row
-    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2 + pool * 4
+    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2
 
 
 def capture(fn):
@@ -302,6 +309,8 @@ class StackLayer:
         self.q = [dn("q", (layer, t), (w.B, w.Hq, w.Dh), torch.float32) for t in range(P)]
         self.nk = [dn("new_k", (layer, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]
         self.nv = [dn("new_v", (layer, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]
+        self.gk = torch.empty((w.B, w.Hkv, w.k, w.Dh), dtype=bf, device=dev)  # gathered Tier-1 rows
+        self.gv = torch.empty_like(self.gk)
 
 
 def run_stack(args, w, dev):
@@ -329,15 +338,20 @@ def run_stack(args, w, dev):
     def step_fn(j):
         def f():
             for Ly in layers:
-                cmc.cmc_decode_step(Ly.q[j], Ly.pk, Ly.pv, idx, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
+                cmc.cmc_decode_step(Ly.q[j], Ly.gk, Ly.gv, None, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
                                     w.scale, out=out, workspace=ws)
         return f
 
-    cmc.cmc_select_cmes(keys, qv, w.k, idx_out=idx, workspace=sel_ws)
+    def select_and_gather():
+        cmc.cmc_select_cmes(keys, qv, w.k, idx_out=idx, workspace=sel_ws)
+        for Ly in layers:
+            cmc.cmc_gather_tier1(Ly.pk, Ly.pv, idx, w.k, out_k=Ly.gk, out_v=Ly.gv)
+
+    select_and_gather()
     graphs = [capture(step_fn(j)) for j in range(P)]
 
     def one_pass():
-        cmc.cmc_select_cmes(keys, qv, w.k, idx_out=idx, workspace=sel_ws)
+        select_and_gather()
         for t in range(steps):
             graphs[t % P].replay()
 
@@ -361,7 +375,7 @@ def run_stack(args, w, dev):
     def launches():
         for r in range(args.launch_reps):
             Ly, j = layers[r % len(layers)], (r // len(layers)) % P
-            cmc.cmc_decode_step(Ly.q[j], Ly.pk, Ly.pv, idx, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
+            cmc.cmc_decode_step(Ly.q[j], Ly.gk, Ly.gv, None, w.k, Ly.wk, Ly.wv, Ly.wc, Ly.nk[j], Ly.nv[j],
                                 w.scale, out=out, workspace=ws)
     g = capture(launches)
     g.replay()

@@ -12,6 +12,7 @@
  * with the cache bounded by K + W + |q| at every generation step.  This
  * library implements the per-step hot path of that policy:
  *   cmc_select_cmes      Tier-1 scoring and top-K selection (once per question)
+ *   cmc_gather_tier1     copy the selected rows' K/V into one block (once per question)
  *   cmc_window_append    Tier-2 ring-buffer append (every step)
  *   cmc_two_tier_decode  decode attention over [selected rows || window]
  *   cmc_decode_step      append + decode fused into one launch (every step)
@@ -248,6 +249,29 @@ cmc_status cmc_denoise(const void *emb, cmc_dtype dtype, const int32_t *n_tokens
                        float *max_cos_out, uint8_t *keep_out, int32_t *kept_idx, int32_t *kept_count,
                        int32_t *chunk_offset, int32_t *n_chunks_out,
                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Tier-1 gather (Sec. 2.5, KV cache assembly: the cache holds the selected
+ * rows M* as one block): copies, once per question, the K/V rows of the
+ * selected memory rows into a contiguous block,
+ *   out_k[b][h][j][:] = cme_k[b][h][idx[b][j]][:]  for j < k_b (same for V),
+ * so that the per-step decode reads it as a pool with idx == NULL and
+ * N = k, streaming whole rows with no index lookups.
+ *
+ *   cme_k/v    [B][Hkv][N][Dh]   (kv_dtype)
+ *   idx        [B][idx_stride] int32, values clamped into [0, N-1] on the
+ *              device; NULL copies rows 0..k-1
+ *   k_len      [B] int32 (device): k_b = k_len[b] clamped into [0, k], or
+ *              NULL for all k; rows j >= k_b of out are left untouched
+ *   out_k/v    [B][Hkv][k][Dh]   (kv_dtype)
+ *
+ * Limits: Hkv >= 1, Dh in {64, 128, 256}, idx_stride >= k when idx is given,
+ * k <= N when it is not.  Bit-exact copy.
+ */
+cmc_status cmc_gather_tier1(const void *cme_k, const void *cme_v, cmc_dtype kv_dtype,
+                            const int32_t *idx, const int32_t *k_len, int idx_stride,
+                            int B, int Hkv, int N, int k, int Dh,
+                            void *out_k, void *out_v, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Tier-2 window.                                                           */

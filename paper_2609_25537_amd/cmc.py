@@ -30,7 +30,8 @@ CMC_F32 = 0
 CMC_BF16 = 1
 
 EXPORTED = [
-    "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_window_append",
+    "cmc_select_workspace_bytes", "cmc_select_cmes", "cmc_select_cmes_ragged", "cmc_gather_tier1",
+    "cmc_window_append",
     "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
     "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_denoise_workspace_bytes",
     "cmc_denoise", "cmc_bridge_workspace_bytes", "cmc_memory_bridge", "cmc_status_string", "cmc_last_error",
@@ -76,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_locate_window.argtypes = [P, P, P, I, I, I, P, I, I, I, P, P, P]
         L.cmc_locate_window.restype = I
+        L.cmc_gather_tier1.argtypes = [P, P, I, P, P, I, I, I, I, I, I, P, P, P]
+        L.cmc_gather_tier1.restype = I
         L.cmc_denoise_workspace_bytes.argtypes = [I, I]
         L.cmc_denoise_workspace_bytes.restype = SZ
         L.cmc_denoise.argtypes = [P, I, P, I, I, I, I, ctypes.c_float, I, I, P, P, P, P, P, P, P, SZ, P]
@@ -343,6 +346,33 @@ def cmc_denoise(emb, g: int = 3, tau: float = 0.05, keep_min_every: int = 16, n_
         r["chunk_offset"] = chunk_offset[:, :nch]
         r["n_chunks"] = n_chunks_out
     return r
+
+
+def cmc_gather_tier1(cme_k, cme_v, idx, k: int, k_len=None, out_k=None, out_v=None, stream=None):
+    """Copy the selected rows' K/V into contiguous [B][Hkv][k][Dh] blocks
+    (row j = pool row idx[b][j]; idx [B][idx_stride] int32 or None for rows
+    0..k-1; k_len [B] int32 or None).  Returns (out_k, out_v)."""
+    import torch
+    _need(cme_k.dim() == 4 and cme_k.is_contiguous() and cme_v.is_contiguous() and cme_v.shape == cme_k.shape,
+          "cme_k/v [B][Hkv][N][Dh]")
+    B, Hkv, N, Dh = cme_k.shape
+    stride = 0
+    if idx is not None:
+        _need(idx.dim() == 2 and idx.shape[0] == B and idx.dtype == torch.int32 and idx.is_contiguous(),
+              "idx [B][idx_stride] int32")
+        stride = int(idx.shape[1])
+    if k_len is not None:
+        _need(k_len.shape == (B,) and k_len.dtype == torch.int32 and k_len.is_contiguous(), "k_len [B] int32")
+    if out_k is None:
+        out_k = torch.empty((B, Hkv, k, Dh), dtype=cme_k.dtype, device=cme_k.device)
+    if out_v is None:
+        out_v = torch.empty((B, Hkv, k, Dh), dtype=cme_k.dtype, device=cme_k.device)
+    _need(out_k.shape == (B, Hkv, k, Dh) and out_v.shape == out_k.shape and out_k.dtype == out_v.dtype == cme_k.dtype,
+          "out_k/v [B][Hkv][k][Dh]")
+    rc = lib().cmc_gather_tier1(_ptr(cme_k), _ptr(cme_v), _kv_dtype(cme_k), _ptr(idx), _ptr(k_len), stride, B, Hkv,
+                                N, int(k), Dh, _ptr(out_k), _ptr(out_v), _stream(stream))
+    _check(rc)
+    return out_k, out_v
 
 
 # ---------------------------------------------------------------- window

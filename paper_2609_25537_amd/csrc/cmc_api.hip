@@ -337,6 +337,32 @@ cmc_status cmc_window_append(void *win_k, void *win_v, cmc_dtype kv_dtype, int32
     return ok();
 }
 
+cmc_status cmc_gather_tier1(const void *cme_k, const void *cme_v, cmc_dtype kv_dtype, const int32_t *idx,
+                            const int32_t *k_len, int idx_stride, int B, int Hkv, int N, int k, int Dh,
+                            void *out_k, void *out_v, void *stream) {
+    if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
+        return fail(CMC_ERR_UNSUPPORTED, "gather: unknown kv_dtype %d", (int)kv_dtype);
+    if (B < 0 || Hkv < 1 || N < 0 || k < 0)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "gather: need B, N, k >= 0 and Hkv >= 1");
+    if (!supported_dh(Dh)) return fail(CMC_ERR_UNSUPPORTED, "gather: Dh=%d not in {64,128,256}", Dh);
+    if (idx && idx_stride < k)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "gather: idx_stride=%d is below k=%d", idx_stride, k);
+    if (!idx && k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "gather: k=%d exceeds N=%d with idx == NULL", k, N);
+    if (k > 0 && N < 1) return fail(CMC_ERR_INVALID_ARGUMENT, "gather: k=%d rows from an empty pool", k);
+    if ((long long)B * Hkv * k * Dh > (1LL << 40)) return fail(CMC_ERR_UNSUPPORTED, "gather: too large");
+    if ((long long)B * Hkv * k == 0) return ok();
+    if (!cme_k || !cme_v || !out_k || !out_v) return fail(CMC_ERR_INVALID_ARGUMENT, "gather: null pointer");
+    if (misaligned(cme_k) || misaligned(cme_v) || misaligned(idx) || misaligned(k_len) || misaligned(out_k) ||
+        misaligned(out_v))
+        return fail(CMC_ERR_UNSUPPORTED, "gather: every pointer must be 16-byte aligned");
+    const int elem = kv_dtype == CMC_BF16 ? 2 : 4;
+    cmc::GatherParams p{cme_k, cme_v, idx, k_len, out_k, out_v, B, Hkv, N, k, idx ? idx_stride : k,
+                        Dh * elem / 16};
+    hipError_t e = cmc::launch_gather(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+    return ok();
+}
+
 // ---------------------------------------------------------------- decode
 
 size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W) {

@@ -70,10 +70,11 @@ struct RowPtrs {
     T *rk, *rv;
 };
 
-// Where the rows of sequence b's virtual key list live, for one kv head:
-// rows [0, k) are pool rows idx[row] (clamped into the pool), rows k.. are
-// ring slots row - k, except that the T_new slots written in this call
-// ((count + t) mod W) are read from the new rows.
+// Where the rows of sequence b's key list live, for one kv head (the
+// layout of the MFMA path's phases, below): rows [0, k) are pool rows
+// idx[row] (clamped into the pool), rows [k, k + W) ring slots row - k
+// (masked as in RingRows), rows [k + W, k + W + T_new) the appended rows,
+// written to ring slots (slot0 + t) mod W.
 template <typename T>
 struct RowMap {
     int stride;               // elements per row (Dh)
@@ -81,7 +82,7 @@ struct RowMap {
     T *winK, *winV;           // ring of this (b, kv head)
     const T *newK, *newV;     // appended rows of this (b, kv head)
     const int32_t *idx;       // this sequence's index list, or nullptr
-    int k, W, nmax, slot0, T_new;
+    int k, W, nmax, slot0, T_new, nvalid;
 };
 
 // Row lookup on values already in registers (free functions over scalars:
@@ -100,16 +101,28 @@ __device__ __forceinline__ RowPtrs<T> row_ptrs(int row, int r, const T *poolK, c
     const bool in_pool = row < k;
     r = r < 0 ? 0 : (r > nmax ? nmax : r);
     const int slot = row - k;
-    int t = slot - slot0;
-    t += t < 0 ? W : 0;
-    const bool is_new = !in_pool && t < T_new;
-    const size_t op = (size_t)r * stride, ow = (size_t)slot * stride, on = (size_t)t * stride;
+    const bool is_new = !in_pool && slot >= W;
+    const int t = slot - W;  // appended row, when is_new
+    int ws = slot0 + t;      // its ring slot
+    ws -= ws >= W ? W : 0;
+    const size_t op = (size_t)r * stride, ow = (size_t)slot * stride, on = (size_t)t * stride,
+                 oa = (size_t)ws * stride;
     RowPtrs<T> o;
     o.k = in_pool ? poolK + op : (is_new ? newK + on : winK + ow);
     o.v = in_pool ? poolV + op : (is_new ? newV + on : winV + ow);
-    o.rk = is_new ? winK + ow : nullptr;
-    o.rv = is_new ? winV + ow : nullptr;
+    o.rk = is_new ? winK + oa : nullptr;
+    o.rv = is_new ? winV + oa : nullptr;
     return o;
+}
+
+// Whether key-list row `row` holds a key of this step (only ring slots can
+// be masked).
+__device__ __forceinline__ bool row_valid(int row, int k, int W, int slot0, int T_new, int nvalid) {
+    const int s = row - k;
+    if (s < 0 || s >= W) return true;
+    int d = s - slot0;
+    d += d < 0 ? W : 0;
+    return s < nvalid && d >= T_new;
 }
 
 // Unpacks a RowMap into locals and defines LOCATE(row) over them.
@@ -122,15 +135,16 @@ __device__ __forceinline__ RowPtrs<T> row_ptrs(int row, int r, const T *poolK, c
     const auto newV_ = (rm).newV;                                                        \
     const int32_t *idx_ = (rm).idx;                                                      \
     const int k_ = (rm).k, W_ = (rm).W, nmax_ = (rm).nmax, slot0_ = (rm).slot0,          \
-              tnew_ = (rm).T_new, stride_ = (rm).stride
+              tnew_ = (rm).T_new, stride_ = (rm).stride, nvalid_ = (rm).nvalid
 #define FETCH(row) fetch_row(row, idx_, k_)
 #define PTRS(row, r) \
     row_ptrs(row, r, poolK_, poolV_, winK_, winV_, newK_, newV_, k_, W_, nmax_, slot0_, tnew_, stride_)
 #define LOCATE(row) PTRS(row, FETCH(row))
+#define VALID(row) row_valid(row, k_, W_, slot0_, tnew_, nvalid_)
 
 template <typename T>
 __device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, int kvh, int DH, int kb,
-                                                 int slot0) {
+                                                 int slot0, int nvalid) {
     RowMap<T> m;
     const size_t head = (size_t)b * p.Hkv + kvh;
     m.poolK = static_cast<const T *>(p.cme_k) + head * (size_t)p.N * DH;
@@ -145,6 +159,7 @@ __device__ __forceinline__ RowMap<T> make_rowmap(const DecodeParams &p, int b, i
     m.nmax = p.N > 0 ? p.N - 1 : 0;
     m.slot0 = slot0;
     m.T_new = p.T_new;
+    m.nvalid = nvalid;
     m.stride = DH;
     return m;
 }
@@ -178,38 +193,88 @@ struct WaveState {
     }
 };
 
+// A workgroup's arrival on its sequence's counter (see decode_kernel): the
+// increment depends on the loaded ring count, so issuing it waits for that
+// load.  Wave 0 arrives once, right after its first K/V loads are in flight
+// (or after its loop if it has none), so that wait never delays them.
+struct Arrival {
+    unsigned *ctr;
+    int cnt_raw;
+    bool pending;  // wave-uniform
+    unsigned prev;
+    __device__ __forceinline__ void arrive() {
+        if (pending) {
+            if (threadIdx.x == 0)
+                prev = __hip_atomic_fetch_add(ctr, (unsigned)(cnt_raw != INT_MIN) /* == 1 */, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+            pending = false;
+        }
+    }
+};
+
 // --------------------------------------------------------------- MFMA loop
 //
-// The MFMA path walks the key list in three phases, each a contiguous run of
-// rows addressed from one uniform base with 32-bit offsets:
-//   pool  rows [0, k):           pool row idx[row] (clamped into the pool);
-//   ring  rows [k, k + n_old):   the n_old = min(count, W - T_new) ring slots
-//                                that survive this call's append, starting
-//                                at slot (count - n_old) mod W;
-//   new   rows [k + n_old, L):   the T_new rows appended in this call, read
+// The key list is walked in three phases, each a contiguous run of rows
+// addressed from one uniform base with 32-bit offsets:
+//   pool  rows [0, kb):          pool row idx[row] (clamped into the pool);
+//   ring  rows [kb, kb + W):     ring slot row - kb, masked unless it holds a
+//                                token that survives this call's append
+//                                (slot < min(count, W), not one of the slots
+//                                (count + t) mod W, t < T_new);
+//   new   rows [kb + W, L):      the T_new rows appended in this call, read
 //                                from new_k/new_v and written to ring slots
 //                                (count + t) mod W.
 // That is the same key set as [pool rows] ++ [ring slots after the append];
-// softmax attention does not depend on key order.
+// softmax attention does not depend on key order.  No address and no phase
+// boundary depends on the ring count, so the first K/V loads are issued
+// without waiting for it; the count only enters the masks and the slots the
+// new rows are written to.  (A masked slot that is being overwritten in the
+// same launch may be read before or after the write: its value is unused.)
 
 struct PoolRows {
     const int32_t *idx;  // this sequence's index list, or nullptr
     int nmax;
+    static constexpr bool kMasked = false;
     __device__ __forceinline__ int key(int row) const { return idx ? idx[row] : row; }
     __device__ __forceinline__ int slot(int, int key) const { return key < 0 ? 0 : (key > nmax ? nmax : key); }
+    __device__ __forceinline__ bool valid(int) const { return true; }
+    __device__ __forceinline__ bool all_valid(int, int) const { return true; }
 };
+// The ring in physical slot order: row `first` is slot 0.  Addresses do not
+// depend on the count; a slot holds a key of this step when it is filled
+// (slot < min(count, W)) and not overwritten by this step's append (slots
+// (count + t) mod W, t < T_new) -- a mask applied at compute time.
 struct RingRows {
-    int first, s_old, W;  // row `first` is ring slot s_old
+    int first, nvalid, cnt_mod, T_new, W;
+    static constexpr bool kMasked = true;
     __device__ __forceinline__ int key(int row) const { return row; }
-    __device__ __forceinline__ int slot(int row, int) const {
-        const int sl = s_old + (row - first);
-        return sl >= W ? sl - W : sl;
+    __device__ __forceinline__ int slot(int row, int) const { return row - first; }
+    __device__ __forceinline__ bool valid(int row) const {
+        const int s = row - first;
+        int d = s - cnt_mod;
+        d += d < 0 ? W : 0;
+        return s < nvalid && d >= T_new;
+    }
+    // Whether every row of [r0, r1) is valid (wave-uniform; in steady state
+    // only the T_new slots being overwritten are masked).
+    __device__ __forceinline__ bool all_valid(int r0, int r1) const {
+        const int s0 = r0 - first, s1 = r1 - first;
+        if (s1 > nvalid) return false;
+        for (int t = 0; t < T_new; ++t) {
+            int sl = cnt_mod + t;
+            sl -= sl >= W ? W : 0;
+            if (sl >= s0 && sl < s1) return false;
+        }
+        return true;
     }
 };
 struct NewRows {
     int first, slot0, W;  // row `first` is appended row 0, bound for ring slot slot0
+    static constexpr bool kMasked = false;
     __device__ __forceinline__ int key(int row) const { return row; }
     __device__ __forceinline__ int slot(int row, int) const { return row - first; }
+    __device__ __forceinline__ bool valid(int) const { return true; }
+    __device__ __forceinline__ bool all_valid(int, int) const { return true; }
     __device__ __forceinline__ int ring_slot(int row) const {
         const int sl = slot0 + (row - first);
         return sl >= W ? sl - W : sl;
@@ -252,7 +317,7 @@ template <int NW, int DH, int G, class Rows, bool RING_WRITE>
 __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, const char *kbase, const char *vbase,
                                            char *ringK, char *ringV, const bf16x8 (&qa_hi)[DH / 32],
                                            const bf16x8 (&qa_lo)[DH / 32], float *s_p,
-                                           WaveState<G, DH / 16> &st) {
+                                           WaveState<G, DH / 16> &st, Arrival &arr) {
     constexpr int SL = DH / 32, VD = DH / 16, RB = DH * 2;
     constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
     constexpr int VW = VB >= 16 ? VB / 16 : 1; // 16-byte words (or one 8-byte word)
@@ -297,7 +362,8 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     // scores); P V on the VALU.
 #define CMC_COMPUTE(B0_, KR_, VR_)                                                                     \
     do {                                                                                             \
-        const bool kval = (B0_) + r16 < r1;                                                          \
+        const bool bfull = rows.all_valid((B0_), min((B0_) + 16, r1)); /* uniform */                \
+        const bool kval = (B0_) + r16 < r1 && (bfull || rows.valid((B0_) + r16));                    \
         floatx4 c = {0.f, 0.f, 0.f, 0.f};                                                            \
         _Pragma("unroll") for (int i = 0; i < SL; ++i) {                                             \
             const bf16x8 kbf = __builtin_bit_cast(bf16x8, KR_[i]);                                   \
@@ -314,7 +380,8 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
                 _Pragma("unroll") for (int i = 0; i < VD; ++i) st.acc[g][i] *= alpha;                \
                 st.m[g] = mb;                                                                        \
             }                                                                                        \
-            pk[g] = fast_exp2(sc - st.m[g]);                                                         \
+            /* a masked key weighs 0 (also before any valid key: m is -inf) */                       \
+            pk[g] = kval ? fast_exp2(sc - st.m[g]) : 0.f;                                            \
             st.l[g] += pk[g];                                                                        \
         }                                                                                            \
         if (q4 == 0) {                                                                               \
@@ -322,6 +389,13 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
         }                                                                                            \
         wave_lds_sync();                                                                             \
         _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
+            if constexpr (Rows::kMasked) {                                                           \
+                /* masked ring slots may hold anything: zero their values (p is 0) */                 \
+                const int vrow = (B0_) + 4 * qq + kq;                                                \
+                if (!bfull && !(vrow < r1 && rows.valid(vrow))) {                                    \
+                    _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = make_uint4(0, 0, 0, 0); \
+                }                                                                                    \
+            }                                                                                        \
             float pv[G];                                                                             \
             _Pragma("unroll") for (int g = 0; g < G; ++g) pv[g] = s_p[(4 * qq + kq) * G + g];         \
             _Pragma("unroll") for (int j = 0; j < VW; ++j) {                                         \
@@ -367,6 +441,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 #pragma unroll 1
         for (; blk < r1; blk += BSTRIDE) {
             CMC_LOAD(blk, kc, kvc, kr, vr);
+            arr.arrive();
             CMC_KEYS(blk + BSTRIDE, kc, kvc);
             CMC_COMPUTE(blk, kr, vr);
         }
@@ -375,6 +450,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     uint4 kA[SL], vA[4][VW], kB[SL], vB[4][VW];
     CMC_KEYS(blk, kc, kvc);
     CMC_LOAD(blk, kc, kvc, kA, vA);
+    arr.arrive();  // after this wave's first loads are in flight
     CMC_KEYS(blk + BSTRIDE, kc, kvc);
 #pragma unroll 1
     while (true) {
@@ -406,38 +482,36 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 
 template <int NW, int DH, int G>
 __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int kb, int c0, int c1,
-                                          int cnt0, int slot0, float *s_p, WaveState<G, DH / 16> &st) {
+                                          int cnt0, int slot0, float *s_p, WaveState<G, DH / 16> &st,
+                                          Arrival &arr) {
     bf16x8 qa_hi[DH / 32], qa_lo[DH / 32];
     load_q_operand<DH, G>(p, b, kvh, qa_hi, qa_lo);
     const size_t head = (size_t)b * p.Hkv + kvh;
     const int T_new = p.W > 0 ? p.T_new : 0;
-    const int n_old = p.W > 0 ? min(cnt0, p.W - T_new) : 0;
-    const int pool_end = kb, ring_end = kb + n_old;
+    const int pool_end = kb, ring_end = kb + p.W;
 
     // pool rows
     {
         const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
-        // The list holds all kb pool rows whatever the ring count, so this
-        // phase's loads need not wait for the count.
-        mfma_phase<NW, DH, G, PoolRows, false>(c0, min(c0 + p.chunk, pool_end), rows, kb, vb, nullptr, nullptr,
-                                           qa_hi, qa_lo, s_p, st);
+        mfma_phase<NW, DH, G, PoolRows, false>(c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qa_hi,
+                                               qa_lo, s_p, st, arr);
     }
     if (p.W > 0) {
         char *wk = static_cast<char *>(p.win_k) + head * (size_t)p.W * DH * 2;
         char *wv = static_cast<char *>(p.win_v) + head * (size_t)p.W * DH * 2;
-        // surviving ring slots
-        const int s_old = (int)(((long long)cnt0 - n_old) % p.W);
-        const RingRows rr{pool_end, s_old, p.W};
+        // the W ring slots in physical order, masked by the count
+        const RingRows rr{pool_end, min(cnt0, p.W), slot0, T_new, p.W};
         mfma_phase<NW, DH, G, RingRows, false>(max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr, nullptr,
-                                           qa_hi, qa_lo, s_p, st);
+                                               qa_hi, qa_lo, s_p, st, arr);
         // rows appended in this call
         if (T_new > 0) {
             const NewRows nr{ring_end, slot0, p.W};
             const char *nk = static_cast<const char *>(p.new_k) + head * (size_t)T_new * DH * 2;
             const char *nv = static_cast<const char *>(p.new_v) + head * (size_t)T_new * DH * 2;
-            mfma_phase<NW, DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st);
+            mfma_phase<NW, DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st,
+                                                 arr);
         }
     }
     // Wave totals: l over the 16 keys of one lane row (rows hold copies),
@@ -484,7 +558,7 @@ __device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T>
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int row = r0 + u * STRIDE + grp;
-            ok[u] = row < c1;
+            ok[u] = row < c1 && VALID(row);
             kr[u] = vr[u] = make_uint4(0, 0, 0, 0);
             if (ok[u]) {
                 const RowPtrs<T> rp = LOCATE(row);
@@ -520,13 +594,13 @@ __device__ __forceinline__ void valu_loop(const DecodeParams &p, const RowMap<T>
             for (int u = 1; u < U; ++u) mb = fmaxf(mb, sc[u][g]);
             mb = lane_reduce<OpMax, LPR, kWave>(mb);
             const float mn = fmaxf(st.m[g], mb);
-            const float alpha = exp2f(st.m[g] - mn);
+            const float alpha = mn == -INFINITY ? 1.f : exp2f(st.m[g] - mn);  // nothing valid yet: keep
             st.l[g] *= alpha;
 #pragma unroll
             for (int i = 0; i < VEC; ++i) st.acc[g][i] *= alpha;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const float pu = exp2f(sc[u][g] - mn);
+                const float pu = ok[u] ? exp2f(sc[u][g] - mn) : 0.f;
                 st.l[g] += pu;
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) st.acc[g][i] = fmaf(pu, vf[u][i], st.acc[g][i]);
@@ -590,12 +664,10 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
-    int cnt0 = 0, cnt_raw = 0, valid = 0, slot0 = 0;
+    int cnt0 = 0, cnt_raw = 0, slot0 = 0;
     if (p.W > 0) {
         cnt_raw = p.win_count[b];
         cnt0 = cnt_raw < 0 ? 0 : cnt_raw;
-        const long long cnt1 = (long long)cnt0 + p.T_new;
-        valid = cnt1 < p.W ? (int)cnt1 : p.W;
         slot0 = cnt0 % p.W;
     }
     int kb = p.k;  // pool rows of this sequence
@@ -603,34 +675,35 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
         const int v = p.k_len[b];
         kb = v < 0 ? 0 : (v > p.k ? p.k : v);
     }
-    const int L = kb + valid;
+    // Key list: kb pool rows, the W ring slots, the T_new appended rows (see
+    // the phases above); its length does not depend on the ring count.  The
+    // split plan covers k + W rows; the last split also takes the appended
+    // ones.
+    const int L = kb + (p.W > 0 ? p.W + p.T_new : 0);
     const int c0 = s * p.chunk;
-    const int c1 = min(c0 + p.chunk, L);
-    const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0);
+    const int c1 = s == p.S - 1 ? L : min(c0 + p.chunk, L);
+    const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0, min(cnt0, p.W));
 
-    // Ring count: every workgroup of the sequence arrives on a counter as
-    // soon as it has read the count (the increment depends on the loaded
-    // value, so it is issued only after that load returns); the last of the
-    // Hkv * S arrivals writes the advanced count and re-arms the counter,
-    // after the main loop.  No data is published through the counter, so no
-    // fence is needed.
+    // Ring count: every workgroup of the sequence arrives on a counter after
+    // it has read the count (the increment depends on the loaded value); the
+    // last of the Hkv * S arrivals writes the advanced count and re-arms the
+    // counter, after the main loop.  No data is published through the
+    // counter, so no fence is needed.
     const bool bump = p.T_new > 0 && p.W > 0;
-    unsigned seq_prev = 0;
-    if (bump && threadIdx.x == 0)
-        seq_prev = __hip_atomic_fetch_add(&p.seq_counter[b], (unsigned)(cnt_raw != INT_MIN) /* == 1 */,
-                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    Arrival arr{p.seq_counter + b, cnt_raw, bump && wave == 0, 0u};
 
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
         __shared__ float s_pw[NW][16 * G];
-        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st);
+        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st, arr);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
+    arr.arrive();  // if wave 0 had no K/V loads
 
-    if (bump && threadIdx.x == 0 && seq_prev == (unsigned)(p.Hkv * p.S - 1)) {
+    if (bump && threadIdx.x == 0 && arr.prev == (unsigned)(p.Hkv * p.S - 1)) {
         p.win_count[b] = cnt0 + p.T_new;
         __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

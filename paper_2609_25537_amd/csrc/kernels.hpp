@@ -9,10 +9,10 @@ namespace cmc {
 
 // A decode workgroup has 4 or 8 waves, each streaming its own 16-key blocks;
 // the workgroup combines them in LDS.  8 waves (at most 256 VGPRs each) are
-// built only for heads whose kernels fit that without spilling: Dh <= 128,
-// or Dh = 256 with one query head per kv head.
+// built only for heads whose kernels fit that without spilling: Dh <= 128
+// with G <= 4, or one query head per kv head.
 constexpr bool decode_waves_ok(int waves, int G, int Dh) {
-    return waves == 4 || (waves == 8 && (Dh <= 128 || G == 1));
+    return waves == 4 || (waves == 8 && ((Dh <= 128 && G <= 4) || G == 1));
 }
 
 struct DecodeParams {
@@ -57,6 +57,16 @@ struct AppendParams {
     int row_vecs;             // 16-byte vectors per row (Dh * elem / 16)
 };
 hipError_t launch_window_append(const AppendParams &p, hipStream_t stream);
+
+struct GatherParams {
+    const void *cme_k, *cme_v;  // [B][Hkv][N][Dh]
+    const int32_t *idx;         // [B][idx_stride] or nullptr: rows 0..k-1
+    const int32_t *k_len;       // [B] or nullptr: all k
+    void *out_k, *out_v;        // [B][Hkv][k][Dh]
+    int B, Hkv, N, k, idx_stride;
+    int row_vecs;               // 16-byte vectors per row
+};
+hipError_t launch_gather(const GatherParams &p, hipStream_t stream);
 
 struct SelectParams {
     const float *sel_keys;    // [B][N][D]

@@ -260,3 +260,27 @@ def test_bridge_validation(kw, code):
 def test_bridge_empty_and_workspace():
     assert _bridge(M=0, h=None) == cmc.CMC_OK
     assert cmc.cmc_bridge_workspace_bytes(10, 128) >= 10 * 128 * 2
+
+
+def _gather(**kw):
+    a = dict(ck=FAKE, cv=FAKE, dt=cmc.CMC_BF16, idx=FAKE, kl=None, stride=8, B=2, Hkv=2, N=16, k=8, Dh=128,
+             ok=FAKE, ov=FAKE, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_gather_tier1(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(stride=4), cmc.CMC_ERR_INVALID_ARGUMENT),            # idx_stride < k
+    (dict(idx=None, k=17), cmc.CMC_ERR_INVALID_ARGUMENT),      # k > N without idx
+    (dict(Dh=96), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(dt=9), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(ok=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(kl=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(Hkv=0), cmc.CMC_ERR_INVALID_ARGUMENT),
+])
+def test_gather_validation(kw, code):
+    assert _gather(**kw) == code
+
+
+def test_gather_empty_ok():
+    assert _gather(B=0) == cmc.CMC_OK and _gather(k=0) == cmc.CMC_OK

@@ -1,6 +1,7 @@
 """Parity at the workloads' full sizes, in the launch configuration the
-benchmark times (one cmc_decode_step per step, the library's own split
-plan): selection bit-exact for every sequence, then all decode steps run on
+benchmark times (selection, the selected rows gathered once, one
+cmc_decode_step per step reading them with idx == NULL, the library's own
+split plan): selection bit-exact for every sequence, then all decode steps run on
 the GPU while the oracle advances its own ring every step and recomputes the
 attention at sampled steps -- the first ones, those around the ring wrap,
 and the last."""
@@ -16,7 +17,7 @@ from tests.inputs import accepted_attempts
 pytestmark = pytest.mark.gpu
 
 
-def _run_full(orc, name, sample_extra=()):
+def _run_full(orc, name, sample_extra=(), gathered=True):
     w = wl.get(name)
     say(f"{name}: generating inputs")
     att = accepted_attempts(w, orc)
@@ -31,6 +32,13 @@ def _run_full(orc, name, sample_extra=()):
     pk, pv = wl.pool_kv(w)
     wk, wv, cnt = wl.window_kv(w)
     d_pk, d_pv, d_wk, d_wv, d_wc = map(to_dev, (pk, pv, wk, wv, cnt))
+    if gathered:
+        # The benchmark's configuration: the selected rows gathered once into
+        # contiguous blocks, the decode reading them with idx == NULL.
+        d_pk, d_pv = cmc.cmc_gather_tier1(d_pk, d_pv, idx, w.k)
+        dec_idx = None
+    else:
+        dec_idx = idx
     ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, DEV)
     out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=DEV)
     samples = sorted({0, 1, w.W - 1, w.W, w.W + 1, w.steps - 1, *sample_extra})
@@ -41,7 +49,7 @@ def _run_full(orc, name, sample_extra=()):
         sampled = t in samples
         q = wl.step_q(w, t) if sampled else None
         d_q = to_dev(q) if sampled else to_dev(np.zeros((w.B, w.Hq, w.Dh), np.float32))
-        cmc.cmc_decode_step(d_q, d_pk, d_pv, idx, w.k, d_wk, d_wv, d_wc, to_dev(nk), to_dev(nv), w.scale,
+        cmc.cmc_decode_step(d_q, d_pk, d_pv, dec_idx, w.k, d_wk, d_wv, d_wc, to_dev(nk), to_dev(nv), w.scale,
                             out=out, workspace=ws)
         if sampled:
             say(f"{name}: step {t}")
@@ -59,6 +67,12 @@ def _run_full(orc, name, sample_extra=()):
 @pytest.mark.timeout(300)
 def test_full_llama3_8b_layer(orc):
     _run_full(orc, "llama3_8b_layer", sample_extra=(2, 100, 1500))
+
+
+@pytest.mark.timeout(300)
+def test_full_llama3_8b_layer_index_list(orc):
+    """The same workload decoding straight from the pool through idx."""
+    _run_full(orc, "llama3_8b_layer", gathered=False)
 
 
 @pytest.mark.timeout(600)

@@ -112,6 +112,37 @@ def test_window_append_ring(orc, dtype, Dh, W, T):
     assert (to_host(dc) == cnt).all()
 
 
+# ------------------------------------------------------------------ gather
+
+@pytest.mark.parametrize("dtype,Dh,idx_mode,k_len", [
+    ("bf16", 128, "idx", None), ("f32", 64, "idx", [5, 0, 9]), ("bf16", 256, "none", None),
+    ("bf16", 128, "clamp", [9, 9, 3]),
+])
+def test_gather_tier1(dtype, Dh, idx_mode, k_len):
+    """Bit-exact copy of the selected rows (numpy indexing as the
+    reference); rows past k_b stay untouched; out-of-range entries clamp."""
+    rng = np.random.default_rng(Dh + len(idx_mode))
+    B, Hkv, N, k, stride = 3, 2, 40, 9, 12
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    cv = _bf16 if dtype == "bf16" else (lambda x: x)
+    pk, pv = cv(f(B, Hkv, N, Dh)), cv(f(B, Hkv, N, Dh))
+    idx = rng.integers(0, N, size=(B, stride)).astype(np.int32)
+    if idx_mode == "clamp":
+        idx[:, 0], idx[:, 1] = -7, N + 100
+    say(f"gather {dtype} Dh={Dh} {idx_mode} k_len={k_len}")
+    fill = np.full((B, Hkv, k, Dh), 7, dtype=pk.dtype)
+    ok, ov = to_dev(fill), to_dev(fill)
+    cmc.cmc_gather_tier1(to_dev(pk), to_dev(pv), None if idx_mode == "none" else to_dev(idx), k,
+                         k_len=None if k_len is None else to_dev(np.array(k_len, np.int32)), out_k=ok, out_v=ov)
+    torch.cuda.synchronize()
+    src = np.arange(k)[None].repeat(B, 0) if idx_mode == "none" else np.clip(idx[:, :k], 0, N - 1)
+    kb = [k] * B if k_len is None else [min(max(x, 0), k) for x in k_len]
+    gk, gv = to_host(ok), to_host(ov)
+    for b in range(B):
+        assert (gk[b, :, :kb[b]] == pk[b][:, src[b, :kb[b]]]).all() and (gv[b, :, :kb[b]] == pv[b][:, src[b, :kb[b]]]).all()
+        assert (gk[b, :, kb[b]:] == 7).all() and (gv[b, :, kb[b]:] == 7).all()
+
+
 # ------------------------------------------------------------------ decode
 
 def _logit_bound_tol(q, keys_f64, scale, vmax, Dh):
