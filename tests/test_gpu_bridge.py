@@ -97,9 +97,11 @@ def _params(rng, Hc, F, Hd, gamma_scale=1.0):
 
 @pytest.mark.parametrize("M,Hc,F,Hd", [
     (1, 64, 128, 128), (129, 64, 128, 256), (300, 128, 256, 128), (256, 1280, 512, 384), (77, 192, 128, 1024),
+    (40, 64, 256, 256), (513, 64, 512, 256), (1000, 192, 768, 512),
 ])
 def test_bridge_shapes(orc, M, Hc, F, Hd):
-    """Tile edges: M not a multiple of 128, several N and K tiles."""
+    """Tile edges: M not a multiple of 128 or 256, several N and K tiles,
+    and K of two 32-wide slices (fewer slices than the pipeline's stages)."""
     rng = np.random.default_rng(M + Hc + F + Hd)
     h = wl.f32_to_bf16_bits(rng.standard_normal((M, Hc)).astype(np.float32))
     _run(orc, h, _params(rng, Hc, F, Hd), nu=0.8, what="shapes")
