@@ -71,7 +71,9 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
     constexpr long long kTargetWG = CMC_DECODE_TARGET_WG;
     constexpr long long kGranule = CMC_DECODE_GRANULE;
     constexpr long long kWideMinPairs = CMC_DECODE_WIDE_MIN_PAIRS;
-    constexpr long long kMaxSplits = 128;  // the merge stages S*G*2 floats in the kernel's LDS
+    // The merge stages S*G*2 floats in the kernel's LDS; one split more is
+    // reserved for appended rows.
+    constexpr long long kMaxSplits = 127;
     DecodePlan pl;
     const long long L = (long long)k + W;
     const long long pairs = (long long)B * Hkv;
@@ -91,9 +93,14 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W) {
     const int G = Hq / Hkv;
     pl.S = (int)S;
     pl.chunk = (int)chunk;
+    // A split plan merges partials anyway: the rows appended in a call then
+    // get a split of their own, so no workgroup handles ring rows and
+    // appended rows one after the other.
+    const long long Sa = S > 1 && W > 0 ? S + 1 : S;
+    pl.S_alloc = (int)Sa;
     pl.counter_bytes = align256((size_t)(B + pairs) * sizeof(unsigned));
-    pl.ml_bytes = S > 1 ? align256((size_t)(pairs * S * G * 2) * sizeof(float)) : 0;
-    pl.acc_bytes = S > 1 ? align256((size_t)(pairs * S * G * Dh) * sizeof(float)) : 0;
+    pl.ml_bytes = Sa > 1 ? align256((size_t)(pairs * Sa * G * 2) * sizeof(float)) : 0;
+    pl.acc_bytes = Sa > 1 ? align256((size_t)(pairs * Sa * G * Dh) * sizeof(float)) : 0;
     pl.total = pl.counter_bytes + pl.ml_bytes + pl.acc_bytes;
     return pl;
 }
@@ -434,7 +441,8 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     p.Hkv = Hkv;
     p.N = N;
     p.T_new = T_new;
-    p.S = pl.S;
+    p.new_split = (pl.S > 1 && T_new > 0) ? 1 : 0;
+    p.S = pl.S + p.new_split;
     p.chunk = pl.chunk;
     p.waves = pl.waves;
     p.qscale = cmc::decode_qscale(scale);

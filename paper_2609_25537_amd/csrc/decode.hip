@@ -11,9 +11,9 @@
 // Fused append: with T_new > 0, the rows appended this step go to slots
 // (count + t) mod W.  The workgroup owning such a slot reads the row from
 // new_k/new_v instead of the ring and writes it into the ring; count is
-// advanced by the last workgroup of the sequence to arrive, after every
-// workgroup has read it.  The result equals cmc_window_append followed by
-// the decode.
+// advanced once every (sequence, kv head) pair has been completed, i.e.
+// after every workgroup of the sequence has read it.  The result equals
+// cmc_window_append followed by the decode.
 //
 // Main loop, two variants:
 //   MFMA (bf16 K/V, G <= 4): a wave takes 16 keys per block.  S = Q K^T is one
@@ -29,6 +29,13 @@
 //     products reduced by a DPP butterfly.
 // Both keep an online softmax per wave (running max in log2 units, q
 // pre-scaled by scale*log2 e), then combine the waves through LDS.
+//
+// Latency (one launch of a single layer at batch 1 is a chain of memory round
+// trips, not a stream): the first K/V loads depend only on kernel arguments.
+// The ring count is fetched with a vector load and read where the masks need
+// it, q is loaded and split after the first K/V loads are issued, and when
+// the key list is split anyway the rows appended in this call get a split of
+// their own, so no workgroup runs two dependent phases.
 //
 // Split merge, inside the same launch: with S == 1 the workgroup writes the
 // output directly.  With S > 1 every workgroup publishes (m, l, acc[Dh]) per
@@ -193,16 +200,35 @@ struct WaveState {
     }
 };
 
-// A workgroup's arrival on its sequence's counter (see decode_kernel): the
-// increment depends on the loaded ring count, so issuing it waits for that
-// load.  Wave 0 arrives once, right after its first K/V loads are in flight
-// (or after its loop if it has none), so that wait never delays them.
+// The ring count, fetched by a wave with a vector load issued after its
+// first K/V loads (nothing waits for it before they are in flight) and read
+// where a mask, a ring slot or the arrival needs it.
+struct RingCount {
+    int raw;
+    bool loaded;  // wave-uniform
+    __device__ __forceinline__ void load(const int32_t *win_count, int b) {
+        if (!loaded) {
+            raw = win_count ? __hip_atomic_load(win_count + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+            loaded = true;
+        }
+    }
+    __device__ __forceinline__ int value() const {  // clamped at 0, wave-uniform
+        const int c = __builtin_amdgcn_readfirstlane(raw);
+        return c < 0 ? 0 : c;
+    }
+};
+
+// One (sequence, kv head) pair's arrival on its sequence's counter, by
+// thread 0 of the workgroup that completes the pair (see decode_kernel):
+// the increment depends on the ring count this wave loaded, so it is issued
+// after that load has returned.  Its returned value is read only when the
+// count is advanced, but the compiler waits for it where the branch ends, so
+// callers issue it next to loads they wait for anyway.
 struct Arrival {
     unsigned *ctr;
-    int cnt_raw;
     bool pending;  // wave-uniform
     unsigned prev;
-    __device__ __forceinline__ void arrive() {
+    __device__ __forceinline__ void arrive(int cnt_raw) {
         if (pending) {
             if (threadIdx.x == 0)
                 prev = __hip_atomic_fetch_add(ctr, (unsigned)(cnt_raw != INT_MIN) /* == 1 */, __ATOMIC_RELAXED,
@@ -239,14 +265,21 @@ struct PoolRows {
     __device__ __forceinline__ int slot(int, int key) const { return key < 0 ? 0 : (key > nmax ? nmax : key); }
     __device__ __forceinline__ bool valid(int) const { return true; }
     __device__ __forceinline__ bool all_valid(int, int) const { return true; }
+    __device__ __forceinline__ void resolve(const RingCount &) {}
 };
 // The ring in physical slot order: row `first` is slot 0.  Addresses do not
 // depend on the count; a slot holds a key of this step when it is filled
 // (slot < min(count, W)) and not overwritten by this step's append (slots
 // (count + t) mod W, t < T_new) -- a mask applied at compute time.
 struct RingRows {
-    int first, nvalid, cnt_mod, T_new, W;
+    int first, T_new, W;
+    int nvalid = 0, cnt_mod = 0;  // set by resolve(), before the first mask
     static constexpr bool kMasked = true;
+    __device__ __forceinline__ void resolve(const RingCount &cnt) {
+        const int c = cnt.value();
+        nvalid = min(c, W);
+        cnt_mod = c % W;
+    }
     __device__ __forceinline__ int key(int row) const { return row; }
     __device__ __forceinline__ int slot(int row, int) const { return row - first; }
     __device__ __forceinline__ bool valid(int row) const {
@@ -269,8 +302,10 @@ struct RingRows {
     }
 };
 struct NewRows {
-    int first, slot0, W;  // row `first` is appended row 0, bound for ring slot slot0
+    int first, W;  // row `first` is appended row 0, bound for ring slot count mod W
+    int slot0 = 0;  // set by resolve()
     static constexpr bool kMasked = false;
+    __device__ __forceinline__ void resolve(const RingCount &cnt) { slot0 = cnt.value() % W; }
     __device__ __forceinline__ int key(int row) const { return row; }
     __device__ __forceinline__ int slot(int row, int) const { return row - first; }
     __device__ __forceinline__ bool valid(int) const { return true; }
@@ -304,6 +339,14 @@ __device__ __forceinline__ void load_q_operand(const DecodeParams &p, int b, int
     }
 }
 
+// q's A operand, filled by the first phase that has a block for the wave,
+// after that block's K/V loads are issued (both round trips overlap).
+template <int DH>
+struct QOperand {
+    bf16x8 hi[DH / 32], lo[DH / 32];
+    bool ready;
+};
+
 // One phase: rows [r0, r1) from bases kbase/vbase (bytes).  A wave takes 16
 // rows per block.  K: the lane's row blk + (lane % 16) in the MFMA B layout
 // (dims 32i + 8*(lane/16) .. +7).  V: four quarters of 4 rows; in quarter qq
@@ -314,9 +357,9 @@ __device__ __forceinline__ void load_q_operand(const DecodeParams &p, int b, int
 // (index-list entries) are fetched one block ahead of the K/V rows, and the
 // K/V rows one block ahead of their use.
 template <int NW, int DH, int G, class Rows, bool RING_WRITE>
-__device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, const char *kbase, const char *vbase,
-                                           char *ringK, char *ringV, const bf16x8 (&qa_hi)[DH / 32],
-                                           const bf16x8 (&qa_lo)[DH / 32], float *s_p,
+__device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh, int r0, int r1, Rows rows,
+                                           const char *kbase, const char *vbase, char *ringK, char *ringV,
+                                           QOperand<DH> &qo, RingCount &cnt, float *s_p,
                                            WaveState<G, DH / 16> &st, Arrival &arr) {
     constexpr int SL = DH / 32, VD = DH / 16, RB = DH * 2;
     constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
@@ -367,8 +410,8 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
         floatx4 c = {0.f, 0.f, 0.f, 0.f};                                                            \
         _Pragma("unroll") for (int i = 0; i < SL; ++i) {                                             \
             const bf16x8 kbf = __builtin_bit_cast(bf16x8, KR_[i]);                                   \
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_hi[i], kbf, c, 0, 0, 0);                 \
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa_lo[i], kbf, c, 0, 0, 0);                 \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo.hi[i], kbf, c, 0, 0, 0);                 \
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo.lo[i], kbf, c, 0, 0, 0);                 \
         }                                                                                            \
         float pk[G];                                                                                 \
         _Pragma("unroll") for (int g = 0; g < G; ++g) {                                              \
@@ -426,12 +469,28 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
         }                                                                                            \
     } while (0)
 
+    // Once the wave's first K/V loads are in flight: fetch the ring count
+    // and q, split q (both round trips overlap the K/V loads'), arrive (an
+    // unsplit launch's workgroup completes its pair), then read the count
+    // into the masks.
+#define CMC_AFTER_FIRST_LOAD()                    \
+    do {                                          \
+        if (!qo.ready) {                          \
+            cnt.load(p.win_count, b);             \
+            load_q_operand<DH, G>(p, b, kvh, qo.hi, qo.lo); \
+            qo.ready = true;                      \
+        }                                         \
+        arr.arrive(cnt.raw);                      \
+        rows.resolve(cnt);                        \
+    } while (0)
+
     // Two register sets used in turn: the next block's K/V loads are in
     // flight while this block computes (the loop is unrolled by two so no
     // registers are copied).  Index-list entries are fetched two blocks
     // ahead and issued before the next block's K/V loads: loads retire in
     // issue order, so waiting for the entries then never waits for the
-    // prefetched K/V rows.
+    // prefetched K/V rows.  The wave's last block prefetches nothing (loads
+    // past the end would be drained by the barrier after the loop).
     int kc, kvc[4], kn, kvn[4];
     if constexpr (!kDoubleBuffer) {
         // Wide heads: one register set (two would cost an extra wave per SIMD
@@ -441,7 +500,7 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
 #pragma unroll 1
         for (; blk < r1; blk += BSTRIDE) {
             CMC_LOAD(blk, kc, kvc, kr, vr);
-            arr.arrive();
+            CMC_AFTER_FIRST_LOAD();
             CMC_KEYS(blk + BSTRIDE, kc, kvc);
             CMC_COMPUTE(blk, kr, vr);
         }
@@ -450,11 +509,15 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
     uint4 kA[SL], vA[4][VW], kB[SL], vB[4][VW];
     CMC_KEYS(blk, kc, kvc);
     CMC_LOAD(blk, kc, kvc, kA, vA);
-    arr.arrive();  // after this wave's first loads are in flight
+    CMC_AFTER_FIRST_LOAD();
     CMC_KEYS(blk + BSTRIDE, kc, kvc);
 #pragma unroll 1
     while (true) {
         int nb = blk + BSTRIDE;
+        if (nb >= r1) {  // wave-uniform
+            CMC_COMPUTE(blk, kA, vA);
+            break;
+        }
         CMC_KEYS(nb + BSTRIDE, kn, kvn);
         CMC_LOAD(nb, kc, kvc, kB, vB);
         kc = kn;
@@ -463,8 +526,11 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
         __builtin_amdgcn_sched_barrier(0);  // keep the prefetch above this block's compute
         CMC_COMPUTE(blk, kA, vA);
         blk = nb;
-        if (blk >= r1) break;
         nb = blk + BSTRIDE;
+        if (nb >= r1) {
+            CMC_COMPUTE(blk, kB, vB);
+            break;
+        }
         CMC_KEYS(nb + BSTRIDE, kn, kvn);
         CMC_LOAD(nb, kc, kvc, kA, vA);
         kc = kn;
@@ -473,19 +539,18 @@ __device__ __forceinline__ void mfma_phase(int r0, int r1, const Rows rows, cons
         __builtin_amdgcn_sched_barrier(0);
         CMC_COMPUTE(blk, kB, vB);
         blk = nb;
-        if (blk >= r1) break;
     }
 #undef CMC_KEYS
 #undef CMC_LOAD
 #undef CMC_COMPUTE
+#undef CMC_AFTER_FIRST_LOAD
 }
 
 template <int NW, int DH, int G>
 __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int kb, int c0, int c1,
-                                          int cnt0, int slot0, float *s_p, WaveState<G, DH / 16> &st,
-                                          Arrival &arr) {
-    bf16x8 qa_hi[DH / 32], qa_lo[DH / 32];
-    load_q_operand<DH, G>(p, b, kvh, qa_hi, qa_lo);
+                                          RingCount &cnt, float *s_p, WaveState<G, DH / 16> &st, Arrival &arr) {
+    QOperand<DH> qo;
+    qo.ready = false;
     const size_t head = (size_t)b * p.Hkv + kvh;
     const int T_new = p.W > 0 ? p.T_new : 0;
     const int pool_end = kb, ring_end = kb + p.W;
@@ -495,23 +560,23 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
-        mfma_phase<NW, DH, G, PoolRows, false>(c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qa_hi,
-                                               qa_lo, s_p, st, arr);
+        mfma_phase<NW, DH, G, PoolRows, false>(p, b, kvh, c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qo,
+                                               cnt, s_p, st, arr);
     }
     if (p.W > 0) {
         char *wk = static_cast<char *>(p.win_k) + head * (size_t)p.W * DH * 2;
         char *wv = static_cast<char *>(p.win_v) + head * (size_t)p.W * DH * 2;
         // the W ring slots in physical order, masked by the count
-        const RingRows rr{pool_end, min(cnt0, p.W), slot0, T_new, p.W};
-        mfma_phase<NW, DH, G, RingRows, false>(max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr, nullptr,
-                                               qa_hi, qa_lo, s_p, st, arr);
+        const RingRows rr{pool_end, T_new, p.W};
+        mfma_phase<NW, DH, G, RingRows, false>(p, b, kvh, max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr,
+                                               nullptr, qo, cnt, s_p, st, arr);
         // rows appended in this call
         if (T_new > 0) {
-            const NewRows nr{ring_end, slot0, p.W};
+            const NewRows nr{ring_end, p.W};
             const char *nk = static_cast<const char *>(p.new_k) + head * (size_t)T_new * DH * 2;
             const char *nv = static_cast<const char *>(p.new_v) + head * (size_t)T_new * DH * 2;
-            mfma_phase<NW, DH, G, NewRows, true>(max(c0, ring_end), c1, nr, nk, nv, wk, wv, qa_hi, qa_lo, s_p, st,
-                                                 arr);
+            mfma_phase<NW, DH, G, NewRows, true>(p, b, kvh, max(c0, ring_end), c1, nr, nk, nv, wk, wv, qo, cnt, s_p,
+                                                 st, arr);
         }
     }
     // Wave totals: l over the 16 keys of one lane row (rows hold copies),
@@ -664,11 +729,18 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
-    int cnt0 = 0, cnt_raw = 0, slot0 = 0;
+    // Ring count.  MFMA path: fetched by each wave after its first K/V loads
+    // (RingCount), so they never wait for it.  VALU path: read up front (its
+    // row map resolves ring slots before the loads).
+    RingCount cnt{0, false};
+    int cnt0 = 0, slot0 = 0;
     if (p.W > 0) {
-        cnt_raw = p.win_count[b];
-        cnt0 = cnt_raw < 0 ? 0 : cnt_raw;
-        slot0 = cnt0 % p.W;
+        if constexpr (!MF) {
+            cnt.raw = p.win_count[b];
+            cnt.loaded = true;
+            cnt0 = cnt.raw < 0 ? 0 : cnt.raw;
+            slot0 = cnt0 % p.W;
+        }
     }
     int kb = p.k;  // pool rows of this sequence
     if (p.k_len) {
@@ -677,36 +749,50 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
     }
     // Key list: kb pool rows, the W ring slots, the T_new appended rows (see
     // the phases above); its length does not depend on the ring count.  The
-    // split plan covers k + W rows; the last split also takes the appended
-    // ones.
+    // split plan covers k + W rows in chunks; the appended rows go to the last
+    // split, or to a split of their own (the last) when p.new_split is set.
+    const int Lkw = kb + p.W;
     const int L = kb + (p.W > 0 ? p.W + p.T_new : 0);
-    const int c0 = s * p.chunk;
-    const int c1 = s == p.S - 1 ? L : min(c0 + p.chunk, L);
+    int c0, c1;
+    if (p.new_split) {
+        const bool own = s == p.S - 1;
+        c0 = own ? Lkw : s * p.chunk;
+        c1 = own ? L : (s == p.S - 2 ? Lkw : min(c0 + p.chunk, Lkw));
+    } else {
+        c0 = s * p.chunk;
+        c1 = s == p.S - 1 ? L : min(c0 + p.chunk, L);
+    }
     const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0, min(cnt0, p.W));
 
-    // Ring count: every workgroup of the sequence arrives on a counter after
-    // it has read the count (the increment depends on the loaded value); the
-    // last of the Hkv * S arrivals writes the advanced count and re-arms the
-    // counter, after the main loop.  No data is published through the
-    // counter, so no fence is needed.
+    // Ring count: the workgroup that completes a (sequence, kv head) pair
+    // arrives on the sequence's counter -- with S == 1 every workgroup, in
+    // its first block; with S > 1 the one that merges the pair, after every
+    // split of the pair has arrived on the pair counter (each after reading
+    // the count).  The last of the Hkv arrivals writes the advanced count and
+    // re-arms the counter.  No data is published through the counter, so no
+    // fence is needed.
     const bool bump = p.T_new > 0 && p.W > 0;
-    Arrival arr{p.seq_counter + b, cnt_raw, bump && wave == 0, 0u};
+    Arrival arr{p.seq_counter + b, bump && wave == 0 && p.S == 1, 0u};
 
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
         __shared__ float s_pw[NW][16 * G];
-        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt0, slot0, s_pw[threadIdx.x >> 6], st, arr);
+        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt, s_pw[threadIdx.x >> 6], st, arr);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
-    arr.arrive();  // if wave 0 had no K/V loads
-
-    if (bump && threadIdx.x == 0 && arr.prev == (unsigned)(p.Hkv * p.S - 1)) {
-        p.win_count[b] = cnt0 + p.T_new;
-        __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (p.W > 0) cnt.load(p.win_count, b);  // a wave without K/V rows
+    arr.arrive(cnt.raw);                     // S == 1 and no K/V rows (or the VALU path)
+    const int cnt_now = MF ? cnt.value() : cnt0;
+#define CMC_BUMP()                                                                         \
+    do {                                                                                 \
+        if (bump && threadIdx.x == 0 && arr.prev == (unsigned)(p.Hkv - 1)) {             \
+            p.win_count[b] = cnt_now + p.T_new;                                          \
+            __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
+        }                                                                                \
+    } while (0)
 
     // Lanes holding each dim group after the wave reduction.
     constexpr int LPR = MF ? 4 : DH / Vec16<T>::N;         // lanes per dim group stride
@@ -740,6 +826,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
             combine_waves<NW, G, DH>(s_m, s_l, s_acc, g, d, num, den);
             outp[t] = den > 0.f ? num / den : 0.f;
         }
+        CMC_BUMP();
     } else {
         // Publish this split's partial with agent-coherent 64-bit stores (two
         // dims per thread), wait for them to complete, then arrive on the
@@ -786,6 +873,8 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
             s_ml[2 * t] = v.x;
             s_ml[2 * t + 1] = v.y;
         }
+        arr.pending = bump && wave == 0;
+        arr.arrive(cnt.raw);  // this workgroup completes the pair; overlaps the merge loads
         __syncthreads();
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
@@ -828,7 +917,9 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
         }
         if (threadIdx.x == 0)
             __hip_atomic_store(&p.pair_counter[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        CMC_BUMP();
     }
+#undef CMC_BUMP
 
 }
 

@@ -32,7 +32,8 @@ struct DecodeParams {
     unsigned *pair_counter;   // [B][Hkv] split arrivals, zero between calls
     unsigned *seq_counter;    // [B] kv-head arrivals, zero between calls
     int k, W, B, Hq, Hkv, N, T_new;
-    int S, chunk;             // key-axis splits and keys per split
+    int S, chunk;             // key-axis splits (launched) and keys per split
+    int new_split;            // 1: the last split takes only the T_new appended rows
     int waves;                // waves per workgroup: 4 or 8
     float qscale;             // scale * log2(e)
 };
@@ -41,7 +42,8 @@ struct DecodeParams {
 // launch agree.  Workspace layout: [sequence counters | pair counters]
 // (zero between calls), then the per-split partials.
 struct DecodePlan {
-    int S = 0, chunk = 0, waves = 4;
+    int S = 0, chunk = 0, waves = 4;  // S splits over the k + W rows
+    int S_alloc = 0;                  // partials reserved: S, plus one for appended rows when S > 1 and W > 0
     size_t counter_bytes = 0, ml_bytes = 0, acc_bytes = 0, total = 0;
 };
 DecodePlan plan_decode(int B, int Hq, int Hkv, int Dh, int k, int W);
