@@ -50,6 +50,31 @@ __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Build-time tuning knob: tile rows per group of the tile order below.
+#ifndef CMC_BRIDGE_GROUP_M
+#define CMC_BRIDGE_GROUP_M 4
+#endif
+
+// Tile order.  Physical workgroup b runs on XCD b % 8, and each XCD takes a
+// contiguous run of logical tiles; the run is walked in groups of
+// CMC_BRIDGE_GROUP_M tile rows, M fastest inside a group, so the tiles an
+// XCD holds at once form a near-square block that shares few A and B
+// strips in its L2 (a row-major walk would stream every B strip once per
+// tile row).
+__device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int &tn) {
+    const int tiles = gridDim.x, bid = blockIdx.x;
+    const int per_xcd = (tiles + 7) / 8;
+    int t = (bid % 8) * per_xcd + bid / 8;
+    if ((tiles % 8) != 0) t = bid;  // uneven split: plain order
+    constexpr int GM = CMC_BRIDGE_GROUP_M;
+    const int group = t / (GM * tiles_n);
+    const int first = group * GM;
+    const int gm = min(GM, tiles_m - first);
+    const int local = t - group * GM * tiles_n;
+    tm = first + local % gm;
+    tn = local / gm;
+}
+
 // WT x WT per wave (4 x 4 or 8 x 8 MFMA tiles of 16 x 16), BK of K per LDS
 // slice; the workgroup tile is 2 WT x 2 WT.
 template <int EPI, int WT, int BK>
@@ -63,15 +88,8 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // Tile order: physical workgroup b runs on XCD b % 8; give each XCD a
-    // contiguous run of logical tiles (N fastest).
-    const int tiles_n = p.N / BN;
-    const int tiles = gridDim.x;
-    const int per_xcd = (tiles + 7) / 8;
-    const int bid = blockIdx.x;
-    int t = (bid % 8) * per_xcd + bid / 8;
-    if ((tiles % 8) != 0) t = bid;  // uneven split: plain order
-    const int tm = t / tiles_n, tn = t % tiles_n;
+    int tm, tn;
+    gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
     // Global -> register -> LDS staging: chunk c = tid + 256 i is row
@@ -166,7 +184,11 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
 // fragment read of it use the same lane mapping and the read is one
 // contiguous, bank-conflict-free ds_read_b128.  Waves 0-1 load the 16 A
 // blocks of a slice, waves 2-3 the 16 B blocks.
-constexpr int kDeepStages = 4;
+#ifndef CMC_BRIDGE_DEEP_STAGES
+#define CMC_BRIDGE_DEEP_STAGES 4
+#endif
+constexpr int kDeepStages = CMC_BRIDGE_DEEP_STAGES;
+static_assert(kDeepStages >= 3 && kDeepStages <= 5, "4 - 5 stages of 32 KB fit the 160 KB of LDS");
 
 template <int EPI>
 __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
@@ -177,13 +199,8 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    const int tiles_n = p.N / BN;
-    const int tiles = gridDim.x;
-    const int per_xcd = (tiles + 7) / 8;
-    const int bid = blockIdx.x;
-    int t = (bid % 8) * per_xcd + bid / 8;
-    if ((tiles % 8) != 0) t = bid;
-    const int tm = t / tiles_n, tn = t % tiles_n;
+    int tm, tn;
+    gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
     // This lane's source rows for the 8 blocks its wave loads per slice.
@@ -222,8 +239,10 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
         // Wait for this wave's loads of slice j (the NS - 2 later slices may
         // stay in flight: 8 loads each), then for every wave's.  A bare
         // s_barrier: the fences of __syncthreads would drain every load.
-        static_assert(NS == 4, "the wait count below assumes 4 stages");
-        __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt <= 16, expcnt and lgkmcnt not waited
+        // s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
+        // at their maxima (not waited).
+        constexpr int kVm = 8 * (NS - 2);
+        __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (15 << 8));
         __builtin_amdgcn_s_barrier();
         // Stage (j - 1) % NS was read by every wave before the barrier: refill it.
         issue(min(j + NS - 1, KT - 1));
