@@ -6,13 +6,15 @@
 // chunks of t tokens; the position of each chunk's first token in C is the
 // offset CME-guided localization needs.
 //
-// denoise_score_kernel: one wave per 16 consecutive tokens.  Lanes split
-// the hidden dimension (16-byte loads); the wave streams the 16 + g rows it
-// needs once, keeping the last g rows in registers, and accumulates the 16
-// + g squared norms and the 16 x g neighbour dot products per lane, then
-// reduces them across the wave.  The halo of g rows is the next wave's
-// first rows, so it is mostly served by L2.  Output: the fp32 statistic
-// max_cos (-inf where a token has no neighbour) and the Eq. 3 bit.
+// denoise_score_kernel: one wave per TT consecutive tokens.  Lanes split
+// the hidden dimension (16-byte loads, 64 x 16 bytes per pass over a row);
+// the wave loads the TT + g rows it needs for P passes at once (one round
+// trip covers a 1280-wide bf16 row), keeps the last g rows of a pass in
+// registers, and accumulates the TT + g squared norms and the TT x g
+// neighbour dot products per lane, then reduces them across the wave.  The
+// halo of g rows is the next wave's first rows, so it is mostly served by
+// L2.  Output: the fp32 statistic max_cos (-inf where a token has no
+// neighbour) and the Eq. 3 bit.
 //
 // denoise_select_kernel: one 1024-thread workgroup per sequence scans the
 // Eq. 3 bits.  With a(i) the last passing position before i (-1 if none),
@@ -29,9 +31,24 @@ namespace cmc {
 
 namespace {
 
-constexpr int kTokensPerWave = 16;
+// Build-time tuning knobs: tokens per wave, row passes loaded at once.
+#ifndef CMC_DENOISE_TOKENS
+#define CMC_DENOISE_TOKENS 8
+#endif
+#ifndef CMC_DENOISE_PASSES
+#define CMC_DENOISE_PASSES 3
+#endif
+constexpr int kTokensPerWave = CMC_DENOISE_TOKENS;
+constexpr int kPasses = CMC_DENOISE_PASSES;
 
 __device__ __forceinline__ int clamp_tokens(int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// c + a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs (v_dot2_f32_bf16).
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
 
 template <typename T>
 struct Lane16;  // one 16-byte lane load widened to fp32
@@ -60,15 +77,26 @@ struct Lane16<uint16_t> {
 
 template <typename T, int G>
 __global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
-    constexpr int TT = kTokensPerWave, R = TT + G, VEC = Lane16<T>::N;
+    constexpr int TT = kTokensPerWave, R = TT + G, VEC = Lane16<T>::N, P = kPasses, SPAN = kWave * VEC;
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int i0 = (blockIdx.x * 4 + wave) * TT;
-    if (i0 >= p.n) return;  // wave-uniform; no barriers below
     const int nb = p.n_tokens ? clamp_tokens(p.n_tokens[b], p.n) : p.n;
     const char *base = static_cast<const char *>(p.emb) + (size_t)b * p.n * p.H * sizeof(T);
     const size_t row_bytes = (size_t)p.H * sizeof(T);
+    __shared__ float s_nn[4][R], s_dd[4][TT][G];
 
+    // Each wave walks groups of TT tokens with the grid's stride (no
+    // barriers below: the LDS staging is private to the wave).
+    for (int i0 = (blockIdx.x * 4 + wave) * TT; i0 < p.n; i0 += gridDim.x * 4 * TT) {
+    if (i0 >= nb) {  // wave-uniform: positions past the sequence have no statistic
+        const int i = i0 + lane;
+        if (lane < TT && i < p.n) {
+            const size_t o = (size_t)b * p.n + i;
+            if (p.max_cos) p.max_cos[o] = -INFINITY;
+            p.pass[o] = 0;
+        }
+        continue;
+    }
     float nn[R], dd[TT][G];
 #pragma unroll
     for (int r = 0; r < R; ++r) nn[r] = 0.f;
@@ -77,55 +105,91 @@ __global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
 #pragma unroll
         for (int d = 0; d < G; ++d) dd[t][d] = 0.f;
 
-    if (i0 < nb) {
-        for (int e0 = lane * VEC; e0 < p.H; e0 += kWave * VEC) {
-            // All R rows of this slice are loaded up front: rows past the
-            // sequence are clamped to its last row (in bounds) and zeroed
-            // after the load, so no load sits behind a branch.
-            uint4 raw[R];
+    {
+        for (int eb = 0; eb < p.H; eb += P * SPAN) {
+            // All R rows of P passes are loaded up front: rows past the
+            // sequence are clamped to its last row and columns past H to the
+            // row's last 16 bytes (in bounds), and zeroed after the load, so
+            // no load sits behind a branch.
+            uint4 raw[P][R];
 #pragma unroll
-            for (int r = 0; r < R; ++r)
-                raw[r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
-                                                          (size_t)e0 * sizeof(T));
-            float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
+            for (int pp = 0; pp < P; ++pp) {
+                const int ec = min(eb + pp * SPAN + lane * VEC, p.H - VEC);
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                float x[VEC];
-                Lane16<T>::widen(raw[r], x);
-                if (i0 + r >= nb) {
+                for (int r = 0; r < R; ++r)
+                    raw[pp][r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
+                                                                  (size_t)ec * sizeof(T));
+            }
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v) x[v] = 0.f;
-                }
+            for (int pp = 0; pp < P; ++pp) {
+                const bool col_on = eb + pp * SPAN + lane * VEC < p.H;
+                if constexpr (sizeof(T) == 2) {
+                    // bf16: v_dot2 on packed pairs (two products per op, fp32
+                    // accumulation, no widening).
+                    uint32_t win[G + 1][4];  // rows r-G .. r (ring by unrolled index)
 #pragma unroll
-                for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
+                    for (int r = 0; r < R; ++r) {
+                        const bool on = col_on && i0 + r < nb;
+                        const uint32_t w[4] = {on ? raw[pp][r].x : 0u, on ? raw[pp][r].y : 0u,
+                                               on ? raw[pp][r].z : 0u, on ? raw[pp][r].w : 0u};
 #pragma unroll
-                for (int d = 1; d <= G; ++d) {
-                    if (r - d >= 0 && r - d < TT) {
-                        const float(&y)[VEC] = win[(r - d) % (G + 1)];
+                        for (int k = 0; k < 4; ++k) nn[r] = dot2_bf16(w[k], w[k], nn[r]);
 #pragma unroll
-                        for (int v = 0; v < VEC; ++v) dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                        for (int d = 1; d <= G; ++d) {
+                            if (r - d >= 0 && r - d < TT) {
+#pragma unroll
+                                for (int k = 0; k < 4; ++k)
+                                    dd[r - d][d - 1] = dot2_bf16(win[(r - d) % (G + 1)][k], w[k], dd[r - d][d - 1]);
+                            }
+                        }
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) win[r % (G + 1)][k] = w[k];
+                    }
+                } else {
+                    float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        float x[VEC];
+                        Lane16<T>::widen(raw[pp][r], x);
+                        if (!col_on || i0 + r >= nb) {
+#pragma unroll
+                            for (int v = 0; v < VEC; ++v) x[v] = 0.f;
+                        }
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
+#pragma unroll
+                        for (int d = 1; d <= G; ++d) {
+                            if (r - d >= 0 && r - d < TT) {
+                                const float(&y)[VEC] = win[(r - d) % (G + 1)];
+#pragma unroll
+                                for (int v = 0; v < VEC; ++v)
+                                    dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                            }
+                        }
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
                     }
                 }
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
             }
         }
     }
-    // Wave sums, staged in LDS private to the wave so that lane t < 16 can
-    // finish token i0 + t from its own registers.
-    __shared__ float s_nn[4][R], s_dd[4][TT][G];
+    // Wave sums (all reductions first, so their exchange steps interleave),
+    // staged in LDS private to the wave so that lane t < TT can finish token
+    // i0 + t from its own registers.
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const float v = lane_reduce<OpSum, 1, kWave>(nn[r]);
-        if (lane == 0) s_nn[wave][r] = v;
-    }
+    for (int r = 0; r < R; ++r) nn[r] = lane_reduce<OpSum, 1, kWave>(nn[r]);
 #pragma unroll
     for (int t = 0; t < TT; ++t)
 #pragma unroll
-        for (int d = 0; d < G; ++d) {
-            const float v = lane_reduce<OpSum, 1, kWave>(dd[t][d]);
-            if (lane == 0) s_dd[wave][t][d] = v;
-        }
+        for (int d = 0; d < G; ++d) dd[t][d] = lane_reduce<OpSum, 1, kWave>(dd[t][d]);
+    if (lane == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) s_nn[wave][r] = nn[r];
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+            for (int d = 0; d < G; ++d) s_dd[wave][t][d] = dd[t][d];
+    }
     asm volatile("" ::: "memory");  // one wave's LDS accesses execute in order
     const int i = i0 + lane;
     float best = -INFINITY;
@@ -141,6 +205,8 @@ __global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
         const size_t o = (size_t)b * p.n + i;
         if (p.max_cos) p.max_cos[o] = best;
         p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
+    }
+    asm volatile("" ::: "memory");  // this group's LDS reads before the next group's writes
     }
 }
 
@@ -263,9 +329,18 @@ __global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoisePara
     if (tid == 0) p.kept_count[b] = count;
 }
 
+// Build-time tuning knob: workgroups per sequence (0: one per 4 TT tokens;
+// otherwise at most this many, each walking its groups with the grid's
+// stride).
+#ifndef CMC_DENOISE_WG_PER_SEQ
+#define CMC_DENOISE_WG_PER_SEQ 0
+#endif
+
 template <typename T>
 hipError_t launch_scores(const DenoiseParams &p, hipStream_t stream) {
-    dim3 grid((p.n + 4 * kTokensPerWave - 1) / (4 * kTokensPerWave), p.B);
+    int gx = (p.n + 4 * kTokensPerWave - 1) / (4 * kTokensPerWave);
+    if (CMC_DENOISE_WG_PER_SEQ > 0 && gx > CMC_DENOISE_WG_PER_SEQ) gx = CMC_DENOISE_WG_PER_SEQ;
+    dim3 grid(gx, p.B);
     switch (p.g) {
         case 1: denoise_score_kernel<T, 1><<<grid, 256, 0, stream>>>(p); break;
         case 2: denoise_score_kernel<T, 2><<<grid, 256, 0, stream>>>(p); break;

@@ -42,10 +42,12 @@ template <> struct Vec16<uint16_t> {
 //
 // Exchanging v with lane (lane ^ M): masks 1 and 2 are DPP
 // quad permutes, 7 and 15 the DPP half-row / row mirrors, 8 a row rotate by
-// 8; 16 and 32 go through ds_swizzle / ds_bpermute (__shfl_xor).  A
-// butterfly over masks {1, 2, 7, 15, 16, 32} (linearly independent bit
-// patterns) reduces a group of 2^n lanes with every lane ending on the
-// bitwise same value, because each step combines symmetric pairs.
+// 8; 16 and 32 are the gfx950 row swaps v_permlane16_swap /
+// v_permlane32_swap (VALU, no LDS round trip, so independent reductions
+// interleave).  A butterfly over masks {1, 2, 7, 15, 16, 32} (linearly
+// independent bit patterns) reduces a group of 2^n lanes with every lane
+// ending on the bitwise same value, because each step combines symmetric
+// pairs.
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {
@@ -59,6 +61,22 @@ struct OpSum {
 struct OpMax {
     __device__ __forceinline__ static float f(float a, float b) { return fmaxf(a, b); }
 };
+
+// f(v, v of lane ^ 16) and f(v, v of lane ^ 32).  Each swap returns the pair
+// {v, partner's v} in a lane-dependent order; the combine ops are
+// commutative, so the result is the same bits in either order.
+template <typename Op>
+__device__ __forceinline__ float combine_xor16(float v) {
+    const unsigned u = __float_as_uint(v);
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+template <typename Op>
+__device__ __forceinline__ float combine_xor32(float v) {
+    const unsigned u = __float_as_uint(v);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 // Combine v over the lane-index bits selected by [LO, HI) (powers of two):
 // lane_reduce<Op, 1, 16> reduces within aligned 16-lane groups,
@@ -75,8 +93,8 @@ __device__ __forceinline__ float lane_reduce(float v) {
         if constexpr (LO <= 1) v = Op::f(v, dpp_mov<0x140>(v));                // ^15 (after ^1,^2,^7)
         else v = Op::f(v, dpp_mov<0x128>(v));                                  // ^8 (row rotate 8)
     }
-    if constexpr (LO <= 16 && HI > 16) v = Op::f(v, __shfl_xor(v, 16));
-    if constexpr (LO <= 32 && HI > 32) v = Op::f(v, __shfl_xor(v, 32));
+    if constexpr (LO <= 16 && HI > 16) v = combine_xor16<Op>(v);
+    if constexpr (LO <= 32 && HI > 32) v = combine_xor32<Op>(v);
     return v;
 }
 
