@@ -6,7 +6,8 @@
 // chunks of t tokens; the position of each chunk's first token in C is the
 // offset CME-guided localization needs.
 //
-// denoise_score_kernel: one wave per TT consecutive tokens.  Lanes split
+// denoise_score_kernel (fp32 embeddings; bf16 too when the Gram kernel below
+// is switched off): one wave per TT consecutive tokens.  Lanes split
 // the hidden dimension (16-byte loads, 64 x 16 bytes per pass over a row);
 // the wave loads the TT + g rows it needs for P passes at once (one round
 // trip covers a 1280-wide bf16 row), keeps the last g rows of a pass in
@@ -15,6 +16,13 @@
 // halo of g rows is the next wave's first rows, so it is mostly served by
 // L2.  Output: the fp32 statistic max_cos (-inf where a token has no
 // neighbour) and the Eq. 3 bit.
+//
+// denoise_gram_kernel (bf16): the same statistic from the Gram matrix of 16
+// consecutive rows -- 16 - g tokens and their g-row halo -- accumulated by
+// v_mfma_f32_16x16x32_bf16 with one fragment as both operands (lane l holds
+// 8 elements of row l % 16, so A = X and B = X^T).  The norms are its
+// diagonal, the neighbour dots its first g super-diagonals; no cross-lane
+// reductions and almost no VALU work, which bounds the VALU variant above.
 //
 // denoise_select_kernel: one 1024-thread workgroup per sequence scans the
 // Eq. 3 bits.  With a(i) the last passing position before i (-1 if none),
@@ -44,6 +52,8 @@ constexpr int kPasses = CMC_DENOISE_PASSES;
 __device__ __forceinline__ int clamp_tokens(int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // c + a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs (v_dot2_f32_bf16).
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
@@ -88,125 +98,212 @@ __global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
     // Each wave walks groups of TT tokens with the grid's stride (no
     // barriers below: the LDS staging is private to the wave).
     for (int i0 = (blockIdx.x * 4 + wave) * TT; i0 < p.n; i0 += gridDim.x * 4 * TT) {
-    if (i0 >= nb) {  // wave-uniform: positions past the sequence have no statistic
-        const int i = i0 + lane;
-        if (lane < TT && i < p.n) {
-            const size_t o = (size_t)b * p.n + i;
-            if (p.max_cos) p.max_cos[o] = -INFINITY;
-            p.pass[o] = 0;
-        }
-        continue;
-    }
-    float nn[R], dd[TT][G];
-#pragma unroll
-    for (int r = 0; r < R; ++r) nn[r] = 0.f;
-#pragma unroll
-    for (int t = 0; t < TT; ++t)
-#pragma unroll
-        for (int d = 0; d < G; ++d) dd[t][d] = 0.f;
-
-    {
-        for (int eb = 0; eb < p.H; eb += P * SPAN) {
-            // All R rows of P passes are loaded up front: rows past the
-            // sequence are clamped to its last row and columns past H to the
-            // row's last 16 bytes (in bounds), and zeroed after the load, so
-            // no load sits behind a branch.
-            uint4 raw[P][R];
-#pragma unroll
-            for (int pp = 0; pp < P; ++pp) {
-                const int ec = min(eb + pp * SPAN + lane * VEC, p.H - VEC);
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-                    raw[pp][r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
-                                                                  (size_t)ec * sizeof(T));
+        if (i0 >= nb) {  // wave-uniform: positions past the sequence have no statistic
+            const int i = i0 + lane;
+            if (lane < TT && i < p.n) {
+                const size_t o = (size_t)b * p.n + i;
+                if (p.max_cos) p.max_cos[o] = -INFINITY;
+                p.pass[o] = 0;
             }
+            continue;
+        }
+        float nn[R], dd[TT][G];
 #pragma unroll
-            for (int pp = 0; pp < P; ++pp) {
-                const bool col_on = eb + pp * SPAN + lane * VEC < p.H;
-                if constexpr (sizeof(T) == 2) {
-                    // bf16: v_dot2 on packed pairs (two products per op, fp32
-                    // accumulation, no widening).
-                    uint32_t win[G + 1][4];  // rows r-G .. r (ring by unrolled index)
+        for (int r = 0; r < R; ++r) nn[r] = 0.f;
 #pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        const bool on = col_on && i0 + r < nb;
-                        const uint32_t w[4] = {on ? raw[pp][r].x : 0u, on ? raw[pp][r].y : 0u,
-                                               on ? raw[pp][r].z : 0u, on ? raw[pp][r].w : 0u};
+        for (int t = 0; t < TT; ++t)
 #pragma unroll
-                        for (int k = 0; k < 4; ++k) nn[r] = dot2_bf16(w[k], w[k], nn[r]);
+            for (int d = 0; d < G; ++d) dd[t][d] = 0.f;
+
+        {
+            for (int eb = 0; eb < p.H; eb += P * SPAN) {
+                // All R rows of P passes are loaded up front: rows past the
+                // sequence are clamped to its last row and columns past H to the
+                // row's last 16 bytes (in bounds), and zeroed after the load, so
+                // no load sits behind a branch.
+                uint4 raw[P][R];
 #pragma unroll
-                        for (int d = 1; d <= G; ++d) {
-                            if (r - d >= 0 && r - d < TT) {
+                for (int pp = 0; pp < P; ++pp) {
+                    const int ec = min(eb + pp * SPAN + lane * VEC, p.H - VEC);
 #pragma unroll
-                                for (int k = 0; k < 4; ++k)
-                                    dd[r - d][d - 1] = dot2_bf16(win[(r - d) % (G + 1)][k], w[k], dd[r - d][d - 1]);
+                    for (int r = 0; r < R; ++r)
+                        raw[pp][r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
+                                                                      (size_t)ec * sizeof(T));
+                }
+#pragma unroll
+                for (int pp = 0; pp < P; ++pp) {
+                    const bool col_on = eb + pp * SPAN + lane * VEC < p.H;
+                    if constexpr (sizeof(T) == 2) {
+                        // bf16: v_dot2 on packed pairs (two products per op, fp32
+                        // accumulation, no widening).
+                        uint32_t win[G + 1][4];  // rows r-G .. r (ring by unrolled index)
+#pragma unroll
+                        for (int r = 0; r < R; ++r) {
+                            const bool on = col_on && i0 + r < nb;
+                            const uint32_t w[4] = {on ? raw[pp][r].x : 0u, on ? raw[pp][r].y : 0u,
+                                                   on ? raw[pp][r].z : 0u, on ? raw[pp][r].w : 0u};
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) nn[r] = dot2_bf16(w[k], w[k], nn[r]);
+#pragma unroll
+                            for (int d = 1; d <= G; ++d) {
+                                if (r - d >= 0 && r - d < TT) {
+#pragma unroll
+                                    for (int k = 0; k < 4; ++k)
+                                        dd[r - d][d - 1] = dot2_bf16(win[(r - d) % (G + 1)][k], w[k], dd[r - d][d - 1]);
+                                }
                             }
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) win[r % (G + 1)][k] = w[k];
                         }
+                    } else {
+                        float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
 #pragma unroll
-                        for (int k = 0; k < 4; ++k) win[r % (G + 1)][k] = w[k];
-                    }
-                } else {
-                    float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
+                        for (int r = 0; r < R; ++r) {
+                            float x[VEC];
+                            Lane16<T>::widen(raw[pp][r], x);
+                            if (!col_on || i0 + r >= nb) {
 #pragma unroll
-                    for (int r = 0; r < R; ++r) {
-                        float x[VEC];
-                        Lane16<T>::widen(raw[pp][r], x);
-                        if (!col_on || i0 + r >= nb) {
-#pragma unroll
-                            for (int v = 0; v < VEC; ++v) x[v] = 0.f;
-                        }
-#pragma unroll
-                        for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
-#pragma unroll
-                        for (int d = 1; d <= G; ++d) {
-                            if (r - d >= 0 && r - d < TT) {
-                                const float(&y)[VEC] = win[(r - d) % (G + 1)];
-#pragma unroll
-                                for (int v = 0; v < VEC; ++v)
-                                    dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                                for (int v = 0; v < VEC; ++v) x[v] = 0.f;
                             }
-                        }
 #pragma unroll
-                        for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
+                            for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
+#pragma unroll
+                            for (int d = 1; d <= G; ++d) {
+                                if (r - d >= 0 && r - d < TT) {
+                                    const float(&y)[VEC] = win[(r - d) % (G + 1)];
+#pragma unroll
+                                    for (int v = 0; v < VEC; ++v)
+                                        dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                                }
+                            }
+#pragma unroll
+                            for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
+                        }
                     }
                 }
             }
         }
-    }
-    // Wave sums (all reductions first, so their exchange steps interleave),
-    // staged in LDS private to the wave so that lane t < TT can finish token
-    // i0 + t from its own registers.
+        // Wave sums (all reductions first, so their exchange steps interleave),
+        // staged in LDS private to the wave so that lane t < TT can finish token
+        // i0 + t from its own registers.
 #pragma unroll
-    for (int r = 0; r < R; ++r) nn[r] = lane_reduce<OpSum, 1, kWave>(nn[r]);
-#pragma unroll
-    for (int t = 0; t < TT; ++t)
-#pragma unroll
-        for (int d = 0; d < G; ++d) dd[t][d] = lane_reduce<OpSum, 1, kWave>(dd[t][d]);
-    if (lane == 0) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) s_nn[wave][r] = nn[r];
+        for (int r = 0; r < R; ++r) nn[r] = lane_reduce<OpSum, 1, kWave>(nn[r]);
 #pragma unroll
         for (int t = 0; t < TT; ++t)
 #pragma unroll
-            for (int d = 0; d < G; ++d) s_dd[wave][t][d] = dd[t][d];
-    }
-    asm volatile("" ::: "memory");  // one wave's LDS accesses execute in order
-    const int i = i0 + lane;
-    float best = -INFINITY;
-    if (lane < TT && i < nb) {
-        const float ni = fmaxf(sqrtf(s_nn[wave][lane]), 1e-8f);
+            for (int d = 0; d < G; ++d) dd[t][d] = lane_reduce<OpSum, 1, kWave>(dd[t][d]);
+        if (lane == 0) {
 #pragma unroll
-        for (int d = 1; d <= G; ++d) {
-            if (i + d < nb)
-                best = fmaxf(best, s_dd[wave][lane][d - 1] / (ni * fmaxf(sqrtf(s_nn[wave][lane + d]), 1e-8f)));
+            for (int r = 0; r < R; ++r) s_nn[wave][r] = nn[r];
+#pragma unroll
+            for (int t = 0; t < TT; ++t)
+#pragma unroll
+                for (int d = 0; d < G; ++d) s_dd[wave][t][d] = dd[t][d];
+        }
+        asm volatile("" ::: "memory");  // one wave's LDS accesses execute in order
+        const int i = i0 + lane;
+        float best = -INFINITY;
+        if (lane < TT && i < nb) {
+            const float ni = fmaxf(sqrtf(s_nn[wave][lane]), 1e-8f);
+#pragma unroll
+            for (int d = 1; d <= G; ++d) {
+                if (i + d < nb)
+                    best = fmaxf(best, s_dd[wave][lane][d - 1] / (ni * fmaxf(sqrtf(s_nn[wave][lane + d]), 1e-8f)));
+            }
+        }
+        if (lane < TT && i < p.n) {
+            const size_t o = (size_t)b * p.n + i;
+            if (p.max_cos) p.max_cos[o] = best;
+            p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
+        }
+        asm volatile("" ::: "memory");  // this group's LDS reads before the next group's writes
+    }
+}
+
+// Build-time tuning knob: 32-column k-steps whose loads are issued together.
+#ifndef CMC_DENOISE_GRAM_BATCH
+#define CMC_DENOISE_GRAM_BATCH 8
+#endif
+
+// Gram matrix of the 16 rows a wave owns: every k-step's loads are clamped
+// in bounds (row to the sequence's last row, column to the row's last 16
+// bytes); with MASK, lanes whose row or column is past the end contribute
+// zeros.  k-steps past the row's end in the last batch are skipped
+// (uniform branch around the MFMA only).
+template <bool MASK>
+__device__ __forceinline__ floatx4 gram_tile(const char *row_base, bool row_on, int q4, int H) {
+    constexpr int KB = CMC_DENOISE_GRAM_BATCH;
+    const int KS = (H + 31) / 32;
+    floatx4 c = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < KS; k0 += KB) {
+        uint4 v[KB];
+#pragma unroll
+        for (int j = 0; j < KB; ++j) {
+            const int col = min((k0 + j) * 32 + 8 * q4, H - 8);
+            v[j] = *reinterpret_cast<const uint4 *>(row_base + (size_t)col * 2);
+        }
+#pragma unroll
+        for (int j = 0; j < KB; ++j) {
+            if (k0 + j < KS) {
+                uint4 x = v[j];
+                if constexpr (MASK) {
+                    if (!row_on || (k0 + j) * 32 + 8 * q4 >= H) x = make_uint4(0, 0, 0, 0);
+                }
+                const bf16x8 f = __builtin_bit_cast(bf16x8, x);
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, f, c, 0, 0, 0);
+            }
         }
     }
-    if (lane < TT && i < p.n) {
-        const size_t o = (size_t)b * p.n + i;
-        if (p.max_cos) p.max_cos[o] = best;
-        p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
-    }
-    asm volatile("" ::: "memory");  // this group's LDS reads before the next group's writes
+    return c;
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void denoise_gram_kernel(DenoiseParams p) {
+    constexpr int TT = 16 - G;  // tokens per wave; rows i0 .. i0 + 15
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, q4 = lane >> 4;
+    const int nb = p.n_tokens ? clamp_tokens(p.n_tokens[b], p.n) : p.n;
+    const char *base = static_cast<const char *>(p.emb) + (size_t)b * p.n * p.H * 2;
+    const size_t row_bytes = (size_t)p.H * 2;
+    __shared__ float s_c[4][16][17];
+
+    for (int i0 = (blockIdx.x * 4 + wave) * TT; i0 < p.n; i0 += gridDim.x * 4 * TT) {
+        if (i0 >= nb) {  // wave-uniform: positions past the sequence have no statistic
+            const int i = i0 + lane;
+            if (lane < TT && i < p.n) {
+                const size_t o = (size_t)b * p.n + i;
+                if (p.max_cos) p.max_cos[o] = -INFINITY;
+                p.pass[o] = 0;
+            }
+            continue;
+        }
+        const bool row_on = i0 + r16 < nb;
+        const char *row_base = base + (size_t)min(i0 + r16, nb - 1) * row_bytes;
+        // Unmasked fast path when all 16 rows exist and the row is whole k-steps.
+        const floatx4 c = (i0 + 16 <= nb && p.H % 32 == 0) ? gram_tile<false>(row_base, row_on, q4, p.H)
+                                                            : gram_tile<true>(row_base, row_on, q4, p.H);
+        // C fragment: lane l, element r -> row 4 (l / 16) + r, column l % 16.
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s_c[wave][4 * q4 + r][r16] = c[r];
+        asm volatile("" ::: "memory");  // one wave's LDS accesses execute in order
+        const int i = i0 + lane;
+        float best = -INFINITY;
+        if (lane < TT && i < nb) {
+            const float ni = fmaxf(sqrtf(s_c[wave][lane][lane]), 1e-8f);
+#pragma unroll
+            for (int d = 1; d <= G; ++d) {
+                if (i + d < nb)
+                    best = fmaxf(best, s_c[wave][lane][lane + d] /
+                                           (ni * fmaxf(sqrtf(s_c[wave][lane + d][lane + d]), 1e-8f)));
+            }
+        }
+        if (lane < TT && i < p.n) {
+            const size_t o = (size_t)b * p.n + i;
+            if (p.max_cos) p.max_cos[o] = best;
+            p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
+        }
+        asm volatile("" ::: "memory");  // this group's LDS reads before the next group's writes
     }
 }
 
@@ -336,8 +433,31 @@ __global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoisePara
 #define CMC_DENOISE_WG_PER_SEQ 0
 #endif
 
+// Build-time tuning knob: 1 scores bf16 embeddings with denoise_gram_kernel.
+#ifndef CMC_DENOISE_MFMA
+#define CMC_DENOISE_MFMA 1
+#endif
+
+template <int G>
+hipError_t launch_gram(const DenoiseParams &p, hipStream_t stream) {
+    constexpr int per_wg = 4 * (16 - G);
+    int gx = (p.n + per_wg - 1) / per_wg;
+    if (CMC_DENOISE_WG_PER_SEQ > 0 && gx > CMC_DENOISE_WG_PER_SEQ) gx = CMC_DENOISE_WG_PER_SEQ;
+    denoise_gram_kernel<G><<<dim3(gx, p.B), 256, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_scores(const DenoiseParams &p, hipStream_t stream) {
+    if (sizeof(T) == 2 && CMC_DENOISE_MFMA) {
+        switch (p.g) {
+            case 1: return launch_gram<1>(p, stream);
+            case 2: return launch_gram<2>(p, stream);
+            case 3: return launch_gram<3>(p, stream);
+            case 4: return launch_gram<4>(p, stream);
+            default: return hipErrorInvalidValue;
+        }
+    }
     int gx = (p.n + 4 * kTokensPerWave - 1) / (4 * kTokensPerWave);
     if (CMC_DENOISE_WG_PER_SEQ > 0 && gx > CMC_DENOISE_WG_PER_SEQ) gx = CMC_DENOISE_WG_PER_SEQ;
     dim3 grid(gx, p.B);

@@ -66,26 +66,31 @@ def test_denoise_neighbourhoods(orc, dtype, g):
     _check_denoise(orc, emb, g, 0.05, 16, [300, 151, 17], chunk_tokens=7, what="neighbourhoods")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("n,H,n_tokens", [
     (1, 8, None), (15, 8, [15, 0]), (16, 16, [16, 1]), (17, 128, [17, 2]), (65, 40, [65, 64]),
-    (1000, 1280, [1000, 999]), (9000, 16, [9000, 8193]),
+    (1000, 1280, [1000, 999]), (9000, 16, [9000, 8193]), (200, 1288, [200, 53]),
 ])
-def test_denoise_sizes(orc, n, H, n_tokens):
-    """Tile edges (16 tokens per wave, 64 per workgroup), the last token,
-    empty and one-token sequences, and sequences longer than one round of
-    the selection scan (8192 positions)."""
+def test_denoise_sizes(orc, dtype, n, H, n_tokens):
+    """Tile edges (8 tokens per wave for fp32; 16 - g rows per wave for
+    bf16), row widths that are not whole 32-column steps (8, 40, 1288), the
+    last token, empty and one-token sequences, and sequences longer than one
+    round of the selection scan (8192 positions)."""
     rng = np.random.default_rng(n + H)
     e = rng.standard_normal((2, n, H)).astype(np.float32)
     e[:, 1:] += 0.2 * e[:, :-1]
-    _check_denoise(orc, e, 3, 0.05, 16, n_tokens, chunk_tokens=256, what="sizes")
+    emb = wl.f32_to_bf16_bits(e) if dtype == "bf16" else e
+    _check_denoise(orc, emb, 3, 0.05, 16, n_tokens, chunk_tokens=256, what="sizes")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("tau,m", [(-2.0, 0), (2.0, 16), (2.0, 1), (0.3, 3), (0.05, 0)])
-def test_denoise_threshold_and_floor(orc, tau, m):
+def test_denoise_threshold_and_floor(orc, dtype, tau, m):
     rng = np.random.default_rng(7)
     e = rng.standard_normal((4, 500, 32)).astype(np.float32)
     e[:, 1:] += 0.4 * e[:, :-1]
-    _check_denoise(orc, e, 3, tau, m, [500, 499, 250, 3], chunk_tokens=32, what="tau/floor")
+    emb = wl.f32_to_bf16_bits(e) if dtype == "bf16" else e
+    _check_denoise(orc, emb, 3, tau, m, [500, 499, 250, 3], chunk_tokens=32, what="tau/floor")
 
 
 def test_denoise_onehot_exact(orc):
@@ -100,11 +105,13 @@ def test_denoise_onehot_exact(orc):
     assert (to_host(r["chunk_offset"]) == ref["chunk_offset"]).all()
 
 
-def test_denoise_zero_rows(orc):
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_denoise_zero_rows(orc, dtype):
     """Zero embeddings: the 1e-8 norm clamp gives cosine 0, never NaN."""
     e = np.random.default_rng(9).standard_normal((1, 50, 16)).astype(np.float32)
     e[0, 10:14] = 0.0
-    _check_denoise(orc, e, 3, 0.0, 0, what="zeros")
+    emb = wl.f32_to_bf16_bits(e) if dtype == "bf16" else e
+    _check_denoise(orc, emb, 3, 0.0, 0, what="zeros")
 
 
 @pytest.mark.timeout(600)
