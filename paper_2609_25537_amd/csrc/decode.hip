@@ -266,6 +266,7 @@ struct PoolRows {
     __device__ __forceinline__ bool valid(int) const { return true; }
     __device__ __forceinline__ bool all_valid(int, int) const { return true; }
     __device__ __forceinline__ void resolve(const RingCount &) {}
+    __device__ __forceinline__ int limit(int r1) const { return r1; }
 };
 // The ring in physical slot order: row `first` is slot 0.  Addresses do not
 // depend on the count; a slot holds a key of this step when it is filled
@@ -280,6 +281,9 @@ struct RingRows {
         nvalid = min(c, W);
         cnt_mod = c % W;
     }
+    // Slots past the filled ones hold no key: once the count is known the
+    // phase ends there (a ring that has not wrapped yet is not read whole).
+    __device__ __forceinline__ int limit(int r1) const { return min(r1, first + nvalid); }
     __device__ __forceinline__ int key(int row) const { return row; }
     __device__ __forceinline__ int slot(int row, int) const { return row - first; }
     __device__ __forceinline__ bool valid(int row) const {
@@ -306,6 +310,7 @@ struct NewRows {
     int slot0 = 0;  // set by resolve()
     static constexpr bool kMasked = false;
     __device__ __forceinline__ void resolve(const RingCount &cnt) { slot0 = cnt.value() % W; }
+    __device__ __forceinline__ int limit(int r1) const { return r1; }
     __device__ __forceinline__ int key(int row) const { return row; }
     __device__ __forceinline__ int slot(int row, int) const { return row - first; }
     __device__ __forceinline__ bool valid(int) const { return true; }
@@ -472,7 +477,7 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
     // Once the wave's first K/V loads are in flight: fetch the ring count
     // and q, split q (both round trips overlap the K/V loads'), arrive (an
     // unsplit launch's workgroup completes its pair), then read the count
-    // into the masks.
+    // into the masks and end the phase at the last filled ring slot.
 #define CMC_AFTER_FIRST_LOAD()                    \
     do {                                          \
         if (!qo.ready) {                          \
@@ -482,6 +487,7 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
         }                                         \
         arr.arrive(cnt.raw);                      \
         rows.resolve(cnt);                        \
+        r1 = rows.limit(r1);                      \
     } while (0)
 
     // Two register sets used in turn: the next block's K/V loads are in
