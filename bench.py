@@ -79,6 +79,9 @@ def parse():
                          "--workload, and a --copy-probe run) into the per-launch HBM traffic record in "
                          "profiles/decode_traffic.json; runs on the CPU")
     ap.add_argument("--copy-probe-mib", type=int, default=1024, help="size the copy probe ran with")
+    ap.add_argument("--vendor-gemm-probe", action="store_true",
+                    help="with a MemoryBridge workload: time torch's bf16 addmm (the vendor BLAS) on the "
+                         "projection's two GEMM shapes instead of the library, for comparison")
     ap.add_argument("--launch-reps", type=int, default=500,
                     help="back-to-back decode launches timed for the roofline figure")
     ap.add_argument("--baseline-steps", type=int, default=4,
@@ -490,6 +493,8 @@ def main():
     if args.workload in wl.DENOISE_WORKLOADS:
         return main_denoise(args, wl.DENOISE_WORKLOADS[args.workload], dev)
     if args.workload in wl.BRIDGE_WORKLOADS:
+        if args.vendor_gemm_probe:
+            return vendor_gemm_probe(wl.BRIDGE_WORKLOADS[args.workload], dev)
         return main_bridge(args, wl.BRIDGE_WORKLOADS[args.workload], dev)
     w = wl.get(args.workload)
     if w.layers != 1:
@@ -684,6 +689,33 @@ def bridge_cpu_baseline(w, budget_s: float):
             break
     return {"value": done / t, "unit": "CME rows/s", "cores": orc.num_threads(), "kind": "oracle",
             "sample": f"{done} of {w.M} rows ({t:.2f} s)"}
+
+
+def vendor_gemm_probe(w, dev, reps: int = 20):
+    """Reference point, not the product path: torch's bf16 addmm (bias added,
+    no activation) on the MemoryBridge's two GEMM shapes, random operands,
+    timed with HIP events over `reps` back-to-back calls."""
+    import torch
+    lines = []
+    for (K, N) in [(w.Hc, w.F), (w.F, w.Hd)]:
+        a = torch.randn(w.M, K, device=dev, dtype=torch.bfloat16)
+        bt = torch.randn(N, K, device=dev, dtype=torch.bfloat16)
+        bias = torch.randn(N, device=dev, dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.addmm(bias, a, bt.t())
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.addmm(bias, a, bt.t())
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        lines.append({"vendor_gemm": "torch.addmm bf16", "M": w.M, "K": K, "N": N, "ms": round(ms, 4),
+                      "tflops": round(2.0 * w.M * K * N / (ms * 1e-3) / 1e12, 1)})
+        del a, bt, bias
+    for ln in lines:
+        print(json.dumps(ln), flush=True)
 
 
 def main_bridge(args, w, dev):
