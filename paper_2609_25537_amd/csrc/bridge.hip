@@ -182,19 +182,26 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
 // row l % 16, k 8 (l / 16) .. +7, exactly the A/B operand of
 // v_mfma_f32_16x16x32_bf16 -- so the global load of a block and the
 // fragment read of it use the same lane mapping and the read is one
-// contiguous, bank-conflict-free ds_read_b128.  Waves 0-1 load the 16 A
-// blocks of a slice, waves 2-3 the 16 B blocks.
+// contiguous, bank-conflict-free ds_read_b128.  Waves 0-1 load the A
+// blocks of a slice, waves 2-3 the B blocks (WT / 16 blocks per wave).
+// WT x WT per wave, 2 WT x 2 WT per workgroup: WT = 128 holds 256
+// accumulators per lane (one wave per SIMD), WT = 64 keeps two workgroups
+// per CU.
 #ifndef CMC_BRIDGE_DEEP_STAGES
 #define CMC_BRIDGE_DEEP_STAGES 4
 #endif
+#ifndef CMC_BRIDGE_DEEP_WT
+#define CMC_BRIDGE_DEEP_WT 128
+#endif
 constexpr int kDeepStages = CMC_BRIDGE_DEEP_STAGES;
-static_assert(kDeepStages >= 3 && kDeepStages <= 5, "4 - 5 stages of 32 KB fit the 160 KB of LDS");
 
-template <int EPI>
+template <int EPI, int WT>
 __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
-    constexpr int WT = 128, BM = 256, BN = 256, BK = 32, T = WT / 16, NS = kDeepStages;
-    constexpr int kBlk = 1024;                       // bytes per 16 x 32 block
-    constexpr int kStage = (BM / 16 + BN / 16) * kBlk;  // 32 KB
+    constexpr int BM = 2 * WT, BN = 2 * WT, BK = 32, T = WT / 16, NS = kDeepStages;
+    constexpr int kBlk = 1024;                          // bytes per 16 x 32 block
+    constexpr int kStage = (BM / 16 + BN / 16) * kBlk;  // WT / 4 KB
+    constexpr int LPW = T;                              // blocks (loads) per wave per slice
+    static_assert(NS >= 3 && NS * kStage <= 160 * 1024, "the stages must fit the 160 KB of LDS");
     __shared__ __attribute__((aligned(1024))) char smem[NS * kStage];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -203,22 +210,22 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
     gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // This lane's source rows for the 8 blocks its wave loads per slice.
+    // This lane's source rows for the LPW blocks its wave loads per slice.
     const bool loads_a = wave < 2;
-    const int blk0 = (wave & 1) * 8;                 // first block (of 16) of this wave's matrix
+    const int blk0 = (wave & 1) * LPW;               // first block (of 2 LPW) of this wave's matrix
     const int fr = lane & 15, fk = 8 * (lane >> 4);
-    const uint16_t *src[8];
+    const uint16_t *src[LPW];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < LPW; ++i) {
         const int r = (blk0 + i) * 16 + fr;
         src[i] = loads_a ? p.A + (size_t)min(m0 + r, p.M - 1) * p.K + fk : p.B + (size_t)(n0 + r) * p.K + fk;
     }
-    const int ldsw = (loads_a ? 0 : (BM / 16) * kBlk) + blk0 * kBlk;  // this wave's 8 blocks, in a stage
+    const int ldsw = (loads_a ? 0 : (BM / 16) * kBlk) + blk0 * kBlk;  // this wave's blocks, in a stage
     auto issue = [&](int slice) {
         const int st = slice % NS;
         char *dst = smem + st * kStage + ldsw;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < LPW; ++i)
             __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)slice * BK),
                                              (__attribute__((address_space(3))) void *)(dst + i * kBlk), 16, 0, 0);
     };
@@ -231,17 +238,18 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
 
     const int KT = p.K / BK;
     // Prologue: slices 0 .. NS-2 in flight.  Past the end the last slice is
-    // loaded again (identical bytes into its own stage), which keeps eight
+    // loaded again (identical bytes into its own stage), which keeps LPW
     // loads per wave per iteration so that the counted wait below stays exact.
 #pragma unroll
     for (int sl = 0; sl < NS - 1; ++sl) issue(min(sl, KT - 1));
     for (int j = 0; j < KT; ++j) {
         // Wait for this wave's loads of slice j (the NS - 2 later slices may
-        // stay in flight: 8 loads each), then for every wave's.  A bare
+        // stay in flight: LPW loads each), then for every wave's.  A bare
         // s_barrier: the fences of __syncthreads would drain every load.
         // s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
         // at their maxima (not waited).
-        constexpr int kVm = 8 * (NS - 2);
+        constexpr int kVm = LPW * (NS - 2);
+        static_assert(kVm < 64, "vmcnt field is 6 bits");
         __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (15 << 8));
         __builtin_amdgcn_s_barrier();
         // Stage (j - 1) % NS was read by every wave before the barrier: refill it.
@@ -427,22 +435,25 @@ hipError_t launch_gemm_t(int epi, const GemmParams &g, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// Build-time tuning knob: 1 runs the deep-pipelined 256 x 256 kernel for the
-// shapes it takes (N % 256 == 0, K % 32 == 0).  On the 49152 x 1280 -> 4096
-// -> 4096 projection it measured 4.11 ms per call against 3.96 ms for the
-// register-staged kernels, so those are the default.
+// Build-time tuning knob: 1 runs the deep-pipelined direct-to-LDS kernel for
+// the shapes it takes (N % (2 CMC_BRIDGE_DEEP_WT) == 0, K % 32 == 0).  On the
+// 49152 x 1280 -> 4096 -> 4096 projection it measured 4.05 ms per call with
+// 256 x 256 tiles and 4 stages (4.02 with 5), 4.35 - 4.66 ms with 128 x 128
+// tiles and 3 - 5 stages, against 3.66 ms for the register-staged kernels,
+// so those are the default.
 #ifndef CMC_BRIDGE_DEEP
 #define CMC_BRIDGE_DEEP 0
 #endif
 
 hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
-    if (CMC_BRIDGE_DEEP && g.N % 256 == 0 && g.K % 32 == 0) {
-        const long long tiles = (long long)((g.M + 255) / 256) * (g.N / 256);
+    constexpr int DB = 2 * CMC_BRIDGE_DEEP_WT;
+    if (CMC_BRIDGE_DEEP && g.N % DB == 0 && g.K % 32 == 0) {
+        const long long tiles = (long long)((g.M + DB - 1) / DB) * (g.N / DB);
         if (tiles == 0) return hipSuccess;
         if (epi == 0)
-            gemm_deep_kernel<0><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+            gemm_deep_kernel<0, CMC_BRIDGE_DEEP_WT><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
         else
-            gemm_deep_kernel<1><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+            gemm_deep_kernel<1, CMC_BRIDGE_DEEP_WT><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
         return hipGetLastError();
     }
     if (CMC_BRIDGE_WAVE_TILE == 128 && g.N % 256 == 0) return launch_gemm_t<128, 32>(epi, g, stream);
