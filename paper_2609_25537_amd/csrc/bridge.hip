@@ -75,9 +75,20 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
     tn = local / gm;
 }
 
+// Build-time tuning knob: register stages of the global -> LDS staging (1 or
+// 2; see gemm_nt_kernel).
+#ifndef CMC_BRIDGE_REG_STAGES
+#define CMC_BRIDGE_REG_STAGES 2
+#endif
+
 // WT x WT per wave (4 x 4 or 8 x 8 MFMA tiles of 16 x 16), BK of K per LDS
-// slice; the workgroup tile is 2 WT x 2 WT.
-template <int EPI, int WT, int BK>
+// slice; the workgroup tile is 2 WT x 2 WT.  RS register stages: with one,
+// slice j + 1 is loaded while slice j feeds the MFMAs and the barrier after
+// storing it drains every load; with two, slice j + 2 is loaded while slices
+// j and j + 1 are computed (two register sets used in turn, the loop unrolled
+// by two) and the barriers wait only for LDS, so each load has two slices of
+// MFMA work to land.
+template <int EPI, int WT, int BK, int RS>
 __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
     constexpr int BM = 2 * WT, BN = 2 * WT, LDK = BK + 8, T = WT / 16;
     constexpr int kRowChunks = BK / 8;                            // 16-byte chunks per tile row
@@ -94,23 +105,21 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
 
     // Global -> register -> LDS staging: chunk c = tid + 256 i is row
     // c / kRowChunks, 16-byte column group c % kRowChunks of the BM x BK slice.
-    // One register stage: slice j + 1 is loaded while slice j feeds the MFMAs.
-    uint4 ra[kChunks], rb[kChunks];
     const int crow0 = tid / kRowChunks, ccol = (tid % kRowChunks) * 8;
     const uint16_t *Ag = p.A + (size_t)ccol, *Bg = p.B + (size_t)n0 * p.K + (size_t)ccol;
-#define CMC_GLOAD(K0_)                                                                                   \
+#define CMC_GLOAD(RA_, RB_, K0_)                                                                         \
     do {                                                                                                 \
         _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
             const int ar = min(m0 + crow0 + kRowsPerPass * i, p.M - 1); /* past M: clamped, discarded */ \
-            ra[i] = *reinterpret_cast<const uint4 *>(Ag + (size_t)ar * p.K + (K0_));                    \
-            rb[i] = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + kRowsPerPass * i) * p.K + (K0_)); \
+            RA_[i] = *reinterpret_cast<const uint4 *>(Ag + (size_t)ar * p.K + (K0_));                   \
+            RB_[i] = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + kRowsPerPass * i) * p.K + (K0_)); \
         }                                                                                                \
     } while (0)
-#define CMC_SSTORE(BUF_)                                                                                 \
+#define CMC_SSTORE(RA_, RB_, BUF_)                                                                       \
     do {                                                                                                 \
         _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
-            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = ra[i];     \
-            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = rb[i];     \
+            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = RA_[i];    \
+            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) = RB_[i];    \
         }                                                                                                \
     } while (0)
 
@@ -122,35 +131,89 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
 
     const int KT = p.K / BK;
     const int fr = lane & 15, fk = 8 * (lane >> 4);
-    CMC_GLOAD(0);
-    CMC_SSTORE(0);
-    __syncthreads();
-    for (int j = 0; j < KT; ++j) {
-        const int buf = j & 1;
-        // The last slice reloads itself: no load sits behind a branch (a
-        // conditional load here made the compiler keep the staging registers
-        // in scratch memory); the copy is never read.
-        CMC_GLOAD(min(j + 1, KT - 1) * BK);
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 32) {
-            bf16x8 a[T], b[T];
-#pragma unroll
-            for (int i = 0; i < T; ++i)
-                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm * WT + i * 16 + fr) * LDK + kk + fk]);
-#pragma unroll
-            for (int jj = 0; jj < T; ++jj)
-                b[jj] = *reinterpret_cast<const bf16x8 *>(&sB[buf][(wn * WT + jj * 16 + fr) * LDK + kk + fk]);
-#pragma unroll
-            for (int i = 0; i < T; ++i)
-#pragma unroll
-                for (int jj = 0; jj < T; ++jj)
-                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
-        }
-        CMC_SSTORE(buf ^ 1);
+#define CMC_MMA(BUF_)                                                                                    \
+    do {                                                                                                 \
+        _Pragma("unroll") for (int kk = 0; kk < BK; kk += 32) {                                          \
+            bf16x8 a[T], b[T];                                                                           \
+            _Pragma("unroll") for (int i = 0; i < T; ++i)                                                \
+                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[BUF_][(wm * WT + i * 16 + fr) * LDK + kk + fk]); \
+            _Pragma("unroll") for (int jj = 0; jj < T; ++jj)                                             \
+                b[jj] = *reinterpret_cast<const bf16x8 *>(&sB[BUF_][(wn * WT + jj * 16 + fr) * LDK + kk + fk]); \
+            _Pragma("unroll") for (int i = 0; i < T; ++i)                                                \
+                _Pragma("unroll") for (int jj = 0; jj < T; ++jj)                                         \
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0); \
+        }                                                                                                \
+    } while (0)
+    // Past the last slice the loads reload it: no load sits behind a branch
+    // (a conditional load here made the compiler keep the staging registers in
+    // scratch memory); such copies are never computed on.
+    if constexpr (RS == 1) {
+        uint4 ra[kChunks], rb[kChunks];
+        CMC_GLOAD(ra, rb, 0);
+        CMC_SSTORE(ra, rb, 0);
         __syncthreads();
+        for (int j = 0; j < KT; ++j) {
+            const int buf = j & 1;
+            CMC_GLOAD(ra, rb, min(j + 1, KT - 1) * BK);
+            CMC_MMA(buf);
+            CMC_SSTORE(ra, rb, buf ^ 1);
+            __syncthreads();
+        }
+    } else {
+        // Barrier after LDS stores that waits for LDS only (s_waitcnt
+        // lgkmcnt(0), vmcnt and expcnt at their maxima): the fences of
+        // __syncthreads would drain the loads in flight.
+#define CMC_LDS_SYNC()                                             \
+    do {                                                           \
+        __builtin_amdgcn_s_waitcnt(0xC07F);                        \
+        __builtin_amdgcn_s_barrier();                              \
+    } while (0)
+        // Each register set is one vector value (arrays carried across the
+        // loop were kept in scratch memory).
+        typedef uint32_t stage_t __attribute__((ext_vector_type(4 * kChunks)));
+        stage_t ra0, rb0, ra1, rb1;
+#define CMC_VLOAD(RA_, RB_, K0_)                                                                         \
+    do {                                                                                                 \
+        _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
+            const int ar = min(m0 + crow0 + kRowsPerPass * i, p.M - 1); /* past M: clamped, discarded */ \
+            const uint4 ta = *reinterpret_cast<const uint4 *>(Ag + (size_t)ar * p.K + (K0_));           \
+            const uint4 tb = *reinterpret_cast<const uint4 *>(Bg + (size_t)(crow0 + kRowsPerPass * i) * p.K + (K0_)); \
+            RA_[4 * i] = ta.x; RA_[4 * i + 1] = ta.y; RA_[4 * i + 2] = ta.z; RA_[4 * i + 3] = ta.w;     \
+            RB_[4 * i] = tb.x; RB_[4 * i + 1] = tb.y; RB_[4 * i + 2] = tb.z; RB_[4 * i + 3] = tb.w;     \
+        }                                                                                                \
+    } while (0)
+#define CMC_VSTORE(RA_, RB_, BUF_)                                                                       \
+    do {                                                                                                 \
+        _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
+            *reinterpret_cast<uint4 *>(&sA[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) =            \
+                make_uint4(RA_[4 * i], RA_[4 * i + 1], RA_[4 * i + 2], RA_[4 * i + 3]);                  \
+            *reinterpret_cast<uint4 *>(&sB[BUF_][(crow0 + kRowsPerPass * i) * LDK + ccol]) =            \
+                make_uint4(RB_[4 * i], RB_[4 * i + 1], RB_[4 * i + 2], RB_[4 * i + 3]);                  \
+        }                                                                                                \
+    } while (0)
+        CMC_VLOAD(ra0, rb0, 0);
+        CMC_VSTORE(ra0, rb0, 0);
+        CMC_VLOAD(ra1, rb1, min(1, KT - 1) * BK);
+        CMC_LDS_SYNC();
+        for (int j = 0; j < KT; j += 2) {
+            // LDS buffer 0 holds slice j; set 1 is bringing slice j + 1.
+            CMC_VLOAD(ra0, rb0, min(j + 2, KT - 1) * BK);
+            CMC_MMA(0);
+            CMC_VSTORE(ra1, rb1, 1);  // buffer 1 was last read before the previous barrier
+            CMC_LDS_SYNC();
+            CMC_VLOAD(ra1, rb1, min(j + 3, KT - 1) * BK);
+            if (j + 1 < KT) CMC_MMA(1);  // uniform
+            CMC_VSTORE(ra0, rb0, 0);      // every wave read buffer 0 before the barrier above
+            CMC_LDS_SYNC();
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // drain the reloads past the end before the workgroup exits
+#undef CMC_LDS_SYNC
+#undef CMC_VLOAD
+#undef CMC_VSTORE
     }
 #undef CMC_GLOAD
 #undef CMC_SSTORE
+#undef CMC_MMA
 
     // C fragment: lane l, element r -> row 4 (l / 16) + r, column l % 16.
 #pragma unroll
@@ -428,10 +491,11 @@ hipError_t launch_gemm_t(int epi, const GemmParams &g, hipStream_t stream) {
     if (g.N % BN != 0 || g.K % BK != 0) return hipErrorInvalidValue;
     const long long tiles = (long long)((g.M + BM - 1) / BM) * (g.N / BN);
     if (tiles == 0) return hipSuccess;
+    constexpr int RS = WT == 128 ? 1 : CMC_BRIDGE_REG_STAGES;  // two sets of 128-wide tiles spill
     if (epi == 0)
-        gemm_nt_kernel<0, WT, BK><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<0, WT, BK, RS><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
     else
-        gemm_nt_kernel<1, WT, BK><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<1, WT, BK, RS><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
     return hipGetLastError();
 }
 
