@@ -22,7 +22,10 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-I", INCLUDE, "-I", CSRC]
+         "-I", INCLUDE, "-I", CSRC,
+         # Leading scalar kernel arguments arrive in SGPRs at wave launch (the
+         # decode kernel passes the fields its first loads need that way).
+         "-mllvm", "-amdgpu-kernarg-preload-count=14"]
 
 
 def _compile(src: str, objdir: str = OBJDIR, defines=()) -> str:

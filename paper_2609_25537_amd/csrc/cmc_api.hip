@@ -400,6 +400,8 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     if (!(scale == scale) || isinf(scale)) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: scale must be finite", fn);
     if (T_new < 0 || (W > 0 && T_new > W))
         return fail(CMC_ERR_INVALID_ARGUMENT, "%s: need 0 <= T_new <= W (got T_new=%d W=%d)", fn, T_new, W);
+    if (T_new > cmc::kMaxAppendRows)
+        return fail(CMC_ERR_UNSUPPORTED, "%s: T_new=%d exceeds %d rows per call", fn, T_new, cmc::kMaxAppendRows);
     if (B > 65535 || Hkv > 65535) return fail(CMC_ERR_UNSUPPORTED, "%s: B and Hkv must be <= 65535", fn);
     if (W == 0) T_new = 0;  // no Tier-2: appending is a no-op
     if (B == 0) return ok();

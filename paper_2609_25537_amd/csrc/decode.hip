@@ -225,13 +225,14 @@ struct RingCount {
 // count is advanced, but the compiler waits for it where the branch ends, so
 // callers issue it next to loads they wait for anyway.
 struct Arrival {
-    unsigned *ctr;
-    bool pending;  // wave-uniform
+    unsigned *ctrs;  // the sequence counters; the address is formed only in arrive(),
+    int b;           // so no wait for that kernel argument precedes the first loads
+    bool pending;    // wave-uniform
     unsigned prev;
     __device__ __forceinline__ void arrive(int cnt_raw) {
         if (pending) {
             if (threadIdx.x == 0)
-                prev = __hip_atomic_fetch_add(ctr, (unsigned)(cnt_raw != INT_MIN) /* == 1 */, __ATOMIC_RELAXED,
+                prev = __hip_atomic_fetch_add(ctrs + b, (unsigned)(cnt_raw != INT_MIN) /* == 1 */, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT);
             pending = false;
         }
@@ -257,11 +258,18 @@ struct Arrival {
 // new rows are written to.  (A masked slot that is being overwritten in the
 // same launch may be read before or after the write: its value is unused.)
 
+// IX: rows through the index list (else the pool is the gathered block and
+// row r is pool row r; the list pointer is then never read).
+template <bool IX>
 struct PoolRows {
-    const int32_t *idx;  // this sequence's index list, or nullptr
+    const int32_t *idx;  // index list base (IX)
+    size_t off;          // this sequence's first entry
     int nmax;
     static constexpr bool kMasked = false;
-    __device__ __forceinline__ int key(int row) const { return idx ? idx[row] : row; }
+    __device__ __forceinline__ int key(int row) const {
+        if constexpr (IX) return idx[off + row];
+        else return row;
+    }
     __device__ __forceinline__ int slot(int, int key) const { return key < 0 ? 0 : (key > nmax ? nmax : key); }
     __device__ __forceinline__ bool valid(int) const { return true; }
     __device__ __forceinline__ bool all_valid(int, int) const { return true; }
@@ -552,7 +560,7 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
 #undef CMC_AFTER_FIRST_LOAD
 }
 
-template <int NW, int DH, int G>
+template <int NW, int DH, int G, bool IX>
 __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int kb, int c0, int c1,
                                           RingCount &cnt, float *s_p, WaveState<G, DH / 16> &st, Arrival &arr) {
     QOperand<DH> qo;
@@ -563,10 +571,10 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
 
     // pool rows
     {
-        const PoolRows rows{p.idx ? p.idx + (size_t)b * p.k : nullptr, p.N > 0 ? p.N - 1 : 0};
+        const PoolRows<IX> rows{p.idx, (size_t)b * p.k, p.N > 0 ? p.N - 1 : 0};
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
-        mfma_phase<NW, DH, G, PoolRows, false>(p, b, kvh, c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qo,
+        mfma_phase<NW, DH, G, PoolRows<IX>, false>(p, b, kvh, c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qo,
                                                cnt, s_p, st, arr);
     }
     if (p.W > 0) {
@@ -728,8 +736,29 @@ __device__ __forceinline__ float combine_waves(const float (&sm)[NW][G], const f
     return M;
 }
 
-template <int NW, typename T, int DH, int G, bool MF>
-__global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
+// The leading arguments are the fields the first K/V loads need (info packs
+// S, new_split, whether k_len is given, and T_new); they arrive in
+// SGPRs at wave launch (kernel-argument preloading, 14 dwords), so those
+// loads never wait for the kernel-argument segment.  The rest of the
+// parameters come from `pm`.
+template <int NW, typename T, int DH, int G, bool MF, bool IX>
+__global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, const void *cme_v, void *win_k,
+                                                            void *win_v, int k, int W, int N, int Hkv, int chunk,
+                                                            int info, DecodeParams pm) {
+    DecodeParams p = pm;
+    p.cme_k = cme_k;
+    p.cme_v = cme_v;
+    p.win_k = win_k;
+    p.win_v = win_v;
+    p.k = k;
+    p.W = W;
+    p.N = N;
+    p.Hkv = Hkv;
+    p.chunk = chunk;
+    p.S = info & 0xFF;
+    p.new_split = (info >> 8) & 1;
+    const bool has_klen = (info >> 10) & 1;
+    p.T_new = (int)((unsigned)info >> 16);
     constexpr int kThreads = NW * kWave;
     constexpr int VEC = MF ? DH / 16 : Vec16<T>::N;  // output dims a lane accumulates
     const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -749,7 +778,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
         }
     }
     int kb = p.k;  // pool rows of this sequence
-    if (p.k_len) {
+    if (has_klen) {
         const int v = p.k_len[b];
         kb = v < 0 ? 0 : (v > p.k ? p.k : v);
     }
@@ -778,13 +807,13 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(DecodeParams p) {
     // re-arms the counter.  No data is published through the counter, so no
     // fence is needed.
     const bool bump = p.T_new > 0 && p.W > 0;
-    Arrival arr{p.seq_counter + b, bump && wave == 0 && p.S == 1, 0u};
+    Arrival arr{p.seq_counter, b, bump && wave == 0 && p.S == 1, 0u};
 
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
         __shared__ float s_pw[NW][16 * G];
-        mfma_loop<NW, DH, G>(p, b, kvh, kb, c0, c1, cnt, s_pw[threadIdx.x >> 6], st, arr);
+        mfma_loop<NW, DH, G, IX>(p, b, kvh, kb, c0, c1, cnt, s_pw[threadIdx.x >> 6], st, arr);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
@@ -933,14 +962,23 @@ template <typename T, int DH, int G>
 hipError_t launch3(const DecodeParams &p, hipStream_t stream) {
     dim3 grid(p.S, p.Hkv, p.B);
     constexpr bool kMf = sizeof(T) == 2 && G >= CMC_MFMA_MIN_G && G <= 4;
+    if (p.S < 1 || p.S > 0xFF || p.T_new < 0 || p.T_new > kMaxAppendRows) return hipErrorInvalidValue;
+    const int info = p.S | (p.new_split << 8) | ((p.k_len != nullptr) << 10) | (p.T_new << 16);
+    const bool ix = kMf && p.idx != nullptr;
+#define CMC_LAUNCH(NW_, IX_)                                                                                     \
+    decode_kernel<NW_, T, DH, G, kMf, IX_><<<grid, NW_ * kWave, 0, stream>>>(p.cme_k, p.cme_v, p.win_k, p.win_v, \
+                                                                             p.k, p.W, p.N, p.Hkv, p.chunk, info, p)
     if (p.waves == 4) {
-        decode_kernel<4, T, DH, G, kMf><<<grid, 4 * kWave, 0, stream>>>(p);
+        if (ix) CMC_LAUNCH(4, kMf);
+        else CMC_LAUNCH(4, false);
     } else if constexpr (decode_waves_ok(8, G, DH)) {
         if (p.waves != 8) return hipErrorInvalidValue;
-        decode_kernel<8, T, DH, G, kMf><<<grid, 8 * kWave, 0, stream>>>(p);
+        if (ix) CMC_LAUNCH(8, kMf);
+        else CMC_LAUNCH(8, false);
     } else {
         return hipErrorInvalidValue;
     }
+#undef CMC_LAUNCH
     return hipGetLastError();
 }
 

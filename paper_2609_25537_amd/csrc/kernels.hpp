@@ -38,6 +38,9 @@ struct DecodeParams {
     float qscale;             // scale * log2(e)
 };
 
+// Rows one decode call may append (the launch packs T_new into 16 bits).
+constexpr int kMaxAppendRows = 65535;
+
 // Key-axis split plan; depends only on sizes, so the workspace query and the
 // launch agree.  Workspace layout: [sequence counters | pair counters]
 // (zero between calls), then the per-split partials.

@@ -180,6 +180,13 @@ def test_decode_step_ragged_needs_new_rows():
     assert _dec_r(step=True, T=0) == cmc.CMC_ERR_INVALID_ARGUMENT
 
 
+def test_decode_step_append_row_limit():
+    """At most 65535 rows appended per call (the launch packs T_new into 16
+    bits); beyond that the call is refused before anything is enqueued."""
+    assert _dec_r(step=True, W=70000, T=65536) == cmc.CMC_ERR_UNSUPPORTED
+    assert "65535" in cmc.last_error()
+
+
 def _loc(**kw):
     a = dict(nrm=FAKE, n=None, ctx=FAKE, B=2, N=64, m=4, off=FAKE, nch=16, ct=0, W=32, al=FAKE, st=FAKE, s=None)
     a.update(kw)
