@@ -75,6 +75,14 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
     tn = local / gm;
 }
 
+// Build-time tuning knob: K slice of the 64 x 64-per-wave kernel (32, 64 or
+// 128; shapes whose K it does not divide use 64).  On the 49152 x 1280 ->
+// 4096 -> 4096 projection: 32 -> 3.31 ms per call (148 VGPRs, 40 KB of LDS:
+// three workgroups per CU), 64 -> 3.48 ms, 128 -> 4.84 ms.
+#ifndef CMC_BRIDGE_BK
+#define CMC_BRIDGE_BK 32
+#endif
+
 // Build-time tuning knob: register stages of the global -> LDS staging (1 or
 // 2; see gemm_nt_kernel).
 #ifndef CMC_BRIDGE_REG_STAGES
@@ -521,6 +529,7 @@ hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
         return hipGetLastError();
     }
     if (CMC_BRIDGE_WAVE_TILE == 128 && g.N % 256 == 0) return launch_gemm_t<128, 32>(epi, g, stream);
+    if (CMC_BRIDGE_BK != 64 && g.K % CMC_BRIDGE_BK == 0) return launch_gemm_t<64, CMC_BRIDGE_BK>(epi, g, stream);
     return launch_gemm_t<64, 64>(epi, g, stream);
 }
 
