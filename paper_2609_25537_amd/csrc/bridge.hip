@@ -83,8 +83,10 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
 #define CMC_BRIDGE_BK 32
 #endif
 
-// Build-time tuning knob: register stages of the global -> LDS staging (1 or
-// 2; see gemm_nt_kernel).
+// Build-time tuning knob: register stages of the global -> LDS staging (1, 2
+// or 3; see gemm_nt_kernel).  With 32-wide K slices three stages need 172
+// VGPRs (two waves per SIMD instead of three) and ran slower (3.50 ms per
+// projection call against 3.25 ms with two).
 #ifndef CMC_BRIDGE_REG_STAGES
 #define CMC_BRIDGE_REG_STAGES 2
 #endif
@@ -168,6 +170,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
             __syncthreads();
         }
     } else {
+        static_assert(RS == 2 || RS == 3, "one, two or three register stages");
         // Barrier after LDS stores that waits for LDS only (s_waitcnt
         // lgkmcnt(0), vmcnt and expcnt at their maxima): the fences of
         // __syncthreads would drain the loads in flight.
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
         // Each register set is one vector value (arrays carried across the
         // loop were kept in scratch memory).
         typedef uint32_t stage_t __attribute__((ext_vector_type(4 * kChunks)));
-        stage_t ra0, rb0, ra1, rb1;
+        stage_t ra0, rb0, ra1, rb1, ra2, rb2;
 #define CMC_VLOAD(RA_, RB_, K0_)                                                                         \
     do {                                                                                                 \
         _Pragma("unroll") for (int i = 0; i < kChunks; ++i) {                                            \
@@ -199,20 +202,43 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
                 make_uint4(RB_[4 * i], RB_[4 * i + 1], RB_[4 * i + 2], RB_[4 * i + 3]);                  \
         }                                                                                                \
     } while (0)
-        CMC_VLOAD(ra0, rb0, 0);
-        CMC_VSTORE(ra0, rb0, 0);
-        CMC_VLOAD(ra1, rb1, min(1, KT - 1) * BK);
-        CMC_LDS_SYNC();
-        for (int j = 0; j < KT; j += 2) {
-            // LDS buffer 0 holds slice j; set 1 is bringing slice j + 1.
-            CMC_VLOAD(ra0, rb0, min(j + 2, KT - 1) * BK);
-            CMC_MMA(0);
-            CMC_VSTORE(ra1, rb1, 1);  // buffer 1 was last read before the previous barrier
+        if constexpr (RS == 2) {
+            CMC_VLOAD(ra0, rb0, 0);
+            CMC_VSTORE(ra0, rb0, 0);
+            CMC_VLOAD(ra1, rb1, min(1, KT - 1) * BK);
             CMC_LDS_SYNC();
-            CMC_VLOAD(ra1, rb1, min(j + 3, KT - 1) * BK);
-            if (j + 1 < KT) CMC_MMA(1);  // uniform
-            CMC_VSTORE(ra0, rb0, 0);      // every wave read buffer 0 before the barrier above
+            for (int j = 0; j < KT; j += 2) {
+                // LDS buffer 0 holds slice j; set 1 is bringing slice j + 1.
+                CMC_VLOAD(ra0, rb0, min(j + 2, KT - 1) * BK);
+                CMC_MMA(0);
+                CMC_VSTORE(ra1, rb1, 1);  // buffer 1 was last read before the previous barrier
+                CMC_LDS_SYNC();
+                CMC_VLOAD(ra1, rb1, min(j + 3, KT - 1) * BK);
+                if (j + 1 < KT) CMC_MMA(1);  // uniform
+                CMC_VSTORE(ra0, rb0, 0);      // every wave read buffer 0 before the barrier above
+                CMC_LDS_SYNC();
+            }
+        } else {
+            // Three sets: slice s + 3 is loaded while slices s .. s + 2 are
+            // computed; LDS buffer s % 2 holds slice s at sub-step s.
+            CMC_VLOAD(ra0, rb0, 0);
+            CMC_VSTORE(ra0, rb0, 0);
+            CMC_VLOAD(ra1, rb1, min(1, KT - 1) * BK);
+            CMC_VLOAD(ra2, rb2, min(2, KT - 1) * BK);
             CMC_LDS_SYNC();
+#define CMC_SUBSTEP(S_, RL_, RBL_, RN_, RBN_)                                                \
+    do {                                                                                     \
+        CMC_VLOAD(RL_, RBL_, min((S_) + 3, KT - 1) * BK);                                    \
+        if ((S_) < KT) CMC_MMA((S_) & 1); /* uniform */                                      \
+        CMC_VSTORE(RN_, RBN_, ((S_) + 1) & 1); /* buffer last read before the last barrier */ \
+        CMC_LDS_SYNC();                                                                      \
+    } while (0)
+            for (int j = 0; j < KT; j += 3) {
+                CMC_SUBSTEP(j, ra0, rb0, ra1, rb1);
+                CMC_SUBSTEP(j + 1, ra1, rb1, ra2, rb2);
+                CMC_SUBSTEP(j + 2, ra2, rb2, ra0, rb0);
+            }
+#undef CMC_SUBSTEP
         }
         __builtin_amdgcn_s_waitcnt(0);  // drain the reloads past the end before the workgroup exits
 #undef CMC_LDS_SYNC
