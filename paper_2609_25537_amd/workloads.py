@@ -139,6 +139,12 @@ WORKLOADS: Dict[str, Workload] = {
                                D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",
                                kv_std=1.0 / math.sqrt(128.0), seed=606, ragged=True,
                                ctx_min=512, ctx_max=16384, ratio=4, q_min=8, q_max=48),
+    # The paper's own cache sizes (batch 8, K = 40 memory rows, W = 130 window
+    # tokens, contexts of up to 3072 tokens at ratio 4 -> 768 CMEs) with Llama
+    # heads: latency context next to the larger configurations.
+    "paper_scale_b8": Workload("paper_scale_b8", B=8, Hq=32, Hkv=8, Dh=128, N=768, D=4096, k=40,
+                               W=130, steps=3000, kv_dtype="bf16", kv_std=1.0 / math.sqrt(128.0),
+                               seed=909),
     # 32-layer Llama-shaped decode stack; baseline is a 32768-token full cache.
     "llama_stack32": Workload("llama_stack32", B=32, Hq=32, Hkv=8, Dh=128, N=8192,
                               D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",

@@ -86,6 +86,13 @@ def test_full_long_wide_d256(orc):
 
 
 @pytest.mark.timeout(900)
+def test_full_paper_scale_b8(orc):
+    """The paper's own cache sizes (B = 8, K = 40, W = 130, N = 768) with
+    Llama heads: k and W not multiples of the 16-row block, a split plan."""
+    _run_full(orc, "paper_scale_b8")
+
+
+@pytest.mark.timeout(900)
 def test_full_llama_stack32_layer(orc):
     """One layer of the 32-layer stack's shape (B=32, 256 (sequence, kv
     head) pairs: one 8-wave workgroup each) from the numpy streams; the
