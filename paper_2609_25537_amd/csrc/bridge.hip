@@ -8,17 +8,20 @@
 // accumulation.  A 256-thread workgroup of 2 x 2 waves computes a 2WT x 2WT
 // tile, each wave WT x WT as (WT/16)^2 v_mfma_f32_16x16x32_bf16 tiles (WT =
 // 64 by default; WT = 128 halves the LDS reads per MFMA flop but leaves one
-// workgroup per CU, and measured no faster).  K advances BK at a time
-// through two LDS buffers: the next slice is loaded into registers while
-// the current one feeds the MFMAs, then stored to the other buffer.  LDS
-// rows are padded by 8 bf16 (80 or 144 bytes) so that the 16-byte fragment
-// reads of 8 consecutive rows hit 8 disjoint groups of 4 banks.  Tiles are handed
-// out so that each XCD (workgroups are dealt round-robin to the 8 XCDs)
-// runs a contiguous run of them, N fastest: the tiles resident on one XCD
-// share their A rows in that XCD's L2.
+// workgroup per CU, and measured no faster).  K advances BK (32 by default)
+// at a time through two LDS buffers, staged from global memory through
+// register sets used in turn (two by default), so a slice's loads have the
+// MFMA work of the slices before it to land.  LDS rows are padded by 8 bf16
+// (80 or 144 bytes) so that the 16-byte fragment reads of 8 consecutive
+// rows hit 8 disjoint groups of 4 banks.  Tiles are handed out so that each
+// XCD (workgroups are dealt round-robin to the 8 XCDs) runs a contiguous run
+// of them, walked in groups of a few tile rows (see gemm_tile).
 //   Epilogue 0 (first layer): + b1, exact GELU, rounded to bf16 (the hidden
 //   activations, kept in the workspace).  Epilogue 1 (second layer): + b2,
 //   fp32 into the output.
+//
+// gemm_deep_kernel: the same product with direct-to-LDS loads and 3 or more LDS
+// stages (a build-time alternative; measured slower here).
 //
 // bridge_norm_kernel: one wave per output row, in place, the row held in
 // registers: mean and biased variance (two passes over the registers),

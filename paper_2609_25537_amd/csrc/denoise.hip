@@ -115,70 +115,68 @@ __global__ __launch_bounds__(256) void denoise_score_kernel(DenoiseParams p) {
 #pragma unroll
             for (int d = 0; d < G; ++d) dd[t][d] = 0.f;
 
-        {
-            for (int eb = 0; eb < p.H; eb += P * SPAN) {
-                // All R rows of P passes are loaded up front: rows past the
-                // sequence are clamped to its last row and columns past H to the
-                // row's last 16 bytes (in bounds), and zeroed after the load, so
-                // no load sits behind a branch.
-                uint4 raw[P][R];
+        for (int eb = 0; eb < p.H; eb += P * SPAN) {
+            // All R rows of P passes are loaded up front: rows past the
+            // sequence are clamped to its last row and columns past H to the
+            // row's last 16 bytes (in bounds), and zeroed after the load, so
+            // no load sits behind a branch.
+            uint4 raw[P][R];
 #pragma unroll
-                for (int pp = 0; pp < P; ++pp) {
-                    const int ec = min(eb + pp * SPAN + lane * VEC, p.H - VEC);
+            for (int pp = 0; pp < P; ++pp) {
+                const int ec = min(eb + pp * SPAN + lane * VEC, p.H - VEC);
 #pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        raw[pp][r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
-                                                                      (size_t)ec * sizeof(T));
-                }
+                for (int r = 0; r < R; ++r)
+                    raw[pp][r] = *reinterpret_cast<const uint4 *>(base + (size_t)min(i0 + r, nb - 1) * row_bytes +
+                                                                  (size_t)ec * sizeof(T));
+            }
 #pragma unroll
-                for (int pp = 0; pp < P; ++pp) {
-                    const bool col_on = eb + pp * SPAN + lane * VEC < p.H;
-                    if constexpr (sizeof(T) == 2) {
-                        // bf16: v_dot2 on packed pairs (two products per op, fp32
-                        // accumulation, no widening).
-                        uint32_t win[G + 1][4];  // rows r-G .. r (ring by unrolled index)
+            for (int pp = 0; pp < P; ++pp) {
+                const bool col_on = eb + pp * SPAN + lane * VEC < p.H;
+                if constexpr (sizeof(T) == 2) {
+                    // bf16: v_dot2 on packed pairs (two products per op, fp32
+                    // accumulation, no widening).
+                    uint32_t win[G + 1][4];  // rows r-G .. r (ring by unrolled index)
 #pragma unroll
-                        for (int r = 0; r < R; ++r) {
-                            const bool on = col_on && i0 + r < nb;
-                            const uint32_t w[4] = {on ? raw[pp][r].x : 0u, on ? raw[pp][r].y : 0u,
-                                                   on ? raw[pp][r].z : 0u, on ? raw[pp][r].w : 0u};
+                    for (int r = 0; r < R; ++r) {
+                        const bool on = col_on && i0 + r < nb;
+                        const uint32_t w[4] = {on ? raw[pp][r].x : 0u, on ? raw[pp][r].y : 0u,
+                                               on ? raw[pp][r].z : 0u, on ? raw[pp][r].w : 0u};
 #pragma unroll
-                            for (int k = 0; k < 4; ++k) nn[r] = dot2_bf16(w[k], w[k], nn[r]);
+                        for (int k = 0; k < 4; ++k) nn[r] = dot2_bf16(w[k], w[k], nn[r]);
 #pragma unroll
-                            for (int d = 1; d <= G; ++d) {
-                                if (r - d >= 0 && r - d < TT) {
+                        for (int d = 1; d <= G; ++d) {
+                            if (r - d >= 0 && r - d < TT) {
 #pragma unroll
-                                    for (int k = 0; k < 4; ++k)
-                                        dd[r - d][d - 1] = dot2_bf16(win[(r - d) % (G + 1)][k], w[k], dd[r - d][d - 1]);
-                                }
+                                for (int k = 0; k < 4; ++k)
+                                    dd[r - d][d - 1] = dot2_bf16(win[(r - d) % (G + 1)][k], w[k], dd[r - d][d - 1]);
                             }
-#pragma unroll
-                            for (int k = 0; k < 4; ++k) win[r % (G + 1)][k] = w[k];
                         }
-                    } else {
-                        float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
 #pragma unroll
-                        for (int r = 0; r < R; ++r) {
-                            float x[VEC];
-                            Lane16<T>::widen(raw[pp][r], x);
-                            if (!col_on || i0 + r >= nb) {
+                        for (int k = 0; k < 4; ++k) win[r % (G + 1)][k] = w[k];
+                    }
+                } else {
+                    float win[G + 1][VEC];  // rows r-G .. r of this lane slice (ring by unrolled index)
 #pragma unroll
-                                for (int v = 0; v < VEC; ++v) x[v] = 0.f;
-                            }
+                    for (int r = 0; r < R; ++r) {
+                        float x[VEC];
+                        Lane16<T>::widen(raw[pp][r], x);
+                        if (!col_on || i0 + r >= nb) {
 #pragma unroll
-                            for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
-#pragma unroll
-                            for (int d = 1; d <= G; ++d) {
-                                if (r - d >= 0 && r - d < TT) {
-                                    const float(&y)[VEC] = win[(r - d) % (G + 1)];
-#pragma unroll
-                                    for (int v = 0; v < VEC; ++v)
-                                        dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
-                                }
-                            }
-#pragma unroll
-                            for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
+                            for (int v = 0; v < VEC; ++v) x[v] = 0.f;
                         }
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) nn[r] = fmaf(x[v], x[v], nn[r]);
+#pragma unroll
+                        for (int d = 1; d <= G; ++d) {
+                            if (r - d >= 0 && r - d < TT) {
+                                const float(&y)[VEC] = win[(r - d) % (G + 1)];
+#pragma unroll
+                                for (int v = 0; v < VEC; ++v)
+                                    dd[r - d][d - 1] = fmaf(y[v], x[v], dd[r - d][d - 1]);
+                            }
+                        }
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) win[r % (G + 1)][v] = x[v];
                     }
                 }
             }
