@@ -5,23 +5,20 @@
 // -- the selection keys of Tier-1.
 //
 // gemm_nt_kernel: C[M][N] = A[M][K] . B[N][K]^T on MFMA, bf16 operands, fp32
-// accumulation.  A 256-thread workgroup of 2 x 2 waves computes a 2WT x 2WT
-// tile, each wave WT x WT as (WT/16)^2 v_mfma_f32_16x16x32_bf16 tiles (WT =
-// 64 by default; WT = 128 halves the LDS reads per MFMA flop but leaves one
-// workgroup per CU, and measured no faster).  K advances BK (32 by default)
-// at a time through two LDS buffers, staged from global memory through
+// accumulation.  A workgroup of WGM x WGN waves computes a tile of WGM WTM x
+// WGN WTN, each wave WTM x WTN as 16 x 16 v_mfma_f32_16x16x32_bf16 tiles:
+// 256 x 256 from eight waves of 128 x 64 where N allows (one workgroup per
+// CU), else 128 x 128 from four waves of 64 x 64 (three per CU).  K advances
+// BK at a time through two LDS buffers, staged from global memory through
 // register sets used in turn (two by default), so a slice's loads have the
 // MFMA work of the slices before it to land.  LDS rows are padded by 8 bf16
 // (80 or 144 bytes) so that the 16-byte fragment reads of 8 consecutive
 // rows hit 8 disjoint groups of 4 banks.  Tiles are handed out so that each
 // XCD (workgroups are dealt round-robin to the 8 XCDs) runs a contiguous run
-// of them, walked in groups of a few tile rows (see gemm_tile).
-//   Epilogue 0 (first layer): + b1, exact GELU, rounded to bf16 (the hidden
-//   activations, kept in the workspace).  Epilogue 1 (second layer): + b2,
-//   fp32 into the output.
-//
-// gemm_deep_kernel: the same product with direct-to-LDS loads and 3 or more LDS
-// stages (a build-time alternative; measured slower here).
+// of them, walked in groups of a few tile rows (see gemm_tile).  The
+// epilogue (store_tile) adds the bias and, for the first layer, applies GELU
+// and rounds to bf16 (the hidden activations, kept in the workspace); the
+// second layer's fp32 result goes to the output.
 //
 // bridge_norm_kernel: one wave per output row, in place, the row held in
 // registers: mean and biased variance (two passes over the registers),
@@ -36,7 +33,6 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGemmThreads = 256;  // 2 x 2 waves
 
 struct GemmParams {
     const uint16_t *A;  // [M][K]
@@ -46,7 +42,19 @@ struct GemmParams {
     int M, N, K;
 };
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+// GELU(x) = x Phi(x), Phi(x) = (1 + erf(x / sqrt 2)) / 2, with erfc(z) for z =
+// |x| / sqrt 2 >= 0 from Abramowitz & Stegun 7.1.26: erfc(z) = t (a1 + t (a2 +
+// t (a3 + t (a4 + t a5)))) exp(-z^2), t = 1 / (1 + p z), absolute error at most
+// 1.5e-7, below the bf16 rounding the hidden activations then take.  Phi(x) is
+// 1 - erfc(z) / 2 for x >= 0 and erfc(z) / 2 below.
+__device__ __forceinline__ float gelu_erf(float x) {
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.f));
+    const float poly =
+        t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f), 0.254829592f);
+    const float half_erfc = 0.5f * poly * __builtin_amdgcn_exp2f(-1.4426950408889634f * z * z);
+    return x * (x >= 0.f ? 1.f - half_erfc : half_erfc);
+}
 
 __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -78,6 +86,38 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
     tn = local / gm;
 }
 
+// Epilogue of one wave's accumulators.  The MFMAs compute each 16 x 16 tile
+// transposed (B rows as the first operand), so lane l, element r holds tile
+// row l % 16, tile column 4 (l / 16) + r: four consecutive columns of one
+// row, written with one 8-byte (bf16) or 16-byte (fp32) store.
+//   Epilogue 0 (first layer): + b1, exact GELU, rounded to bf16.
+//   Epilogue 1 (second layer): + b2, fp32.
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void store_tile(const GemmParams &p, const floatx4 (&acc)[TM][TN], int r0, int c0,
+                                           int lane) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = c0 + j * 16 + 4 * (lane >> 4);
+        const float4 bias = *reinterpret_cast<const float4 *>(p.bias + col);  // 16-byte aligned
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = r0 + i * 16 + (lane & 15);
+            if (row < p.M) {
+                const float v0 = acc[i][j][0] + bias.x, v1 = acc[i][j][1] + bias.y;
+                const float v2 = acc[i][j][2] + bias.z, v3 = acc[i][j][3] + bias.w;
+                if constexpr (EPI == 0) {
+                    const uint2 w = make_uint2((uint32_t)to_bf16_rne(gelu_erf(v0)) | ((uint32_t)to_bf16_rne(gelu_erf(v1)) << 16),
+                                               (uint32_t)to_bf16_rne(gelu_erf(v2)) | ((uint32_t)to_bf16_rne(gelu_erf(v3)) << 16));
+                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(p.C) + (size_t)row * p.N + col) = w;
+                } else {
+                    *reinterpret_cast<float4 *>(static_cast<float *>(p.C) + (size_t)row * p.N + col) =
+                        make_float4(v0, v1, v2, v3);
+                }
+            }
+        }
+    }
+}
+
 // Build-time tuning knob: K slice of the 64 x 64-per-wave kernel (32, 64 or
 // 128; shapes whose K it does not divide use 64).  On the 49152 x 1280 ->
 // 4096 -> 4096 projection: 32 -> 3.31 ms per call (148 VGPRs, 40 KB of LDS:
@@ -101,16 +141,19 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
 // j and j + 1 are computed (two register sets used in turn, the loop unrolled
 // by two) and the barriers wait only for LDS, so each load has two slices of
 // MFMA work to land.
-template <int EPI, int WT, int BK, int RS>
-__global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
-    constexpr int BM = 2 * WT, BN = 2 * WT, LDK = BK + 8, T = WT / 16;
-    constexpr int kRowChunks = BK / 8;                            // 16-byte chunks per tile row
-    constexpr int kChunks = BM * kRowChunks / kGemmThreads;       // per thread per matrix per slice
-    constexpr int kRowsPerPass = kGemmThreads / kRowChunks;
+template <int EPI, int WTM, int WTN, int WGM, int WGN, int BK, int RS>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams p) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int BM = WGM * WTM, BN = WGN * WTN, LDK = BK + 8, TM = WTM / 16, TN = WTN / 16;
+    static_assert(BM == BN, "the A and B slices share one staging map");
+    constexpr int kRowChunks = BK / 8;                  // 16-byte chunks per tile row
+    constexpr int kChunks = BM * kRowChunks / NT;       // per thread per matrix per slice
+    constexpr int kRowsPerPass = NT / kRowChunks;
+    static_assert(kChunks * NT == BM * kRowChunks, "whole chunks per thread");
     __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDK];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
 
     int tm, tn;
     gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
@@ -136,25 +179,25 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
         }                                                                                                \
     } while (0)
 
-    floatx4 acc[T][T];
+    floatx4 acc[TM][TN];
 #pragma unroll
-    for (int i = 0; i < T; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < T; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < TN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     const int KT = p.K / BK;
     const int fr = lane & 15, fk = 8 * (lane >> 4);
 #define CMC_MMA(BUF_)                                                                                    \
     do {                                                                                                 \
         _Pragma("unroll") for (int kk = 0; kk < BK; kk += 32) {                                          \
-            bf16x8 a[T], b[T];                                                                           \
-            _Pragma("unroll") for (int i = 0; i < T; ++i)                                                \
-                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[BUF_][(wm * WT + i * 16 + fr) * LDK + kk + fk]); \
-            _Pragma("unroll") for (int jj = 0; jj < T; ++jj)                                             \
-                b[jj] = *reinterpret_cast<const bf16x8 *>(&sB[BUF_][(wn * WT + jj * 16 + fr) * LDK + kk + fk]); \
-            _Pragma("unroll") for (int i = 0; i < T; ++i)                                                \
-                _Pragma("unroll") for (int jj = 0; jj < T; ++jj)                                         \
-                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0); \
+            bf16x8 a[TM], b[TN];                                                                         \
+            _Pragma("unroll") for (int i = 0; i < TM; ++i)                                               \
+                a[i] = *reinterpret_cast<const bf16x8 *>(&sA[BUF_][(wm * WTM + i * 16 + fr) * LDK + kk + fk]); \
+            _Pragma("unroll") for (int jj = 0; jj < TN; ++jj)                                            \
+                b[jj] = *reinterpret_cast<const bf16x8 *>(&sB[BUF_][(wn * WTN + jj * 16 + fr) * LDK + kk + fk]); \
+            _Pragma("unroll") for (int i = 0; i < TM; ++i)                                               \
+                _Pragma("unroll") for (int jj = 0; jj < TN; ++jj)                                        \
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[jj], a[i], acc[i][jj], 0, 0, 0); \
         }                                                                                                \
     } while (0)
     // Past the last slice the loads reload it: no load sits behind a branch
@@ -252,143 +295,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_nt_kernel(GemmParams p) {
 #undef CMC_SSTORE
 #undef CMC_MMA
 
-    // C fragment: lane l, element r -> row 4 (l / 16) + r, column l % 16.
-#pragma unroll
-    for (int j = 0; j < T; ++j) {
-        const int col = n0 + wn * WT + j * 16 + fr;
-        const float bias = p.bias[col];
-#pragma unroll
-        for (int i = 0; i < T; ++i) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = m0 + wm * WT + i * 16 + 4 * (lane >> 4) + r;
-                if (row < p.M) {
-                    const float v = acc[i][j][r] + bias;
-                    if constexpr (EPI == 0)
-                        static_cast<uint16_t *>(p.C)[(size_t)row * p.N + col] = to_bf16_rne(gelu_erf(v));
-                    else
-                        static_cast<float *>(p.C)[(size_t)row * p.N + col] = v;
-                }
-            }
-        }
-    }
-}
-
-// Deep-pipelined variant: 256 x 256 workgroup tile (128 x 128 per wave),
-// K in slices of 32 staged through NS LDS stages by direct-to-LDS loads
-// (global_load_lds, 16 bytes per lane), so NS - 1 slices are in flight with
-// no registers held for them.  Each 16-row x 32-k block of a slice occupies
-// 1 KB of LDS in MFMA fragment order -- lane l's 16 bytes at offset 16 l are
-// row l % 16, k 8 (l / 16) .. +7, exactly the A/B operand of
-// v_mfma_f32_16x16x32_bf16 -- so the global load of a block and the
-// fragment read of it use the same lane mapping and the read is one
-// contiguous, bank-conflict-free ds_read_b128.  Waves 0-1 load the A
-// blocks of a slice, waves 2-3 the B blocks (WT / 16 blocks per wave).
-// WT x WT per wave, 2 WT x 2 WT per workgroup: WT = 128 holds 256
-// accumulators per lane (one wave per SIMD), WT = 64 keeps two workgroups
-// per CU.
-#ifndef CMC_BRIDGE_DEEP_STAGES
-#define CMC_BRIDGE_DEEP_STAGES 4
-#endif
-#ifndef CMC_BRIDGE_DEEP_WT
-#define CMC_BRIDGE_DEEP_WT 128
-#endif
-constexpr int kDeepStages = CMC_BRIDGE_DEEP_STAGES;
-
-template <int EPI, int WT>
-__global__ __launch_bounds__(kGemmThreads) void gemm_deep_kernel(GemmParams p) {
-    constexpr int BM = 2 * WT, BN = 2 * WT, BK = 32, T = WT / 16, NS = kDeepStages;
-    constexpr int kBlk = 1024;                          // bytes per 16 x 32 block
-    constexpr int kStage = (BM / 16 + BN / 16) * kBlk;  // WT / 4 KB
-    constexpr int LPW = T;                              // blocks (loads) per wave per slice
-    static_assert(NS >= 3 && NS * kStage <= 160 * 1024, "the stages must fit the 160 KB of LDS");
-    __shared__ __attribute__((aligned(1024))) char smem[NS * kStage];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    int tm, tn;
-    gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-
-    // This lane's source rows for the LPW blocks its wave loads per slice.
-    const bool loads_a = wave < 2;
-    const int blk0 = (wave & 1) * LPW;               // first block (of 2 LPW) of this wave's matrix
-    const int fr = lane & 15, fk = 8 * (lane >> 4);
-    const uint16_t *src[LPW];
-#pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-        const int r = (blk0 + i) * 16 + fr;
-        src[i] = loads_a ? p.A + (size_t)min(m0 + r, p.M - 1) * p.K + fk : p.B + (size_t)(n0 + r) * p.K + fk;
-    }
-    const int ldsw = (loads_a ? 0 : (BM / 16) * kBlk) + blk0 * kBlk;  // this wave's blocks, in a stage
-    auto issue = [&](int slice) {
-        const int st = slice % NS;
-        char *dst = smem + st * kStage + ldsw;
-#pragma unroll
-        for (int i = 0; i < LPW; ++i)
-            __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)slice * BK),
-                                             (__attribute__((address_space(3))) void *)(dst + i * kBlk), 16, 0, 0);
-    };
-
-    floatx4 acc[T][T];
-#pragma unroll
-    for (int i = 0; i < T; ++i)
-#pragma unroll
-        for (int j = 0; j < T; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    const int KT = p.K / BK;
-    // Prologue: slices 0 .. NS-2 in flight.  Past the end the last slice is
-    // loaded again (identical bytes into its own stage), which keeps LPW
-    // loads per wave per iteration so that the counted wait below stays exact.
-#pragma unroll
-    for (int sl = 0; sl < NS - 1; ++sl) issue(min(sl, KT - 1));
-    for (int j = 0; j < KT; ++j) {
-        // Wait for this wave's loads of slice j (the NS - 2 later slices may
-        // stay in flight: LPW loads each), then for every wave's.  A bare
-        // s_barrier: the fences of __syncthreads would drain every load.
-        // s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
-        // at their maxima (not waited).
-        constexpr int kVm = LPW * (NS - 2);
-        static_assert(kVm < 64, "vmcnt field is 6 bits");
-        __builtin_amdgcn_s_waitcnt((kVm & 15) | ((kVm >> 4) << 14) | (7 << 4) | (15 << 8));
-        __builtin_amdgcn_s_barrier();
-        // Stage (j - 1) % NS was read by every wave before the barrier: refill it.
-        issue(min(j + NS - 1, KT - 1));
-        const char *stg = smem + (j % NS) * kStage;
-        bf16x8 a[T], b[T];
-#pragma unroll
-        for (int i = 0; i < T; ++i)
-            a[i] = *reinterpret_cast<const bf16x8 *>(stg + (wm * T + i) * kBlk + lane * 16);
-#pragma unroll
-        for (int jj = 0; jj < T; ++jj)
-            b[jj] = *reinterpret_cast<const bf16x8 *>(stg + (BM / 16 + wn * T + jj) * kBlk + lane * 16);
-#pragma unroll
-        for (int i = 0; i < T; ++i)
-#pragma unroll
-            for (int jj = 0; jj < T; ++jj)
-                acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // drain the reloads past the end before the workgroup exits
-
-#pragma unroll
-    for (int j = 0; j < T; ++j) {
-        const int col = n0 + wn * WT + j * 16 + fr;
-        const float bias = p.bias[col];
-#pragma unroll
-        for (int i = 0; i < T; ++i) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = m0 + wm * WT + i * 16 + 4 * (lane >> 4) + r;
-                if (row < p.M) {
-                    const float v = acc[i][j][r] + bias;
-                    if constexpr (EPI == 0)
-                        static_cast<uint16_t *>(p.C)[(size_t)row * p.N + col] = to_bf16_rne(gelu_erf(v));
-                    else
-                        static_cast<float *>(p.C)[(size_t)row * p.N + col] = v;
-                }
-            }
-        }
-    }
+    store_tile<EPI, TM, TN>(p, acc, m0 + wm * WTM, n0 + wn * WTN, lane);
 }
 
 // One wave per row; the row stays in registers (NV float4 per lane, Hd <=
@@ -513,53 +420,48 @@ hipError_t launch_norm(const BridgeParams &p, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// Build-time tuning knob: wave tile of the bridge GEMMs, 64 (128 x 128 per
-// workgroup, two workgroups per CU) or 128 (256 x 256, one per CU; for N a
-// multiple of 256).  Measured on the 49152 x 1280 -> 4096 -> 4096 workload:
-// 64 is slightly faster; both are held back by global-load latency with one
-// slice in flight.
-#ifndef CMC_BRIDGE_WAVE_TILE
-#define CMC_BRIDGE_WAVE_TILE 64
-#endif
-
-template <int WT, int BK>
+template <int WTM, int WTN, int WGM, int WGN, int BK, int RS>
 hipError_t launch_gemm_t(int epi, const GemmParams &g, hipStream_t stream) {
-    constexpr int BM = 2 * WT, BN = 2 * WT;
+    constexpr int BM = WGM * WTM, BN = WGN * WTN, NT = 64 * WGM * WGN;
     if (g.N % BN != 0 || g.K % BK != 0) return hipErrorInvalidValue;
     const long long tiles = (long long)((g.M + BM - 1) / BM) * (g.N / BN);
     if (tiles == 0) return hipSuccess;
-    constexpr int RS = WT == 128 ? 1 : CMC_BRIDGE_REG_STAGES;  // two sets of 128-wide tiles spill
     if (epi == 0)
-        gemm_nt_kernel<0, WT, BK, RS><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<0, WTM, WTN, WGM, WGN, BK, RS><<<(unsigned)tiles, NT, 0, stream>>>(g);
     else
-        gemm_nt_kernel<1, WT, BK, RS><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
+        gemm_nt_kernel<1, WTM, WTN, WGM, WGN, BK, RS><<<(unsigned)tiles, NT, 0, stream>>>(g);
     return hipGetLastError();
 }
 
-// Build-time tuning knob: 1 runs the deep-pipelined direct-to-LDS kernel for
-// the shapes it takes (N % (2 CMC_BRIDGE_DEEP_WT) == 0, K % 32 == 0).  On the
-// 49152 x 1280 -> 4096 -> 4096 projection it measured 4.05 ms per call with
-// 256 x 256 tiles and 4 stages (4.02 with 5), 4.35 - 4.66 ms with 128 x 128
-// tiles and 3 - 5 stages, against 3.66 ms for the register-staged kernels,
-// so those are the default.
-#ifndef CMC_BRIDGE_DEEP
-#define CMC_BRIDGE_DEEP 0
+// Build-time tuning knob: 1 runs N % 256 == 0 shapes on 256 x 256 tiles of
+// eight waves, 128 x 64 each (one workgroup per CU), with K slices of
+// CMC_BRIDGE_BIG_BK and CMC_BRIDGE_BIG_STAGES register stages; other shapes
+// (and 0) use 128 x 128 tiles of four 64 x 64 waves.  On the 49152 x 1280 ->
+// 4096 -> 4096 projection: 128 x 128 tiles 3.22 ms per call; 256 x 256 tiles
+// with 32-wide slices 3.14 ms (two stages) and 2.99 ms (three), with 64-wide
+// slices 3.05 ms (one stage) and 2.94 ms (two); the same with the transposed
+// accumulators' vector stores 2.79 ms.  A direct-to-LDS variant of the
+// 256 x 256 tile (four or five LDS stages, fragment reads interleaved with
+// the MFMAs) measured 2.95 - 3.06 ms.
+#ifndef CMC_BRIDGE_BIG
+#define CMC_BRIDGE_BIG 1
+#endif
+#ifndef CMC_BRIDGE_BIG_BK
+#define CMC_BRIDGE_BIG_BK 64
+#endif
+#ifndef CMC_BRIDGE_BIG_STAGES
+#define CMC_BRIDGE_BIG_STAGES 2
 #endif
 
 hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
-    constexpr int DB = 2 * CMC_BRIDGE_DEEP_WT;
-    if (CMC_BRIDGE_DEEP && g.N % DB == 0 && g.K % 32 == 0) {
-        const long long tiles = (long long)((g.M + DB - 1) / DB) * (g.N / DB);
-        if (tiles == 0) return hipSuccess;
-        if (epi == 0)
-            gemm_deep_kernel<0, CMC_BRIDGE_DEEP_WT><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
-        else
-            gemm_deep_kernel<1, CMC_BRIDGE_DEEP_WT><<<(unsigned)tiles, kGemmThreads, 0, stream>>>(g);
-        return hipGetLastError();
+    if constexpr (CMC_BRIDGE_BIG) {
+        if (g.N % 256 == 0 && g.K % CMC_BRIDGE_BIG_BK == 0)
+            return launch_gemm_t<128, 64, 2, 4, CMC_BRIDGE_BIG_BK, CMC_BRIDGE_BIG_STAGES>(epi, g, stream);
     }
-    if (CMC_BRIDGE_WAVE_TILE == 128 && g.N % 256 == 0) return launch_gemm_t<128, 32>(epi, g, stream);
-    if (CMC_BRIDGE_BK != 64 && g.K % CMC_BRIDGE_BK == 0) return launch_gemm_t<64, CMC_BRIDGE_BK>(epi, g, stream);
-    return launch_gemm_t<64, 64>(epi, g, stream);
+    constexpr int RS = CMC_BRIDGE_REG_STAGES;
+    if (CMC_BRIDGE_BK != 64 && g.K % CMC_BRIDGE_BK == 0)
+        return launch_gemm_t<64, 64, 2, 2, CMC_BRIDGE_BK, RS>(epi, g, stream);
+    return launch_gemm_t<64, 64, 2, 2, 64, RS>(epi, g, stream);
 }
 
 }  // namespace
