@@ -33,7 +33,6 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-
 struct GemmParams {
     const uint16_t *A;  // [M][K]
     const uint16_t *B;  // [N][K]
@@ -56,8 +55,10 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return x * (x >= 0.f ? 1.f - half_erfc : half_erfc);
 }
 
+// fp32 -> bf16, round to nearest even; NaN stays NaN (quiet).
 __device__ __forceinline__ uint16_t to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
@@ -93,7 +94,7 @@ __device__ __forceinline__ void gemm_tile(int tiles_m, int tiles_n, int &tm, int
 // of one row's column tiles are issued back to back, so its cache lines are
 // complete when they leave L2 (column tiles outermost wrote 1.4 - 2.4x the
 // output bytes to HBM).
-//   Epilogue 0 (first layer): + b1, exact GELU, rounded to bf16.
+//   Epilogue 0 (first layer): + b1, GELU (erf form), rounded to bf16.
 //   Epilogue 1 (second layer): + b2, fp32.
 template <int EPI, int TM, int TN>
 __device__ __forceinline__ void store_tile(const GemmParams &p, const floatx4 (&acc)[TM][TN], int r0, int c0,
@@ -113,9 +114,9 @@ __device__ __forceinline__ void store_tile(const GemmParams &p, const floatx4 (&
                 const float v0 = acc[i][j][0] + bias.x, v1 = acc[i][j][1] + bias.y;
                 const float v2 = acc[i][j][2] + bias.z, v3 = acc[i][j][3] + bias.w;
                 if constexpr (EPI == 0) {
-                    const uint2 w = make_uint2((uint32_t)to_bf16_rne(gelu_erf(v0)) | ((uint32_t)to_bf16_rne(gelu_erf(v1)) << 16),
-                                               (uint32_t)to_bf16_rne(gelu_erf(v2)) | ((uint32_t)to_bf16_rne(gelu_erf(v3)) << 16));
-                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(p.C) + (size_t)row * p.N + col) = w;
+                    auto h = [](float v) { return (uint32_t)to_bf16_rne(gelu_erf(v)); };
+                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(p.C) + (size_t)row * p.N + col) =
+                        make_uint2(h(v0) | (h(v1) << 16), h(v2) | (h(v3) << 16));
                 } else {
                     *reinterpret_cast<float4 *>(static_cast<float *>(p.C) + (size_t)row * p.N + col) =
                         make_float4(v0, v1, v2, v3);
@@ -125,24 +126,26 @@ __device__ __forceinline__ void store_tile(const GemmParams &p, const floatx4 (&
     }
 }
 
-// Build-time tuning knob: K slice of the 64 x 64-per-wave kernel (32, 64 or
+// Build-time tuning knob: K slice of the 128 x 128-tile kernel (32, 64 or
 // 128; shapes whose K it does not divide use 64).  On the 49152 x 1280 ->
-// 4096 -> 4096 projection: 32 -> 3.31 ms per call (148 VGPRs, 40 KB of LDS:
-// three workgroups per CU), 64 -> 3.48 ms, 128 -> 4.84 ms.
+// 4096 -> 4096 projection run on that kernel alone: 32 -> 3.31 ms per call
+// (148 VGPRs, 40 KB of LDS: three workgroups per CU), 64 -> 3.48 ms, 128 ->
+// 4.84 ms.
 #ifndef CMC_BRIDGE_BK
 #define CMC_BRIDGE_BK 32
 #endif
 
-// Build-time tuning knob: register stages of the global -> LDS staging (1, 2
-// or 3; see gemm_nt_kernel).  With 32-wide K slices three stages need 172
-// VGPRs (two waves per SIMD instead of three) and ran slower (3.50 ms per
-// projection call against 3.25 ms with two).
+// Build-time tuning knob: register stages of the 128 x 128-tile kernel's
+// global -> LDS staging (1, 2 or 3; see gemm_nt_kernel).  With 32-wide K
+// slices three stages need 172 VGPRs (two waves per SIMD instead of three)
+// and ran slower (3.50 ms per projection call against 3.25 ms with two).
 #ifndef CMC_BRIDGE_REG_STAGES
 #define CMC_BRIDGE_REG_STAGES 2
 #endif
 
-// WT x WT per wave (4 x 4 or 8 x 8 MFMA tiles of 16 x 16), BK of K per LDS
-// slice; the workgroup tile is 2 WT x 2 WT.  RS register stages: with one,
+// WTM x WTN per wave (TM x TN MFMA tiles of 16 x 16), WGM x WGN waves, BK of
+// K per LDS slice; the workgroup tile is WGM WTM x WGN WTN.  RS register
+// stages: with one,
 // slice j + 1 is loaded while slice j feeds the MFMAs and the barrier after
 // storing it drains every load; with two, slice j + 2 is loaded while slices
 // j and j + 1 are computed (two register sets used in turn, the loop unrolled
@@ -166,7 +169,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams p) {
     gemm_tile((p.M + BM - 1) / BM, p.N / BN, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // Global -> register -> LDS staging: chunk c = tid + 256 i is row
+    // Global -> register -> LDS staging: chunk c = tid + NT i is row
     // c / kRowChunks, 16-byte column group c % kRowChunks of the BM x BK slice.
     const int crow0 = tid / kRowChunks, ccol = (tid % kRowChunks) * 8;
     const uint16_t *Ag = p.A + (size_t)ccol, *Bg = p.B + (size_t)n0 * p.K + (size_t)ccol;
