@@ -184,12 +184,12 @@ __device__ __forceinline__ void wave_lds_sync() { asm volatile("" ::: "memory");
 // softmax weight below 2^-126 contributes nothing at fp32 precision anyway).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// 16-byte load; NT marks it non-temporal (streamed K/V rows that are not
-// re-read within the launch).  The double-buffered MFMA path (Dh <= 128)
-// loads its K/V rows that way: on a 64-sequence Mistral-shaped batch a
-// launch took 66.1 us against 74.1 us with ordinary loads, on the 32-layer
-// stack 36.5 against 38.4 us; the single-buffered Dh = 256 path was 2.7%
-// slower with them and keeps ordinary loads.
+// 16-byte load; NT marks it non-temporal.  The MFMA path loads its V rows
+// that way and its K rows with ordinary loads.  Launch times, with the
+// Mistral-shaped batch rotated over 8 copies so that nothing is reused from
+// the last-level cache (ordinary / V non-temporal / K and V / K only):
+// 74.7 / 66.1 / 66.7 / 70.1 us; the 32-layer stack 38.4 / 36.3 / 36.3 /
+// 36.7 us; the Dh = 256 layer 136.5 / 128.4 / 139.6 / 127.8 us.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 template <bool NT = false>
 __device__ __forceinline__ uint4 ld16(const void *p) {
@@ -418,12 +418,12 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
     do {                                                                                             \
         {                                                                                            \
             const uint32_t o = (uint32_t)rows.slot(min((B0_) + r16, r1 - 1), K_) * RB + koff;       \
-            _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = ld16<kDoubleBuffer>(kbase + o + 64 * i);        \
+            _Pragma("unroll") for (int i = 0; i < SL; ++i) KR_[i] = ld16(kbase + o + 64 * i);        \
         }                                                                                            \
         _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
             const uint32_t o = (uint32_t)rows.slot(min((B0_) + 4 * qq + kq, r1 - 1), V_[qq]) * RB + voff; \
             if constexpr (VB >= 16) {                                                                \
-                _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = ld16<kDoubleBuffer>(vbase + o + 16 * j);  \
+                _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = ld16<true>(vbase + o + 16 * j);  \
             } else {                                                                                 \
                 const uint2 t = *reinterpret_cast<const uint2 *>(vbase + o);                         \
                 VR_[qq][0] = make_uint4(t.x, t.y, 0, 0);                                             \
