@@ -420,7 +420,7 @@ def run_stack(args, w, dev):
     torch.cuda.reset_peak_memory_stats()
     res = {"ms": ms, "steps": steps, "P": P, "t_launch": t_launch, "baseline": None,
            "footprint_GB": {"two_tier_peak_allocated": round(peak_two_tier, 2)}}
-    if args.baseline_steps <= 0:
+    if args.baseline_steps <= 0 or w.full_ctx <= 0:
         return res
 
     # Uncompressed baseline: the same decode kernel over every cached token.

@@ -150,6 +150,12 @@ WORKLOADS: Dict[str, Workload] = {
                               D=4096, k=512, W=1024, steps=3000, kv_dtype="bf16",
                               kv_std=1.0 / math.sqrt(128.0), seed=505, layers=32,
                               full_ctx=32768),
+    # The Mistral-shaped batch over 8 copies of its layer (3.2 GB of K/V):
+    # consecutive launches reuse nothing from the 256 MB last-level cache.
+    "mistral7b_batch64_x8": Workload("mistral7b_batch64_x8", B=64, Hq=32, Hkv=8, Dh=128,
+                                     N=4096, D=4096, k=512, W=1024, steps=3000,
+                                     kv_dtype="bf16", kv_std=1.0 / math.sqrt(128.0),
+                                     seed=303, layers=8),
 }
 
 
