@@ -24,7 +24,8 @@
 //     level of fp32 accumulation.  P V runs on the VALU in fp32 in four
 //     quarters of 4 keys: lane l owns key (l & 3) of each quarter and Dh/16
 //     dims; the p values reach that layout through 16 x G floats of LDS
-//     private to the wave.
+//     private to the wave.  V rows are loaded non-temporally, K rows with
+//     ordinary loads (see ld16).
 //   VALU (fp32 K/V, or G = 8): 16-byte lane loads, LPR lanes per row, dot
 //     products reduced by a DPP butterfly.
 // Both keep an online softmax per wave (running max in log2 units, q
