@@ -23,6 +23,8 @@
 // bridge_norm_kernel: one wave per output row, in place, the row held in
 // registers: mean and biased variance (two passes over the registers),
 // LayerNorm with gamma/beta, nu tanh, the row norm, and the cap.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 

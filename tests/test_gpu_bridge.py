@@ -107,6 +107,15 @@ def test_bridge_shapes(orc, M, Hc, F, Hd):
     _run(orc, h, _params(rng, Hc, F, Hd), nu=0.8, what="shapes")
 
 
+def test_bridge_more_tiles_than_cus(orc):
+    """More 256 x 256 tiles than CUs (33 x 8 = 264 for the first layer), so
+    workgroups of a persistent grid take several tiles; every row checked."""
+    rng = np.random.default_rng(8)
+    M, Hc, F, Hd = 8192 + 77, 64, 2048, 512
+    h = wl.f32_to_bf16_bits(rng.standard_normal((M, Hc)).astype(np.float32))
+    _run(orc, h, _params(rng, Hc, F, Hd), nu=0.8, what="many tiles")
+
+
 @pytest.mark.parametrize("gamma_scale,nu", [(0.02, 1.0), (0.2, 0.5), (3.0, 2.0)])
 def test_bridge_cap_regimes(orc, gamma_scale, nu):
     """Small LayerNorm outputs (cap inactive), rows near the cap, saturated
