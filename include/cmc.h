@@ -175,7 +175,7 @@ size_t cmc_bridge_workspace_bytes(int M, int F);
 /*
  * MemoryBridge projection (Sec. 2.2): each CME vector h (encoder width Hc)
  * becomes a decoder-ready memory row of width Hd,
- *   hidden = GELU(h W1^T + b1)                      (exact erf GELU)
+ *   hidden = GELU(h W1^T + b1)                      (erf form, not the tanh one)
  *   m_hat  = LayerNorm(hidden W2^T + b2)            (gamma, beta, biased variance,
  *                                                    eps inside the square root:
  *                                                    the appendix's nn.LayerNorm)
@@ -196,8 +196,9 @@ size_t cmc_bridge_workspace_bytes(int M, int F);
  *
  * Limits: M >= 0; Hc % 64 == 0, F % 128 == 0, Hd % 128 == 0 (the GEMM tile);
  * nu > 0 and eps >= 0 finite.  Arithmetic: bf16 operands, fp32 accumulation
- * (MFMA), the second layer reads the bf16 hidden activations; LayerNorm,
- * tanh and the cap in fp32.
+ * (MFMA); erf evaluated to within 1.5e-7 absolute (Abramowitz & Stegun
+ * 7.1.26), below the bf16 rounding of the hidden activations, which the
+ * second layer reads; LayerNorm, tanh and the cap in fp32.
  */
 cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1,
                              const void *w2, const float *b2,
