@@ -57,11 +57,11 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return x * (x >= 0.f ? 1.f - half_erfc : half_erfc);
 }
 
-// fp32 -> bf16, round to nearest even; NaN stays NaN (quiet).
-__device__ __forceinline__ uint16_t to_bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+// Two fp32 values -> packed bf16 (low half first), round to nearest even
+// (one v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
 
 // Build-time tuning knob: tile rows per group of the tile order below.
@@ -116,9 +116,8 @@ __device__ __forceinline__ void store_tile(const GemmParams &p, const floatx4 (&
                 const float v0 = acc[i][j][0] + bias.x, v1 = acc[i][j][1] + bias.y;
                 const float v2 = acc[i][j][2] + bias.z, v3 = acc[i][j][3] + bias.w;
                 if constexpr (EPI == 0) {
-                    auto h = [](float v) { return (uint32_t)to_bf16_rne(gelu_erf(v)); };
                     *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(p.C) + (size_t)row * p.N + col) =
-                        make_uint2(h(v0) | (h(v1) << 16), h(v2) | (h(v3) << 16));
+                        make_uint2(pack_bf16x2(gelu_erf(v0), gelu_erf(v1)), pack_bf16x2(gelu_erf(v2), gelu_erf(v3)));
                 } else {
                     *reinterpret_cast<float4 *>(static_cast<float *>(p.C) + (size_t)row * p.N + col) =
                         make_float4(v0, v1, v2, v3);
