@@ -256,6 +256,37 @@ def test_decode_wide_workgroups(orc, B, Hkv, G, Dh, dtype, N, k, W, fill):
                  seed=B * Hkv + G + Dh, steps=3, fused=W > 0)
 
 
+def _random_decode_config(seed):
+    """A seeded random decode configuration within the ABI's limits."""
+    r = np.random.default_rng(seed)
+    Dh = int(r.choice([64, 128, 256]))
+    G = int(r.choice([1, 2, 4, 8]))
+    Hkv = int(r.choice([1, 2, 3, 4]))
+    B = int(r.integers(1, 7))
+    N = int(r.integers(1, 700))
+    k = int(r.integers(0, N + 1))
+    W = int(r.choice([0, int(r.integers(1, 9)), int(r.integers(9, 400))]))
+    if k + W == 0:
+        k = 1
+    fill = int(r.integers(0, W + 1)) if W else 0
+    return dict(B=B, Hq=G * Hkv, Hkv=Hkv, Dh=Dh, N=N, k=k, W=W, fill=fill,
+                dtype=str(r.choice(["f32", "bf16"])), fused=bool(W and r.integers(0, 2)),
+                t_new=int(r.integers(1, max(2, min(W, 6)))) if W else 1, idx_none=bool(r.integers(0, 4) == 0))
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_decode_random_configs(orc, seed):
+    """Seeded random shapes (head size, group size, batch, pool, k, ring size and
+    fill, dtype, fused append with several rows, identity index) against the
+    oracle, two steps each."""
+    c = _random_decode_config(1000 + seed)
+    if c["idx_none"]:
+        c["N"] = max(c["N"], c["k"])
+    t_new = c["t_new"] if c["fused"] else 1
+    _decode_case(orc, c["B"], c["Hq"], c["Hkv"], c["Dh"], c["N"], c["k"], c["W"], c["fill"], c["dtype"],
+                 seed=2000 + seed, steps=2, idx_none=c["idx_none"], fused=c["fused"], t_new=t_new)
+
+
 def test_decode_empty_window_zero_output(orc):
     """k = 0 and an empty ring: zeros, like the oracle."""
     _decode_case(orc, B=1, Hq=4, Hkv=4, Dh=64, N=10, k=0, W=4, fill=0, dtype="f32", seed=1, steps=1)
