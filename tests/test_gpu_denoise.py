@@ -83,6 +83,23 @@ def test_denoise_sizes(orc, dtype, n, H, n_tokens):
     _check_denoise(orc, emb, 3, 0.05, 16, n_tokens, chunk_tokens=256, what="sizes")
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_denoise_random_configs(orc, seed):
+    """Seeded random batch, length, width, neighbourhood, threshold, floor,
+    chunk size, dtype and per-sequence lengths against the oracle."""
+    r = np.random.default_rng(3000 + seed)
+    dtype = str(r.choice(["f32", "bf16"]))
+    B, n = int(r.integers(1, 5)), int(r.integers(1, 2500))
+    H = int(r.integers(1, 100)) * (8 if dtype == "bf16" else 4)
+    g, m = int(r.integers(1, 5)), int(r.choice([0, 1, int(r.integers(2, 40))]))
+    tau = float(r.choice([0.0, 0.05, 0.3, 0.8]))
+    n_tokens = [int(r.integers(0, n + 1)) for _ in range(B)]
+    e = r.standard_normal((B, n, H)).astype(np.float32)
+    e[:, 1:] += float(r.uniform(0.0, 1.5)) * e[:, :-1]
+    emb = wl.f32_to_bf16_bits(e) if dtype == "bf16" else e
+    _check_denoise(orc, emb, g, tau, m, n_tokens, chunk_tokens=int(r.choice([0, 1, 7, 256])), what=f"random {seed}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("tau,m", [(-2.0, 0), (2.0, 16), (2.0, 1), (0.3, 3), (0.05, 0)])
 def test_denoise_threshold_and_floor(orc, dtype, tau, m):

@@ -70,6 +70,17 @@ def test_select_sizes(orc, B, N, D, k):
     _check_select(orc, keys, qv, k, f"sizes")
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_select_random_configs(orc, seed):
+    """Seeded random batch, pool size, key width and k (well-separated scores,
+    some with exact duplicate rows)."""
+    r = np.random.default_rng(4000 + seed)
+    B, N = int(r.integers(1, 9)), int(r.integers(1, 20000))
+    D, k = 4 * int(r.integers(1, 80)), int(r.integers(0, N + 1))
+    keys, qv = _separated(B, N, D, seed=5000 + seed, dup_every=int(r.choice([0, 0, 6])))
+    _check_select(orc, keys, qv, k, f"random {seed}")
+
+
 @pytest.mark.parametrize("N,k", [(64, 16), (1000, 100), (20000, 700)])
 def test_select_exact_ties(orc, N, k):
     keys, qv = _separated(2, N, 8, seed=7, dup_every=4)
