@@ -488,7 +488,7 @@ def main():
         pmc_summary(args)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               "(each sequence shards independently across GPUs, see the design notes).", file=sys.stderr)
         sys.exit(2)
     import torch
