@@ -64,7 +64,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5, help="timed passes (each = select + decode_steps)")
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="llama3_8b_layer")
+    from paper_2609_25537_amd import workloads as _wl
+    names = [*_wl.WORKLOADS, *_wl.DENOISE_WORKLOADS, *_wl.BRIDGE_WORKLOADS]
+    ap.add_argument("--workload", default="llama3_8b_layer", metavar="NAME",
+                    help="one of: " + ", ".join(names))
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's 3000")
     ap.add_argument("--step-pool", type=int, default=None,
                     help="distinct per-step input sets (rotated); default all steps up to 4096 rows of q")
