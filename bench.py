@@ -88,6 +88,10 @@ def parse():
                          "projection's two GEMM shapes instead of the library, for comparison")
     ap.add_argument("--launch-reps", type=int, default=500,
                     help="back-to-back decode launches timed for the roofline figure")
+    ap.add_argument("--batched", choices=["auto", "on", "off"], default="auto",
+                    help="add the batched legs (the 32-layer stack's decode launches and the Mistral-shaped batch "
+                         "over 8 layer copies, launches rotating so that nothing is served from the last-level "
+                         "cache) to the JSON line; auto: with the default workload")
     ap.add_argument("--baseline-steps", type=int, default=4,
                     help="stack workloads: timed decode steps of the uncompressed-cache baseline (0: skip it)")
     return ap.parse_args()
@@ -165,22 +169,31 @@ def run_pass(inp: Inputs, steps: int):
         inp.decode_step(t % inp.P)
 
 
-def decode_bytes(w) -> int:
-    """Algorithmic bytes of one decode-step launch with the ring full: K and
-    V of the k + W keys of each sequence (the newest row read from the
-    appended input; a ragged sequence has its own k_b + q_b pool rows, read
-    from the gathered Tier-1 block), the appended row written into the ring,
-    q and out."""
+def decode_bytes(w, counts=None) -> float:
+    """Algorithmic bytes of one decode-step launch: K and V of each
+    sequence's pool rows (k, or a ragged sequence's own k_b + q_b, read from
+    the gathered Tier-1 block) and of its ring rows -- min(count_b + 1, W)
+    with count_b the tokens in the ring before the launch (its filled slots,
+    one of which the appended row replaces once the ring is full, plus that
+    row read from the input) -- the appended row written into the ring, q
+    and out.  counts None: every ring full.  counts may be [B] or [L][B] (L
+    launches: the mean over them)."""
     from paper_2609_25537_amd import workloads as wl
     if w.ragged:
         rs = wl.ragged_sizes(w)
         pool = int(np.minimum(rs["n_rows"], w.k).sum() + rs["q_rows"].sum())
     else:
         pool = w.B * w.k
+    if counts is None:
+        ring = w.B * w.W
+    else:
+        c = np.asarray(counts, np.int64).reshape(-1, w.B)
+        ring = float(np.minimum(c + 1, w.W).sum(axis=1).mean())
     row = w.Dh * w.kv_bytes * 2
-    kv = w.Hkv * (pool + w.B * w.W) * row
+    kv = w.Hkv * (pool + ring) * row
     ring_write = w.B * w.Hkv * row
-    return kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2
+    total = kv + ring_write + w.B * w.Hq * w.Dh * 4 * 2
+    return int(total) if counts is None else float(total)
 
 
 def capture(fn):
@@ -215,11 +228,13 @@ def time_decode_launch(inp: Inputs, reps: int = 500):
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
     s.synchronize()
+    c0 = inp.wc.cpu().numpy().astype(np.int64)  # ring fills before the timed launches
     a.record(s)
     g.replay()
     b.record(s)
     b.synchronize()
-    return a.elapsed_time(b) / reps * 1e-3  # seconds
+    counts = c0[None, :] + np.arange(reps, dtype=np.int64)[:, None]
+    return a.elapsed_time(b) / reps * 1e-3, counts  # seconds, [reps][B] counts before each launch
 
 
 def cpu_baseline(w, budget_s: float):
@@ -308,10 +323,17 @@ def pmc_summary(args):
     write, nw = _counter_values(wd, "WRITE_SIZE", "decode_kernel")
     fs, ws = known_kib / copy_fetch, known_kib / copy_write
     fetch_b, write_b = fetch * fs * 1024, write * ws * 1024
+    # The counted run starts from the workload's initial ring fills and
+    # appends one row per dispatch: the median dispatch (the median counter
+    # value, the fetch growing with the fill) saw fill + n // 2 tokens.
+    alg = decode_bytes(w)
+    if w.layers == 1:
+        _, _, cnt0 = wl.window_kv(w)
+        alg = round(decode_bytes(w, cnt0.astype(np.int64) + nf // 2))
     rec = {"kernel_hash": decode_kernel_hash(), "bytes_per_launch": round(fetch_b + write_b),
            "fetch_bytes": round(fetch_b), "write_bytes": round(write_b),
            "fetch_kib_raw": fetch, "write_kib_raw": write, "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
-           "dispatches": [nf, nw], "algorithmic_bytes": decode_bytes(w)}
+           "dispatches": [nf, nw], "algorithmic_bytes": alg, "algorithmic_bytes_rings_full": decode_bytes(w)}
     data = {}
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
@@ -341,6 +363,65 @@ class StackLayer:
         self.nv = [dn("new_v", (layer, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]
         self.gk = torch.empty((w.B, w.Hkv, w.k, w.Dh), dtype=bf, device=dev)  # gathered Tier-1 rows
         self.gv = torch.empty_like(self.gk)
+
+
+def batched_leg(name: str, dev, reps: int = 512, P: int = 4):
+    """Launch-level HBM figure of a batched workload, for the same JSON line
+    as the headline: its decode launches (cmc_decode_step, rings full)
+    rotating over the workload's layers (the 32-layer stack; the Mistral-
+    shaped batch over 8 layer copies), replayed from a graph and timed with
+    HIP events on the replay stream.  The Tier-1 blocks are drawn directly
+    as the gathered rows the decode reads (the selection does not change
+    the launch).  Throughput is attention-only tokens/s for all layers."""
+    import torch
+    from paper_2609_25537_amd import cmc
+    from paper_2609_25537_amd import workloads as wl
+    w = wl.get(name)
+    bf = torch.bfloat16 if w.kv_dtype == "bf16" else torch.float32
+    dn = lambda role, ids, shape, dt=bf: wl.device_normal(w.seed, role, ids, shape, w.kv_std, dev, dt)
+    layers = []
+    for l in range(w.layers):
+        layers.append(dict(gk=dn("cme_k", (l, 1), (w.B, w.Hkv, w.k, w.Dh)),
+                           gv=dn("cme_v", (l, 1), (w.B, w.Hkv, w.k, w.Dh)),
+                           wk=dn("win_k", (l,), (w.B, w.Hkv, w.W, w.Dh)),
+                           wv=dn("win_v", (l,), (w.B, w.Hkv, w.W, w.Dh)),
+                           wc=torch.full((w.B,), w.W, dtype=torch.int32, device=dev),
+                           q=[dn("q", (l, t), (w.B, w.Hq, w.Dh), torch.float32) for t in range(P)],
+                           nk=[dn("new_k", (l, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)],
+                           nv=[dn("new_v", (l, t), (w.B, w.Hkv, 1, w.Dh)) for t in range(P)]))
+    out = torch.empty((w.B, w.Hq, w.Dh), dtype=torch.float32, device=dev)
+    ws = cmc.decode_workspace(w.B, w.Hq, w.Hkv, w.Dh, w.k, w.W, dev)
+    L = len(layers)
+
+    def launches():
+        for r in range(reps):
+            Ly, j = layers[r % L], (r // L) % P
+            cmc.cmc_decode_step(Ly["q"][j], Ly["gk"], Ly["gv"], None, w.k, Ly["wk"], Ly["wv"], Ly["wc"],
+                                Ly["nk"][j], Ly["nv"][j], w.scale, out=out, workspace=ws)
+
+    g = capture(launches)
+    st = torch.cuda.current_stream()
+    g.replay()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.synchronize()
+    a.record(st)
+    g.replay()
+    b.record(st)
+    b.synchronize()
+    t = a.elapsed_time(b) / reps * 1e-3
+    nbytes = decode_bytes(w)
+    achieved = nbytes / t / 1e9
+    del g, layers, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Dh": w.Dh, "k": w.k, "W": w.W,
+            "layers_rotated": L, "launches_timed": reps,
+            "kernel": "decode_kernel (cmc_decode_step), rings full",
+            "launch_us": round(t * 1e6, 3), "bytes_per_launch": nbytes,
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(w),
+                         "cache_resident": False},
+            "tokens_per_s_all_layers": round(w.B / (L * t), 1)}
 
 
 def run_stack(args, w, dev):
@@ -556,20 +637,29 @@ def main():
     tokens = w.B * steps * args.steps
     value = tokens / (ms * 1e-3)
 
-    t_launch = time_decode_launch(inp, args.launch_reps)
-    nbytes = decode_bytes(w)
+    P_inputs = inp.P
+    t_launch, counts = time_decode_launch(inp, args.launch_reps)
+    nbytes = decode_bytes(w, counts)
     achieved = nbytes / t_launch / 1e9
     sel_ms = time_select(inp)
     stream = stream_read_probe(dev)
     traffic = recorded_traffic(w)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "decode_kernel (cmc_decode_step)", "bytes_per_launch": nbytes,
+                "kernel": "decode_kernel (cmc_decode_step)", "bytes_per_launch": round(nbytes),
+                "rings_full": bool((counts >= w.W).all()),
                 "launch_us": round(t_launch * 1e6, 3),
                 "stream_read_GBs": stream, "frac_of_stream_read": round(achieved / stream, 4),
                 # bytes touched between reuses below the 256 MB last-level cache: the figure is
                 # cache-resident latency, not an HBM bandwidth claim
                 "cache_resident": nbytes * w.layers < LLC_BYTES}
+
+    batched = None
+    if args.batched == "on" or (args.batched == "auto" and w.name == "llama3_8b_layer"):
+        del inp, graph
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        batched = [batched_leg("llama_stack32", dev), batched_leg("mistral7b_batch64_x8", dev)]
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -590,7 +680,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Dh": w.Dh, "N": w.N,
                    "D": w.D, "k": w.k, "W": w.W, "decode_steps": steps, "layers": w.layers,
-                   "kv_dtype": w.kv_dtype, "step_input_sets": inp.P, "graph": bool(graph),
+                   "kv_dtype": w.kv_dtype, "step_input_sets": P_inputs, "graph": not args.eager,
                    **({"ragged": {"ctx_tokens": [w.ctx_min, w.ctx_max], "ratio": w.ratio,
                                   "question_rows": [w.q_min, w.q_max]}} if w.ragged else {})},
         "roofline": roofline,
@@ -598,6 +688,10 @@ def main():
         "select_ms": round(sel_ms, 4),
         "attention_only": True,
     }
+    if batched is not None:
+        # the >= 70% HBM figures at the Llama/Mistral head geometry (Hq 32, Hkv 8, Dh 128): batched
+        # launches whose bytes between reuses exceed the last-level cache
+        line["batched"] = batched
     txt = json.dumps(line)
     print(txt, flush=True)
     if args.out:

@@ -21,7 +21,8 @@
  *   cmc_denoise          graph-based context denoising before compression
  *                        (Sec. 2.1, once per context)
  *   cmc_memory_bridge    MemoryBridge projection of CME vectors into selection
- *                        keys (Sec. 2.2, once per context)
+ *                        keys (Sec. 2.3, once per context), and the CME norms
+ *                        that localization ranks
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
@@ -68,15 +69,20 @@ typedef enum cmc_dtype {
 /* ------------------------------------------------------------------------ */
 
 /* Bytes of workspace cmc_select_cmes needs for these sizes (0 is a valid
- * answer only when B*N == 0).  Returns 0 for invalid sizes. */
+ * answer only when B*N == 0): the B*N fp32 scores when scores_out is NULL.
+ * The top-k state lives in registers, so k does not enter.  Returns 0 for
+ * invalid sizes. */
 size_t cmc_select_workspace_bytes(int B, int N);
 
 /*
  * Question-guided top-K selection (Sec. 2.5, Tier-1 paragraph and its score
  * equation; Eq. 2 of the problem statement, M* = TopK(M, q, K)).
  *
- *   sel_keys   [B][N][D] fp32  decoder-ready memory rows m_j of each sequence,
- *                              row j = document position j (Sec. 2.3, eq. M)
+ *   sel_keys   [B][N][D]       decoder-ready memory rows m_j of each sequence,
+ *                              row j = document position j (Sec. 2.3, eq. M),
+ *                              fp32 or bf16 bit patterns as key_dtype says
+ *                              (bf16 halves the bytes read; each element is
+ *                              widened exactly to fp32)
  *   q_vec      [B][D]    fp32  mean-pooled question embedding q_vec
  *   idx_out    [B][k]    int32 the k rows with the largest
  *                              score_j = m_j.q / (max(|m_j|,1e-8) max(|q|,1e-8)),
@@ -85,10 +91,11 @@ size_t cmc_select_workspace_bytes(int B, int N);
  *   scores_out [B][N]    fp32  the cosine scores, or NULL
  *   workspace  >= cmc_select_workspace_bytes(B, N) bytes, any content
  *
- * Limits: B >= 0, 0 <= k <= N <= 32768, D >= 4 and D % 4 == 0.
+ * Limits: B >= 0, 0 <= k <= N <= 32768, D >= 4 and D % 4 == 0 (fp32 keys)
+ * or D % 8 == 0 (bf16 keys), else CMC_ERR_UNSUPPORTED.
  * Arithmetic: fp32 with a fixed reduction order (run-to-run bit-identical).
  */
-cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec,
+cmc_status cmc_select_cmes(const void *sel_keys, cmc_dtype key_dtype, const float *q_vec,
                            int B, int N, int D, int k,
                            int32_t *idx_out, float *scores_out,
                            void *workspace, size_t workspace_bytes, void *stream);
@@ -117,16 +124,19 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec,
  *   k_out      [B] int32           k_b + q_b (the k_len of the ragged decode
  *                                  calls), or NULL
  *   norms_out  [B][N] fp32         |m_j| of every candidate row (0 past n_b),
- *                                  from the same pass over the keys, for
- *                                  cmc_locate_window; or NULL
- *   sel_keys, q_vec, scores_out, workspace: as cmc_select_cmes (N is the row
- *   stride of sel_keys, scores_out and norms_out)
+ *                                  from the same pass over the keys; or NULL.
+ *                                  (These are the capped memory rows: not the
+ *                                  norms CME-guided localization ranks, see
+ *                                  cmc_locate_window.)
+ *   sel_keys, key_dtype, q_vec, scores_out, workspace: as cmc_select_cmes (N
+ *   is the row stride of sel_keys, scores_out and norms_out)
  *
- * Limits: B >= 0, N >= 0, k >= 0, idx_stride >= k, D >= 4 and D % 4 == 0,
- * N <= 32768.  k may exceed N (then k_b = n_b).  With n_b = N and no question
- * rows the result equals cmc_select_cmes.
+ * Limits: B >= 0, N >= 0, k >= 0, idx_stride >= k, D >= 4 and D % 4 == 0
+ * (fp32 keys) or D % 8 == 0 (bf16 keys), N <= 32768.  k may exceed N (then
+ * k_b = n_b).  With n_b = N and no question rows the result equals
+ * cmc_select_cmes.
  */
-cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec,
+cmc_status cmc_select_cmes_ragged(const void *sel_keys, cmc_dtype key_dtype, const float *q_vec,
                                   const int32_t *n_rows, const int32_t *q_rows,
                                   int B, int N, int D, int k, int idx_stride,
                                   int32_t *idx_out, int32_t *k_out, float *scores_out,
@@ -135,15 +145,22 @@ cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec,
 
 /*
  * CME-guided Tier-2 localization (appendix on Tier-2 window localization:
- * when the answer offset alpha is not known, take the offset of the chunk
- * whose CME has the largest norm; the window start then follows the Tier-2
- * window equation of Sec. 2.5).  Each chunk (segment) contributes
- * mems_per_chunk consecutive rows of M (Sec. 2.3), so row j belongs to
- * chunk j / mems_per_chunk.  Offsets are in tokens of the context C.
+ * when the answer offset alpha is not known, alpha is taken as the offset of
+ * the chunk whose CME has the largest norm; the window start then follows
+ * the Tier-2 window equation of Sec. 2.5).  The CMEs are the encoder's hidden
+ * states at the placeholder positions (Sec. 2.2); each chunk (segment)
+ * contributes mems_per_chunk consecutive rows (Sec. 2.2, the concatenation
+ * H^(c)), so row j belongs to chunk j / mems_per_chunk.  Offsets are in
+ * tokens of the context C.
  *
- *   norms        [B][N] fp32   row norms, e.g. norms_out of
- *                              cmc_select_cmes_ragged; the decision is made
- *                              on these values
+ *   norms        [B][N] fp32   norms of the CME vectors h, e.g. h_norms_out
+ *                              of cmc_memory_bridge (B contexts of N rows
+ *                              each); the decision is made on these values.
+ *                              The capped memory rows m (the bridge output)
+ *                              do not rank: Sec. 2.3's cap sets the norm of
+ *                              every row whose nu tanh(m_hat) exceeds 2 nu to
+ *                              exactly 2 nu, which at decoder widths is every
+ *                              row.
  *   n_rows       [B] int32     rows of sequence b (clamped into [0, N]), or
  *                              NULL for all N
  *   ctx_len      [B] int32     |C| of sequence b, in tokens
@@ -173,7 +190,7 @@ cmc_status cmc_locate_window(const float *norms, const int32_t *n_rows, const in
 size_t cmc_bridge_workspace_bytes(int M, int F);
 
 /*
- * MemoryBridge projection (Sec. 2.2): each CME vector h (encoder width Hc)
+ * MemoryBridge projection (Sec. 2.3): each CME vector h (encoder width Hc)
  * becomes a decoder-ready memory row of width Hd,
  *   hidden = GELU(h W1^T + b1)                      (erf form, not the tanh one)
  *   m_hat  = LayerNorm(hidden W2^T + b2)            (gamma, beta, biased variance,
@@ -190,6 +207,9 @@ size_t cmc_bridge_workspace_bytes(int M, int F);
  *   w2       [Hd][F] bf16     second layer; b2 [Hd] fp32
  *   ln_gamma, ln_beta [Hd] fp32
  *   out      [M][Hd] fp32
+ *   h_norms_out [M] fp32      |h_j|_2 of every input row (bf16 widened exactly,
+ *            squares summed in fp32 in a fixed order), the norms that
+ *            cmc_locate_window ranks; or NULL
  *   workspace >= cmc_bridge_workspace_bytes(M, F) bytes, any content; after
  *            the call it holds the hidden activations, [M][F] bf16 (rounded
  *            to nearest even from fp32)
@@ -204,7 +224,8 @@ cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1,
                              const void *w2, const float *b2,
                              const float *ln_gamma, const float *ln_beta,
                              float nu, float ln_eps, int M, int Hc, int F, int Hd,
-                             float *out, void *workspace, size_t workspace_bytes, void *stream);
+                             float *out, float *h_norms_out,
+                             void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Context denoising.                                                       */

@@ -12,11 +12,12 @@ keeps the cache bounded by K + W + |q|) and ``two_tier_decode`` (softmax
 attention over the assembled cache), plus ``select_ragged`` and
 ``two_tier_decode_ragged`` (the same definitions per sequence, for batches
 whose sequences differ in size), and ``row_norms`` / ``locate`` (CME-guided
-Tier-2 localization, from the appendix on window localization), and
+Tier-2 localization, from the appendix on window localization, ranking the
+norms of the encoder's CME vectors h of Sec. 2.2), and
 ``denoise_scores`` / ``denoise_select`` (graph-based context denoising,
 Sec. 2.1 Eq. 3 with the minimum keep interval), and ``bridge_hidden`` /
 ``bridge_out`` (the MemoryBridge projection and its norm-calibrated tanh
-cap, Sec. 2.2).
+cap, Sec. 2.3).
 
 ``Oracle(path)`` binds any build of the same source (the tests use it to
 load deliberately mutated builds and show that the pins reject them); the
@@ -62,6 +63,14 @@ def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
+def _keys(a: np.ndarray):
+    """(contiguous array, 1 if it holds bf16 bit patterns else 0); uint16
+    arrays are bf16, anything else is taken as fp32."""
+    if a.dtype == np.uint16:
+        return np.ascontiguousarray(a), 1
+    return np.ascontiguousarray(a, np.float32), 0
+
+
 def _check(rc: int, what: str):
     if rc != 0:
         raise OracleError(f"{what}: oracle returned {rc}")
@@ -73,14 +82,14 @@ class Oracle:
     def __init__(self, path: str):
         lib = ctypes.CDLL(path)
         P, I = ctypes.c_void_p, ctypes.c_int
-        lib.oracle_select.argtypes = [P, P, I, I, I, I, P, P, P]
+        lib.oracle_select.argtypes = [P, I, P, I, I, I, I, P, P, P]
         lib.oracle_select.restype = I
         lib.oracle_window_append.argtypes = [P, P, I, P, P, P, I, I, I, I, I]
         lib.oracle_window_append.restype = I
         lib.oracle_two_tier_decode.argtypes = [P, P, P, I, P, I, P, P, P, I,
                                                I, I, I, I, I, ctypes.c_double, P]
         lib.oracle_two_tier_decode.restype = I
-        lib.oracle_row_norms.argtypes = [P, I, I, I, P]
+        lib.oracle_row_norms.argtypes = [P, I, ctypes.c_longlong, I, P]
         lib.oracle_row_norms.restype = I
         lib.oracle_locate.argtypes = [P, P, I, I, I, P, I, I, P, I, P, P]
         lib.oracle_locate.restype = I
@@ -109,20 +118,21 @@ class Oracle:
 
     def select(self, sel_keys: np.ndarray, q_vec: np.ndarray, k: int
                ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
-        """Tier-1 selection.  sel_keys [B][N][D] fp32, q_vec [B][D] fp32.
+        """Tier-1 selection.  sel_keys [B][N][D] fp32 (or uint16: bf16 bit
+        patterns), q_vec [B][D] fp32.
 
         Returns (idx [B][k] int32 ascending, scores [B][N] fp64, gap [B]
         fp64), gap being the relative gap between the k-th and (k+1)-th
         largest scores (+inf when k is 0 or N).
         """
-        keys = np.ascontiguousarray(sel_keys, np.float32)
+        keys, bf = _keys(sel_keys)
         q = np.ascontiguousarray(q_vec, np.float32)
         B, N, D = keys.shape
         assert q.shape == (B, D)
         idx = np.zeros((B, k), np.int32)
         scores = np.zeros((B, N), np.float64)
         gap = np.zeros((B,), np.float64)
-        rc = self.lib.oracle_select(_ptr(keys), _ptr(q), B, N, D, int(k),
+        rc = self.lib.oracle_select(_ptr(keys), bf, _ptr(q), B, N, D, int(k),
                                     _ptr(idx), _ptr(scores), _ptr(gap))
         _check(rc, "select")
         return idx, scores, gap
@@ -199,12 +209,15 @@ class Oracle:
         """The whole MemoryBridge in fp64 (hidden layer not rounded)."""
         return self.bridge_out(self.bridge_hidden(h, w1, b1), w2, b2, gamma, beta, nu, eps)
 
-    def row_norms(self, sel_keys: np.ndarray) -> np.ndarray:
-        """||m_j|| of every row, fp64 [B][N]."""
-        keys = np.ascontiguousarray(sel_keys, np.float32)
-        B, N, D = keys.shape
-        out = np.zeros((B, N), np.float64)
-        _check(self.lib.oracle_row_norms(_ptr(keys), B, N, D, _ptr(out)), "row_norms")
+    def row_norms(self, rows: np.ndarray) -> np.ndarray:
+        """||x|| over the last axis of rows [..., D] (fp32, or uint16: bf16
+        bit patterns), fp64 with the leading shape (e.g. the CME vectors h
+        [M][Hc] -> [M], memory rows [B][N][D] -> [B][N])."""
+        x, bf = _keys(rows)
+        D = x.shape[-1]
+        R = int(np.prod(x.shape[:-1]))
+        out = np.zeros(x.shape[:-1], np.float64)
+        _check(self.lib.oracle_row_norms(_ptr(x), bf, R, D, _ptr(out)), "row_norms")
         return out
 
     def locate(self, norms: np.ndarray, ctx_len: np.ndarray, W: int, mems_per_chunk: int,

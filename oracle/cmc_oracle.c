@@ -114,14 +114,15 @@ static int by_value(const void *a, const void *b)
 }
 
 /*
- * sel_keys [B][N][D] fp32, q_vec [B][D] fp32.
+ * sel_keys [B][N][D] fp32, or bf16 bit patterns when keys_bf16 is set;
+ * q_vec [B][D] fp32.
  * idx_out  [B][k] int32: the K best-scoring rows, written in ascending order
  *          ("re-ordered by original document position").
  * scores_out [B][N] double cosine scores, or NULL.
  * gap_out  [B] double, or NULL: (s_(k) - s_(k+1)) / |s_(k)| for the k-th and
  *          (k+1)-th largest scores; +inf when k == 0 or k == N.
  */
-int oracle_select(const float *sel_keys, const float *q_vec, int B, int N, int D, int k,
+int oracle_select(const void *sel_keys, int keys_bf16, const float *q_vec, int B, int N, int D, int k,
                   int32_t *idx_out, double *scores_out, double *gap_out)
 {
     if (B < 0 || N < 0 || D <= 0 || k < 0 || k > N || (B > 0 && (!sel_keys || !q_vec)))
@@ -141,11 +142,12 @@ int oracle_select(const float *sel_keys, const float *q_vec, int B, int N, int D
         double qn = sqrt(qq);
         ranked *r = all + (size_t)b * N;
         for (int j = 0; j < N; ++j) {
-            const float *m = sel_keys + ((size_t)b * N + j) * D;
+            const size_t row = ((size_t)b * N + j) * D;
             double dot = 0.0, mm = 0.0;
             for (int d = 0; d < D; ++d) {
-                dot += (double)m[d] * (double)q[d];
-                mm += (double)m[d] * (double)m[d];
+                const double m = load_elem(sel_keys, keys_bf16, row + d);
+                dot += m * (double)q[d];
+                mm += m * m;
             }
             double mn = sqrt(mm);
             double s = dot / (fmax(mn, 1e-8) * fmax(qn, 1e-8));
@@ -228,7 +230,7 @@ int oracle_window_append(void *win_k, void *win_v, int elem_bytes, int32_t *win_
 }
 
 /* ------------------------------------------------------------------ */
-/* MemoryBridge (Sec. 2.2): a two-layer MLP with GELU, LayerNorm on its */
+/* MemoryBridge (Sec. 2.3): a two-layer MLP with GELU, LayerNorm on its */
 /* output (the appendix's nn.LayerNorm formula), then the norm-         */
 /* calibrated tanh cap of the section's equation.                      */
 /* ------------------------------------------------------------------ */
@@ -415,22 +417,30 @@ int oracle_denoise_select(const double *max_cos, const int32_t *n_tokens, int B,
 
 /* ------------------------------------------------------------------ */
 /* CME-guided Tier-2 localization (appendix on Tier-2 window           */
-/* localization: alpha is the offset of the chunk that produced the    */
-/* highest-norm CME; the midpoint heuristic uses alpha = |C|/2).  Each */
+/* localization: alpha is the token offset of the chunk whose CME has */
+/* the largest norm; the midpoint heuristic uses alpha = |C|/2).  Each */
 /* segment contributes m^(c) consecutive rows of M (Sec. 2.3).         */
 /* ------------------------------------------------------------------ */
 
-/* norms_out[b][j] = ||m_j||_2 of sel_keys[b][j][:]. */
-int oracle_row_norms(const float *sel_keys, int B, int N, int D, double *norms_out)
+/*
+ * norms_out[r] = ||x_r||_2 of the R rows of rows[R][D] (fp32, or bf16 bit
+ * patterns when is_bf16 is set).  Localization ranks the norms of the CME
+ * vectors h, the encoder's hidden states at the placeholder positions
+ * (Sec. 2.2): the decoder-ready rows after Sec. 2.3's cap cannot serve,
+ * since the cap sets the norm of every row whose nu tanh(m_hat) exceeds
+ * 2 nu to exactly 2 nu.
+ */
+int oracle_row_norms(const void *rows, int is_bf16, long long R, int D, double *norms_out)
 {
-    if (B < 0 || N < 0 || D < 1)
+    if (R < 0 || D < 1)
         return ORACLE_BAD_ARG;
     #pragma omp parallel for schedule(static)
-    for (long long r = 0; r < (long long)B * N; ++r) {
-        const float *m = sel_keys + (size_t)r * D;
+    for (long long r = 0; r < R; ++r) {
         double s = 0.0;
-        for (int d = 0; d < D; ++d)
-            s += (double)m[d] * (double)m[d];
+        for (int d = 0; d < D; ++d) {
+            const double x = load_elem(rows, is_bf16, (size_t)r * D + d);
+            s += x * x;
+        }
         norms_out[r] = sqrt(s);
     }
     return ORACLE_OK;

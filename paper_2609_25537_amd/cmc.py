@@ -59,7 +59,7 @@ def lib() -> ctypes.CDLL:
         P, I, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
         L.cmc_select_workspace_bytes.argtypes = [I, I]
         L.cmc_select_workspace_bytes.restype = SZ
-        L.cmc_select_cmes.argtypes = [P, P, I, I, I, I, P, P, P, SZ, P]
+        L.cmc_select_cmes.argtypes = [P, I, P, I, I, I, I, P, P, P, SZ, P]
         L.cmc_select_cmes.restype = I
         L.cmc_window_append.argtypes = [P, P, I, P, P, P, I, I, I, I, I, P]
         L.cmc_window_append.restype = I
@@ -73,7 +73,7 @@ def lib() -> ctypes.CDLL:
         L.cmc_decode_step.argtypes = [P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
                                       ctypes.c_float, P, P, SZ, P]
         L.cmc_decode_step.restype = I
-        L.cmc_select_cmes_ragged.argtypes = [P, P, P, P, I, I, I, I, I, P, P, P, P, P, SZ, P]
+        L.cmc_select_cmes_ragged.argtypes = [P, I, P, P, P, I, I, I, I, I, P, P, P, P, P, SZ, P]
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_locate_window.argtypes = [P, P, P, I, I, I, P, I, I, I, P, P, P]
         L.cmc_locate_window.restype = I
@@ -85,8 +85,8 @@ def lib() -> ctypes.CDLL:
         L.cmc_denoise.restype = I
         L.cmc_bridge_workspace_bytes.argtypes = [I, I]
         L.cmc_bridge_workspace_bytes.restype = SZ
-        L.cmc_memory_bridge.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, ctypes.c_float, I, I, I, I, P, P, SZ,
-                                        P]
+        L.cmc_memory_bridge.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, ctypes.c_float, I, I, I, I, P, P, P,
+                                        SZ, P]
         L.cmc_memory_bridge.restype = I
         L.cmc_select_cmes_ragged.restype = I
         L.cmc_two_tier_decode_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, I, I, I, I, I, I,
@@ -145,7 +145,7 @@ def _kv_dtype(t) -> int:
         return CMC_BF16
     if t.dtype == torch.float32:
         return CMC_F32
-    raise TypeError(f"K/V tensors must be float32 or bfloat16, got {t.dtype}")
+    raise TypeError(f"expected a float32 or bfloat16 tensor, got {t.dtype}")
 
 
 def _need(cond: bool, msg: str) -> None:
@@ -161,13 +161,13 @@ def cmc_select_workspace_bytes(B: int, N: int) -> int:
 
 def cmc_select_cmes(sel_keys, q_vec, k: int, idx_out=None, scores_out=None, workspace=None,
                     stream=None):
-    """Tier-1 selection.  sel_keys [B][N][D] fp32, q_vec [B][D] fp32 (device).
-    Returns idx_out [B][k] int32 (ascending)."""
+    """Tier-1 selection.  sel_keys [B][N][D] fp32 or bf16, q_vec [B][D] fp32
+    (device).  Returns idx_out [B][k] int32 (ascending)."""
     import torch
     _need(sel_keys.dim() == 3 and sel_keys.is_contiguous(), "sel_keys must be contiguous [B][N][D]")
     B, N, D = sel_keys.shape
     _need(q_vec.shape == (B, D) and q_vec.is_contiguous(), "q_vec must be contiguous [B][D]")
-    _need(sel_keys.dtype == torch.float32 and q_vec.dtype == torch.float32, "fp32 inputs expected")
+    _need(q_vec.dtype == torch.float32, "q_vec must be fp32")
     if idx_out is None:
         idx_out = torch.empty((B, k), dtype=torch.int32, device=sel_keys.device)
     _need(idx_out.shape == (B, k) and idx_out.dtype == torch.int32 and idx_out.is_contiguous(),
@@ -180,7 +180,7 @@ def cmc_select_cmes(sel_keys, q_vec, k: int, idx_out=None, scores_out=None, work
                                 device=sel_keys.device)
     if workspace is not None:
         ws_bytes = workspace.numel() * workspace.element_size()
-    rc = lib().cmc_select_cmes(_ptr(sel_keys), _ptr(q_vec), B, N, D, int(k), _ptr(idx_out),
+    rc = lib().cmc_select_cmes(_ptr(sel_keys), _kv_dtype(sel_keys), _ptr(q_vec), B, N, D, int(k), _ptr(idx_out),
                                _ptr(scores_out), _ptr(workspace), ws_bytes, _stream(stream))
     _check(rc)
     return idx_out
@@ -191,13 +191,13 @@ def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_str
                            stream=None):
     """Ragged Tier-1 selection: sequence b's candidates are its first
     n_rows[b] rows; q_rows[b] pinned question rows (pool rows n_b ..) follow
-    the selected ones.  n_rows/q_rows [B] int32 (device).  Returns
-    (idx_out [B][idx_stride] int32, k_out [B] int32)."""
+    the selected ones.  sel_keys fp32 or bf16; n_rows/q_rows [B] int32
+    (device).  Returns (idx_out [B][idx_stride] int32, k_out [B] int32)."""
     import torch
     _need(sel_keys.dim() == 3 and sel_keys.is_contiguous(), "sel_keys must be contiguous [B][N][D]")
     B, N, D = sel_keys.shape
     _need(q_vec.shape == (B, D) and q_vec.is_contiguous(), "q_vec must be contiguous [B][D]")
-    _need(sel_keys.dtype == torch.float32 and q_vec.dtype == torch.float32, "fp32 inputs expected")
+    _need(q_vec.dtype == torch.float32, "q_vec must be fp32")
     _need(n_rows.shape == (B,) and n_rows.dtype == torch.int32 and n_rows.is_contiguous(), "n_rows [B] int32")
     if q_rows is not None:
         _need(q_rows.shape == (B,) and q_rows.dtype == torch.int32 and q_rows.is_contiguous(), "q_rows [B] int32")
@@ -220,7 +220,8 @@ def cmc_select_cmes_ragged(sel_keys, q_vec, n_rows, k: int, q_rows=None, idx_str
         workspace = torch.empty(max(1, cmc_select_workspace_bytes(B, N)), dtype=torch.uint8, device=dev)
     if workspace is not None:
         ws_bytes = workspace.numel() * workspace.element_size()
-    rc = lib().cmc_select_cmes_ragged(_ptr(sel_keys), _ptr(q_vec), _ptr(n_rows), _ptr(q_rows), B, N, D,
+    rc = lib().cmc_select_cmes_ragged(_ptr(sel_keys), _kv_dtype(sel_keys), _ptr(q_vec), _ptr(n_rows), _ptr(q_rows),
+                                      B, N, D,
                                       int(k), stride, _ptr(idx_out), _ptr(k_out), _ptr(scores_out),
                                       _ptr(norms_out), _ptr(workspace), ws_bytes, _stream(stream))
     _check(rc)
@@ -263,11 +264,11 @@ def cmc_bridge_workspace_bytes(M: int, F: int) -> int:
 
 
 def cmc_memory_bridge(h, w1, b1, w2, b2, ln_gamma, ln_beta, nu: float, ln_eps: float = 1e-5, out=None,
-                      workspace=None, stream=None):
+                      h_norms_out=None, workspace=None, stream=None):
     """MemoryBridge projection.  h [M][Hc] bf16, w1 [F][Hc] bf16, b1 [F] fp32,
     w2 [Hd][F] bf16, b2/ln_gamma/ln_beta [Hd] fp32 (device).  Returns out
     [M][Hd] fp32; the workspace (if given) then holds the hidden activations
-    [M][F] bf16."""
+    [M][F] bf16, and h_norms_out (if given, [M] fp32) the norms |h_j|."""
     import torch
     bf, f32 = torch.bfloat16, torch.float32
     _need(h.dim() == 2 and h.dtype == bf and h.is_contiguous(), "h must be contiguous bf16 [M][Hc]")
@@ -281,11 +282,15 @@ def cmc_memory_bridge(h, w1, b1, w2, b2, ln_gamma, ln_beta, nu: float, ln_eps: f
     if out is None:
         out = torch.empty((M, Hd), dtype=f32, device=h.device)
     _need(out.shape == (M, Hd) and out.dtype == f32 and out.is_contiguous(), "out [M][Hd] fp32")
+    if h_norms_out is not None:
+        _need(h_norms_out.numel() == M and h_norms_out.dtype == f32 and h_norms_out.is_contiguous(),
+              "h_norms_out [M] fp32")
     if workspace is None:
         workspace = torch.empty(max(1, cmc_bridge_workspace_bytes(M, F)), dtype=torch.uint8, device=h.device)
     ws_bytes = workspace.numel() * workspace.element_size()
     rc = lib().cmc_memory_bridge(_ptr(h), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(ln_gamma), _ptr(ln_beta),
-                                 float(nu), float(ln_eps), M, Hc, F, Hd, _ptr(out), _ptr(workspace), ws_bytes,
+                                 float(nu), float(ln_eps), M, Hc, F, Hd, _ptr(out), _ptr(h_norms_out),
+                                 _ptr(workspace), ws_bytes,
                                  _stream(stream))
     _check(rc)
     return out

@@ -1,4 +1,4 @@
-// MemoryBridge (Sec. 2.2): each CME vector h (encoder width Hc) becomes a
+// MemoryBridge (Sec. 2.3): each CME vector h (encoder width Hc) becomes a
 // decoder-ready memory row
 //   m_hat = LayerNorm(W2 GELU(W1 h + b1) + b2)          (LayerNorm per the appendix)
 //   m     = nu tanh(m_hat) * min(1, 2 nu / |nu tanh(m_hat)|)   (the section's cap)
@@ -23,6 +23,11 @@
 // bridge_norm_kernel: one wave per output row, in place, the row held in
 // registers: mean and biased variance (two passes over the registers),
 // LayerNorm with gamma/beta, nu tanh, the row norm, and the cap.
+//
+// cme_norm_kernel (optional): |h_j| of every input row, the norms that
+// CME-guided localization ranks (the capped output rows cannot serve: the
+// cap pins the norm of every row whose nu tanh(m_hat) exceeds 2 nu at
+// exactly 2 nu, which at decoder widths is every row).
 #include <algorithm>
 
 #include "device_common.hpp"
@@ -418,6 +423,27 @@ __global__ __launch_bounds__(256) void bridge_norm_wide_kernel(BridgeParams p) {
     }
 }
 
+// Norms of the CME vectors h themselves (the encoder's hidden states at the
+// placeholder positions), for CME-guided window localization: one wave per
+// row, 16-byte loads of 8 bf16 elements widened exactly, squares summed in
+// fp32 in a fixed per-lane order, then the DPP/permlane butterfly.  Runs
+// before the first GEMM, so that GEMM then finds h in the last-level cache.
+__global__ __launch_bounds__(256) void cme_norm_kernel(const uint16_t *h, int M, int Hc, float *norms) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= M) return;  // wave-uniform; no barriers
+    const uint4 *h4 = reinterpret_cast<const uint4 *>(h + (size_t)row * Hc);
+    float s = 0.f;
+    for (int c = lane; c < Hc / 8; c += kWave) {
+        float x[8];
+        Vec16<uint16_t>::widen(h4[c], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s = fmaf(x[e], x[e], s);
+    }
+    s = lane_reduce<OpSum, 1, kWave>(s);
+    if (lane == 0) norms[row] = sqrtf(s);
+}
+
 hipError_t launch_norm(const BridgeParams &p, hipStream_t stream) {
     const unsigned grid = (unsigned)((p.M + 3) / 4);
     if (p.Hd <= 256 * 4)
@@ -480,8 +506,14 @@ hipError_t launch_gemm(int epi, const GemmParams &g, hipStream_t stream) {
 
 hipError_t launch_memory_bridge(const BridgeParams &p, hipStream_t stream) {
     if (p.M == 0) return hipSuccess;
+    hipError_t e;
+    if (p.h_norms) {
+        cme_norm_kernel<<<(unsigned)((p.M + 3) / 4), 256, 0, stream>>>(p.h, p.M, p.Hc, p.h_norms);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     GemmParams g1{p.h, p.w1, p.b1, p.hidden, p.M, p.F, p.Hc};
-    hipError_t e = launch_gemm(0, g1, stream);
+    e = launch_gemm(0, g1, stream);
     if (e != hipSuccess) return e;
     GemmParams g2{p.hidden, p.w2, p.b2, p.out, p.M, p.Hd, p.F};
     e = launch_gemm(1, g2, stream);

@@ -38,6 +38,18 @@ bool supported_dh(int dh) { return dh == 64 || dh == 128 || dh == 256; }
 
 size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
+// Checks shared by the uniform and ragged selection: the key type and the
+// key width it allows (16-byte vectors of 4 fp32 or 8 bf16 elements).
+cmc_status check_keys(const char *fn, cmc_dtype key_dtype, int D) {
+    if (key_dtype != CMC_F32 && key_dtype != CMC_BF16)
+        return fail(CMC_ERR_UNSUPPORTED, "%s: unknown key_dtype %d", fn, (int)key_dtype);
+    const int vec = key_dtype == CMC_BF16 ? 8 : 4;
+    if (D % vec != 0)
+        return fail(CMC_ERR_UNSUPPORTED, "%s: D=%d must be a multiple of %d for %s keys", fn, D, vec,
+                    key_dtype == CMC_BF16 ? "bf16" : "fp32");
+    return CMC_OK;
+}
+
 }  // namespace
 
 // Build-time tuning knob: the number of 4-wave decode workgroups the split
@@ -138,13 +150,13 @@ size_t cmc_select_workspace_bytes(int B, int N) {
     return align256((size_t)B * (size_t)N * sizeof(float));
 }
 
-cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int N, int D, int k,
-                           int32_t *idx_out, float *scores_out, void *workspace,
-                           size_t workspace_bytes, void *stream) {
+cmc_status cmc_select_cmes(const void *sel_keys, cmc_dtype key_dtype, const float *q_vec, int B, int N, int D,
+                           int k, int32_t *idx_out, float *scores_out, void *workspace, size_t workspace_bytes,
+                           void *stream) {
     if (B < 0 || N < 0 || k < 0 || D < 4)
         return fail(CMC_ERR_INVALID_ARGUMENT, "select: need B >= 0, N >= 0, k >= 0, D >= 4 (got B=%d N=%d k=%d D=%d)", B, N, k, D);
     if (k > N) return fail(CMC_ERR_INVALID_ARGUMENT, "select: k=%d exceeds N=%d", k, N);
-    if (D % 4 != 0) return fail(CMC_ERR_UNSUPPORTED, "select: D=%d must be a multiple of 4", D);
+    if (cmc_status st = check_keys("select", key_dtype, D)) return st;
     if (N > cmc::kSelectMaxN) return fail(CMC_ERR_UNSUPPORTED, "select: N=%d exceeds %d", N, cmc::kSelectMaxN);
     if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "select: B=%d exceeds 65535", B);
     if ((long long)B * N == 0) return ok();
@@ -161,21 +173,22 @@ cmc_status cmc_select_cmes(const float *sel_keys, const float *q_vec, int B, int
                         workspace ? workspace_bytes : (size_t)0);
         scores = static_cast<float *>(workspace);
     }
-    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, k, nullptr, nullptr, nullptr, nullptr};
+    cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, k, nullptr, nullptr, nullptr, nullptr,
+                        key_dtype == CMC_BF16};
     hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }
 
-cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, const int32_t *n_rows,
-                                  const int32_t *q_rows, int B, int N, int D, int k, int idx_stride,
-                                  int32_t *idx_out, int32_t *k_out, float *scores_out, float *norms_out,
-                                  void *workspace, size_t workspace_bytes, void *stream) {
+cmc_status cmc_select_cmes_ragged(const void *sel_keys, cmc_dtype key_dtype, const float *q_vec,
+                                  const int32_t *n_rows, const int32_t *q_rows, int B, int N, int D, int k,
+                                  int idx_stride, int32_t *idx_out, int32_t *k_out, float *scores_out,
+                                  float *norms_out, void *workspace, size_t workspace_bytes, void *stream) {
     if (B < 0 || N < 0 || k < 0 || D < 4)
         return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: need B >= 0, N >= 0, k >= 0, D >= 4 (got B=%d N=%d k=%d D=%d)", B, N, k, D);
     if (idx_stride < k)
         return fail(CMC_ERR_INVALID_ARGUMENT, "select_ragged: idx_stride=%d is below k=%d", idx_stride, k);
-    if (D % 4 != 0) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: D=%d must be a multiple of 4", D);
+    if (cmc_status st = check_keys("select_ragged", key_dtype, D)) return st;
     if (N > cmc::kSelectMaxN) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: N=%d exceeds %d", N, cmc::kSelectMaxN);
     if (B > 65535) return fail(CMC_ERR_UNSUPPORTED, "select_ragged: B=%d exceeds 65535", B);
     if (B == 0) return ok();
@@ -197,7 +210,7 @@ cmc_status cmc_select_cmes_ragged(const float *sel_keys, const float *q_vec, con
         scores = static_cast<float *>(workspace);
     }
     cmc::SelectParams p{sel_keys, q_vec, scores, idx_out, B, N, D, k, idx_stride, n_rows, q_rows, k_out,
-                        norms_out};
+                        norms_out, key_dtype == CMC_BF16};
     hipError_t e = cmc::launch_select(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select_ragged launch");
     return ok();
@@ -235,7 +248,8 @@ size_t cmc_bridge_workspace_bytes(int M, int F) {
 
 cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1, const void *w2, const float *b2,
                              const float *ln_gamma, const float *ln_beta, float nu, float ln_eps, int M, int Hc,
-                             int F, int Hd, float *out, void *workspace, size_t workspace_bytes, void *stream) {
+                             int F, int Hd, float *out, float *h_norms_out, void *workspace, size_t workspace_bytes,
+                             void *stream) {
     if (M < 0 || Hc < 1 || F < 1 || Hd < 1)
         return fail(CMC_ERR_INVALID_ARGUMENT, "bridge: need M >= 0 and Hc, F, Hd >= 1");
     if (!(nu > 0.f) || isinf(nu) || !(ln_eps >= 0.f) || isinf(ln_eps))
@@ -250,7 +264,8 @@ cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1, con
     if (!h || !w1 || !b1 || !w2 || !b2 || !ln_gamma || !ln_beta || !out)
         return fail(CMC_ERR_INVALID_ARGUMENT, "bridge: null pointer");
     if (misaligned(h) || misaligned(w1) || misaligned(b1) || misaligned(w2) || misaligned(b2) ||
-        misaligned(ln_gamma) || misaligned(ln_beta) || misaligned(out) || misaligned(workspace))
+        misaligned(ln_gamma) || misaligned(ln_beta) || misaligned(out) || misaligned(h_norms_out) ||
+        misaligned(workspace))
         return fail(CMC_ERR_UNSUPPORTED, "bridge: every pointer must be 16-byte aligned");
     const size_t need = cmc_bridge_workspace_bytes(M, F);
     if (!workspace || workspace_bytes < need)
@@ -258,7 +273,7 @@ cmc_status cmc_memory_bridge(const void *h, const void *w1, const float *b1, con
                     workspace ? workspace_bytes : (size_t)0);
     cmc::BridgeParams p{static_cast<const uint16_t *>(h), static_cast<const uint16_t *>(w1), b1,
                         static_cast<const uint16_t *>(w2), b2, ln_gamma, ln_beta, static_cast<uint16_t *>(workspace),
-                        out, M, Hc, F, Hd, nu, ln_eps};
+                        out, h_norms_out, M, Hc, F, Hd, nu, ln_eps};
     hipError_t e = cmc::launch_memory_bridge(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "bridge launch");
     return ok();

@@ -236,23 +236,38 @@ struct RingCount {
     }
 };
 
-// One (sequence, kv head) pair's arrival on its sequence's counter, by
-// thread 0 of the workgroup that completes the pair (see decode_kernel):
-// the increment depends on the ring count this wave loaded, so it is issued
-// after that load has returned.  Its returned value is read only when the
-// count is advanced, but the compiler waits for it where the branch ends, so
-// callers issue it next to loads they wait for anyway.
+// Arrival on the sequence's counter once this wave's read of the ring count
+// has returned (the increments below depend on the value read, so they are
+// issued after it).  With `lds` set (an unsplit plan) the waves of the
+// workgroup first count themselves on a workgroup counter in LDS, and only
+// the last of them arrives on the sequence's counter: the arrival then
+// follows every count read of the workgroup, at the cost of one LDS atomic
+// per wave (a device-scope atomic from every wave would make each wave's
+// next load waits include that atomic's latency, since loads and atomics
+// return in order).  The returned value is read only when the count is
+// advanced, but the compiler waits for it where the branch ends, so callers
+// issue it next to loads they wait for anyway.  prev stays ~0u in lanes
+// that did not arrive.
 struct Arrival {
     unsigned *ctrs;  // the sequence counters; the address is formed only in arrive(),
     int b;           // so no wait for that kernel argument precedes the first loads
     bool pending;    // wave-uniform
     unsigned prev;
+    unsigned *lds;   // workgroup counter (zeroed before a barrier), or nullptr
+    unsigned nw;     // waves of the workgroup
     __device__ __forceinline__ void arrive(int cnt_raw) {
         if (pending) {
-            if (threadIdx.x == 0)
-                prev = __hip_atomic_fetch_add(ctrs + b, (unsigned)(cnt_raw != INT_MIN) /* == 1 */, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
             pending = false;
+            const unsigned one = (unsigned)(cnt_raw != INT_MIN);  // == 1, after the count load returned
+            const bool lane0 = (threadIdx.x & 63) == 0;
+            bool last = true;
+            if (lds) {
+                unsigned r = 0;
+                if (lane0) r = __hip_atomic_fetch_add(lds, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                last = __builtin_amdgcn_readfirstlane(r) == nw - 1;  // wave-uniform
+            }
+            if (last && lane0)
+                prev = __hip_atomic_fetch_add(ctrs + b, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 };
@@ -436,7 +451,9 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
     // scores); P V on the VALU.
 #define CMC_COMPUTE(B0_, KR_, VR_)                                                                     \
     do {                                                                                             \
-        const bool bfull = rows.all_valid((B0_), min((B0_) + 16, r1)); /* uniform */                \
+        /* uniform; a block reaching past r1 is never "full": its rows past the */                    \
+        /* phase end may have been loaded before r1 was limited by the count */                     \
+        const bool bfull = (B0_) + 16 <= r1 && rows.all_valid((B0_), (B0_) + 16);                   \
         const bool kval = (B0_) + r16 < r1 && (bfull || rows.valid((B0_) + r16));                    \
         floatx4 c = {0.f, 0.f, 0.f, 0.f};                                                            \
         _Pragma("unroll") for (int i = 0; i < SL; ++i) {                                             \
@@ -464,7 +481,8 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
         wave_lds_sync();                                                                             \
         _Pragma("unroll") for (int qq = 0; qq < 4; ++qq) {                                           \
             if constexpr (Rows::kMasked) {                                                           \
-                /* masked ring slots may hold anything: zero their values (p is 0) */                 \
+                /* masked ring slots (and unfilled slots past r1) may hold anything, */              \
+                /* NaN included: zero their values, since 0 * NaN is NaN (p is 0) */                  \
                 const int vrow = (B0_) + 4 * qq + kq;                                                \
                 if (!bfull && !(vrow < r1 && rows.valid(vrow))) {                                    \
                     _Pragma("unroll") for (int j = 0; j < VW; ++j) VR_[qq][j] = make_uint4(0, 0, 0, 0); \
@@ -817,15 +835,25 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
     }
     const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0, min(cnt0, p.W));
 
-    // Ring count: the workgroup that completes a (sequence, kv head) pair
-    // arrives on the sequence's counter -- with S == 1 every workgroup, in
-    // its first block; with S > 1 the one that merges the pair, after every
-    // split of the pair has arrived on the pair counter (each after reading
-    // the count).  The last of the Hkv arrivals writes the advanced count and
-    // re-arms the counter.  No data is published through the counter, so no
-    // fence is needed.
+    // Ring count.  It may be advanced only after every wave of the
+    // sequence's workgroups has read it, so one arrival per (sequence, kv
+    // head) pair on the sequence's counter follows all of that pair's reads:
+    //   S == 1: each wave, once its own count load has returned (in its first
+    //     block, or after the loop if it had none), counts itself on the
+    //     workgroup's LDS counter; the last wave arrives for the pair;
+    //   S > 1: each split arrives on its pair counter after a barrier that
+    //     follows every count read of its workgroup; the merging workgroup
+    //     (the last split of the pair) then arrives for the pair.
+    // The last of the Hkv arrivals writes the advanced count and re-arms the
+    // counter, at its workgroup's end.  No data is published through the
+    // counter, so no fence is needed.
     const bool bump = p.T_new > 0 && p.W > 0;
-    Arrival arr{p.seq_counter, b, bump && wave == 0 && p.S == 1, 0u};
+    __shared__ unsigned s_reads;
+    if (bump && p.S == 1) {  // launch-uniform
+        if (threadIdx.x == 0) s_reads = 0u;
+        __syncthreads();
+    }
+    Arrival arr{p.seq_counter, b, bump && p.S == 1, ~0u, p.S == 1 ? &s_reads : nullptr, (unsigned)NW};
 
     WaveState<G, VEC> st;
     st.init();
@@ -841,7 +869,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
     const int cnt_now = MF ? cnt.value() : cnt0;
 #define CMC_BUMP()                                                                         \
     do {                                                                                 \
-        if (bump && threadIdx.x == 0 && arr.prev == (unsigned)(p.Hkv - 1)) {             \
+        if (bump && arr.prev == (unsigned)(p.Hkv - 1)) { /* one lane per sequence */   \
             p.win_count[b] = cnt_now + p.T_new;                                          \
             __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
         }                                                                                \

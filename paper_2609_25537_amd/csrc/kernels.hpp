@@ -74,7 +74,7 @@ struct GatherParams {
 hipError_t launch_gather(const GatherParams &p, hipStream_t stream);
 
 struct SelectParams {
-    const float *sel_keys;    // [B][N][D]
+    const void *sel_keys;     // [B][N][D] fp32 or bf16 (keys_bf16)
     const float *q_vec;       // [B][D]
     float *scores;            // [B][N]
     int32_t *idx_out;         // [B][idx_stride]
@@ -84,6 +84,7 @@ struct SelectParams {
     const int32_t *q_rows;    // [B] pinned question rows per sequence, or nullptr: none
     int32_t *k_out;           // [B] entries written per sequence, or nullptr
     float *norms;             // [B][N] row norms |m_j| (0 past n_b), or nullptr
+    bool keys_bf16;           // sel_keys holds bf16 bit patterns
 };
 constexpr int kSelectMaxN = 32768;
 hipError_t launch_select(const SelectParams &p, hipStream_t stream);
@@ -125,6 +126,7 @@ struct BridgeParams {
     const float *ln_beta;       // [Hd]
     uint16_t *hidden;           // [M][F] bf16 (workspace)
     float *out;                 // [M][Hd]
+    float *h_norms;             // [M] |h_j|, or nullptr
     int M, Hc, F, Hd;
     float nu, eps;
 };

@@ -3,9 +3,10 @@
 // document order.
 //
 // score_kernel: one wave per memory row (R rows per wave).  The dot product
-// and |m_j|^2 come out of ONE pass over the row (16-byte loads, fp32 FMA in
-// a fixed per-lane order, then a DPP/permlane butterfly), |q|^2 from the same
-// loop over q.  Zero norms are clamped to 1e-8, so a zero row scores 0.
+// and |m_j|^2 come out of ONE pass over the row (16-byte loads of fp32 or
+// bf16 keys, bf16 widened exactly, fp32 FMA in a fixed per-lane order, then a
+// DPP/permlane butterfly), |q|^2 from the same loop over q (fp32).  Zero
+// norms are clamped to 1e-8, so a zero row scores 0.
 //
 // topk_kernel: one 1024-thread workgroup per sequence.  Scores become
 // order-preserving uint32 keys (kept in registers, 32 per thread, so N <=
@@ -33,7 +34,60 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int clamp_count(int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
 
-template <int R>
+// One row's dot product with q and its squared norm, accumulated per lane
+// over 16-byte vectors of the row (4 fp32 or 8 bf16 elements, widened
+// exactly); |q|^2 from the same loop over q.
+template <int R, bool BF16>
+__device__ __forceinline__ void score_rows(const SelectParams &p, int b, int j0, int nb, int lane, float (&dot)[R],
+                                           float (&nn)[R], float &qq) {
+    const float4 *q4 = reinterpret_cast<const float4 *>(p.q_vec + (size_t)b * p.D);
+    const char *rows[R];
+    constexpr int EB = BF16 ? 2 : 4;  // bytes per key element
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = min(j0 + r, nb - 1);
+        rows[r] = static_cast<const char *>(p.sel_keys) + ((size_t)b * p.N + j) * p.D * EB;
+    }
+    constexpr int E = 16 / EB;  // elements per 16-byte vector
+    const int DV = p.D / E;
+#pragma unroll 2
+    for (int c = lane; c < DV; c += kWave) {
+        float qv[E];
+#pragma unroll
+        for (int i = 0; i < E / 4; ++i) {
+            const float4 t = q4[c * (E / 4) + i];
+            qv[4 * i + 0] = t.x;
+            qv[4 * i + 1] = t.y;
+            qv[4 * i + 2] = t.z;
+            qv[4 * i + 3] = t.w;
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) qq = fmaf(qv[e], qv[e], qq);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            // Non-temporal: each key row is read once (0.81 -> 0.74 ms on the
+            // 64 x 4096 x 4096 fp32 Mistral-shaped batch).
+            const f32x4 mw = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(rows[r] + (size_t)c * 16));
+            float mv[E];
+            if constexpr (BF16) {
+                const uint4 u = make_uint4(__float_as_uint(mw.x), __float_as_uint(mw.y), __float_as_uint(mw.z),
+                                           __float_as_uint(mw.w));
+                Vec16<uint16_t>::widen(u, mv);
+            } else {
+                mv[0] = mw.x;
+                mv[1] = mw.y;
+                mv[2] = mw.z;
+                mv[3] = mw.w;
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e) dot[r] = fmaf(mv[e], qv[e], dot[r]);
+#pragma unroll
+            for (int e = 0; e < E; ++e) nn[r] = fmaf(mv[e], mv[e], nn[r]);
+        }
+    }
+}
+
+template <int R, bool BF16>
 __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
     const int b = blockIdx.y;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -50,41 +104,10 @@ __global__ __launch_bounds__(256) void score_kernel(SelectParams p) {
         return;
     }
 
-    const int D4 = p.D / 4;
-    const float4 *q4 = reinterpret_cast<const float4 *>(p.q_vec + (size_t)b * p.D);
-    const float4 *rows[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int j = min(j0 + r, nb - 1);
-        rows[r] = reinterpret_cast<const float4 *>(p.sel_keys + ((size_t)b * p.N + j) * p.D);
-    }
     float dot[R], nn[R], qq = 0.f;
 #pragma unroll
     for (int r = 0; r < R; ++r) dot[r] = nn[r] = 0.f;
-
-#pragma unroll 2
-    for (int c = lane; c < D4; c += kWave) {
-        const float4 qv = q4[c];
-        qq = fmaf(qv.x, qv.x, qq);
-        qq = fmaf(qv.y, qv.y, qq);
-        qq = fmaf(qv.z, qv.z, qq);
-        qq = fmaf(qv.w, qv.w, qq);
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            // Non-temporal: each key row is read once (0.81 -> 0.74 ms on the
-            // 64 x 4096 x 4096 Mistral-shaped batch).
-            const f32x4 mw = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(&rows[r][c]));
-            const float4 mv = make_float4(mw.x, mw.y, mw.z, mw.w);
-            dot[r] = fmaf(mv.x, qv.x, dot[r]);
-            dot[r] = fmaf(mv.y, qv.y, dot[r]);
-            dot[r] = fmaf(mv.z, qv.z, dot[r]);
-            dot[r] = fmaf(mv.w, qv.w, dot[r]);
-            nn[r] = fmaf(mv.x, mv.x, nn[r]);
-            nn[r] = fmaf(mv.y, mv.y, nn[r]);
-            nn[r] = fmaf(mv.z, mv.z, nn[r]);
-            nn[r] = fmaf(mv.w, mv.w, nn[r]);
-        }
-    }
+    score_rows<R, BF16>(p, b, j0, nb, lane, dot, nn, qq);
     qq = lane_reduce<OpSum, 1, kWave>(qq);
     const float qn = fmaxf(sqrtf(qq), 1e-8f);
 #pragma unroll
@@ -285,10 +308,12 @@ hipError_t launch_select(const SelectParams &p, hipStream_t stream) {
         const long long rows = (long long)p.B * p.N;
         if (rows >= 65536) {
             dim3 grid((p.N + 15) / 16, p.B);
-            score_kernel<4><<<grid, 256, 0, stream>>>(p);
+            if (p.keys_bf16) score_kernel<4, true><<<grid, 256, 0, stream>>>(p);
+            else score_kernel<4, false><<<grid, 256, 0, stream>>>(p);
         } else {
             dim3 grid((p.N + 3) / 4, p.B);
-            score_kernel<1><<<grid, 256, 0, stream>>>(p);
+            if (p.keys_bf16) score_kernel<1, true><<<grid, 256, 0, stream>>>(p);
+            else score_kernel<1, false><<<grid, 256, 0, stream>>>(p);
         }
         e = hipGetLastError();
     }

@@ -420,7 +420,7 @@ def denoise_emb(w: DenoiseWorkload, b: Optional[int] = None) -> np.ndarray:
 
 @dataclasses.dataclass(frozen=True)
 class BridgeWorkload:
-    """MemoryBridge inputs (Sec. 2.2): M CME vectors of the encoder width Hc
+    """MemoryBridge inputs (Sec. 2.3): M CME vectors of the encoder width Hc
     projected through hidden width F to the decoder width Hd.  Weights are
     nn.Linear-scaled draws (N(0, 1/fan_in)), biases N(0, 0.02^2), LayerNorm
     gamma 1 + N(0, 0.1^2) and beta N(0, 0.1^2), all rounded to bf16 where

@@ -470,12 +470,34 @@ def pin_decode_ragged_history(orc):
 
 
 def pin_row_norms_library(orc):
-    """Row norms vs numpy's own norm routine."""
+    """Row norms vs numpy's own norm routine: fp32 rows [B][N][D], and bf16
+    CME vectors [M][Hc] (bit patterns widened here by a shift)."""
     rng = np.random.default_rng(51)
     keys = rng.standard_normal((3, 17, 9)).astype(np.float32)
     keys[1, 4] = 0.0
     ref = np.linalg.norm(keys.astype(np.float64), axis=2)
     _close(orc.row_norms(keys), ref, 1e-12, "row norms")
+    h = _bf16(rng.standard_normal((37, 64)).astype(np.float32) * 3.0)
+    h[5] = 0
+    wide = (h.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    _close(orc.row_norms(h), np.linalg.norm(wide, axis=1), 1e-12, "bf16 row norms")
+
+
+def pin_select_bf16_keys(orc):
+    """Selection on bf16 keys equals selection on their exact fp32 widening
+    (indices and scores), the widening done here by a shift of the bits."""
+    rng = np.random.default_rng(52)
+    for B, N, D, k in [(2, 40, 16, 7), (3, 9, 8, 9), (1, 200, 24, 31)]:
+        keys = _bf16(rng.standard_normal((B, N, D)).astype(np.float32))
+        keys[0, 3] = keys[0, 1]          # an exact tie
+        wide = (keys.astype(np.uint32) << 16).view(np.float32)
+        q = rng.standard_normal((B, D)).astype(np.float32)
+        i1, s1, g1 = orc.select(keys, q, k)
+        i2, s2, g2 = orc.select(wide, q, k)
+        assert (i1 == i2).all(), "bf16 keys select differently from their widening"
+        _close(s1, s2, 0.0, "bf16 key scores")
+        for b in range(B):
+            assert brute.exact_topk(wide[b], q[b], k) == i1[b].tolist(), "bf16 keys vs exact ranking"
 
 
 def pin_locate_cases(orc):

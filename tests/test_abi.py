@@ -46,22 +46,41 @@ def test_window_start_matches_golden():
 FAKE = 1 << 20  # 16-byte aligned non-null address, never dereferenced: calls below fail validation first
 
 
-@pytest.mark.parametrize("args,code", [
-    ((FAKE, FAKE, 1, 4, 8, 5, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),   # k > N
-    ((FAKE, FAKE, 1, 4, 6, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),        # D % 4
-    ((FAKE, FAKE, 1, 40000, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),    # N too big
-    ((FAKE, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 16, None), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
-    ((None, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),
-    ((FAKE + 4, FAKE, 2, 64, 8, 2, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_UNSUPPORTED),   # alignment
-    ((FAKE, FAKE, 2, 64, 8, -1, FAKE, None, FAKE, 1 << 20, None), cmc.CMC_ERR_INVALID_ARGUMENT),
+def _sel(**kw):
+    a = dict(keys=FAKE, kd=cmc.CMC_F32, qv=FAKE, B=2, N=64, D=8, k=2, idx=FAKE, sc=None, ws=FAKE, wsb=1 << 20,
+             s=None)
+    a.update(kw)
+    return cmc.lib().cmc_select_cmes(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=1, N=4, k=5), cmc.CMC_ERR_INVALID_ARGUMENT),        # k > N
+    (dict(D=6), cmc.CMC_ERR_UNSUPPORTED),                       # D % 4 (fp32 keys)
+    (dict(D=12, kd=cmc.CMC_BF16), cmc.CMC_ERR_UNSUPPORTED),     # D % 8 (bf16 keys)
+    (dict(kd=5), cmc.CMC_ERR_UNSUPPORTED),                      # unknown key dtype
+    (dict(N=40000), cmc.CMC_ERR_UNSUPPORTED),                   # N too big
+    (dict(wsb=16), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
+    (dict(keys=None), cmc.CMC_ERR_INVALID_ARGUMENT),
+    (dict(keys=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # alignment
+    (dict(k=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
 ])
-def test_select_validation(args, code):
-    assert cmc.lib().cmc_select_cmes(*args) == code
+def test_select_validation(kw, code):
+    assert _sel(**kw) == code
     assert cmc.last_error()
 
 
+def test_select_signature_takes_key_dtype():
+    """The boundary's selection takes the key type right after the keys:
+    (sel_keys, key_dtype, q_vec, B, N, D, k, idx_out, scores_out, workspace,
+    workspace_bytes, stream); bf16 keys with D % 8 == 0 pass validation."""
+    assert _sel(B=0, kd=cmc.CMC_BF16, D=16) == cmc.CMC_OK
+    assert _sel(D=16, kd=cmc.CMC_BF16, wsb=16) == cmc.CMC_ERR_WORKSPACE_TOO_SMALL  # got past the dtype checks
+    assert len(cmc.lib().cmc_select_cmes.argtypes) == 12
+    assert len(cmc.lib().cmc_select_cmes_ragged.argtypes) == 17
+
+
 def test_select_empty_is_ok():
-    assert cmc.lib().cmc_select_cmes(None, None, 0, 10, 8, 3, None, None, None, 0, None) == cmc.CMC_OK
+    assert _sel(keys=None, qv=None, B=0, N=10, k=3, idx=None, ws=None, wsb=0) == cmc.CMC_OK
     assert cmc.last_error() == ""
 
 
@@ -127,8 +146,8 @@ def test_append_without_window_is_noop():
 
 
 def _sel_r(**kw):
-    a = dict(keys=FAKE, qv=FAKE, n=FAKE, qr=None, B=2, N=64, D=8, k=4, stride=6, idx=FAKE, kout=FAKE,
-             sc=None, nrm=None, ws=FAKE, wsb=1 << 20, s=None)
+    a = dict(keys=FAKE, kd=cmc.CMC_F32, qv=FAKE, n=FAKE, qr=None, B=2, N=64, D=8, k=4, stride=6, idx=FAKE,
+             kout=FAKE, sc=None, nrm=None, ws=FAKE, wsb=1 << 20, s=None)
     a.update(kw)
     return cmc.lib().cmc_select_cmes_ragged(*a.values())
 
@@ -138,6 +157,8 @@ def _sel_r(**kw):
     (dict(stride=3), cmc.CMC_ERR_INVALID_ARGUMENT),           # idx_stride < k
     (dict(idx=None), cmc.CMC_ERR_INVALID_ARGUMENT),
     (dict(D=6), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(D=12, kd=cmc.CMC_BF16), cmc.CMC_ERR_UNSUPPORTED),   # D % 8 (bf16 keys)
+    (dict(kd=3), cmc.CMC_ERR_UNSUPPORTED),
     (dict(N=40000), cmc.CMC_ERR_UNSUPPORTED),
     (dict(wsb=16), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
     (dict(qr=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # alignment
@@ -243,7 +264,7 @@ def test_denoise_workspace_query():
 
 def _bridge(**kw):
     a = dict(h=FAKE, w1=FAKE, b1=FAKE, w2=FAKE, b2=FAKE, g=FAKE, be=FAKE, nu=1.0, eps=1e-5, M=10, Hc=64, F=128,
-             Hd=128, out=FAKE, ws=FAKE, wsb=1 << 20, s=None)
+             Hd=128, out=FAKE, hn=None, ws=FAKE, wsb=1 << 20, s=None)
     a.update(kw)
     return cmc.lib().cmc_memory_bridge(*a.values())
 
@@ -258,6 +279,7 @@ def _bridge(**kw):
     (dict(M=-1), cmc.CMC_ERR_INVALID_ARGUMENT),
     (dict(b2=None), cmc.CMC_ERR_INVALID_ARGUMENT),
     (dict(w1=FAKE + 2), cmc.CMC_ERR_UNSUPPORTED),
+    (dict(hn=FAKE + 4), cmc.CMC_ERR_UNSUPPORTED),             # h_norms_out alignment
     (dict(wsb=100), cmc.CMC_ERR_WORKSPACE_TOO_SMALL),
 ])
 def test_bridge_validation(kw, code):

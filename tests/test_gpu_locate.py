@@ -1,12 +1,15 @@
 """CME-guided Tier-2 localization on the GPU vs the oracle, through the C
-ABI: row norms from the selection pass (within 1e-6 relative of the fp64
-norms), and the chosen chunk offset and window start (bit-exact, decided on
-the same fp32 norms on both sides)."""
+ABI: row norms (from the selection pass, and the CME norms |h_j| from the
+MemoryBridge call, which localization ranks) within their fp32 bounds of the
+fp64 norms, and the chosen chunk offset and window start (bit-exact, decided
+on the same fp32 norms on both sides, and on the bridge workload against the
+oracle's whole fp64 chain)."""
 import numpy as np
 import pytest
 import torch
 
 from paper_2609_25537_amd import cmc
+from paper_2609_25537_amd import workloads as wl
 from tests.gpu_util import DEV, say, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
@@ -87,3 +90,53 @@ def test_select_then_locate(orc):
     ref_a, ref_s = orc.locate(orc.row_norms(keys), ctx, 512, m, n_rows, None, 4 * m)
     assert (to_host(alpha) == ref_a).all() and (to_host(start) == ref_s).all()
     assert to_host(alpha).tolist()[:3] == [(s // m) * 4 * m for s in star[:3]]
+
+
+def _norm_rel_bound(H: int) -> float:
+    """Relative error bound of the kernel's fp32 norm of an H-wide bf16 row:
+    each lane sums its squares in one chain of ceil(H / 512) * 8 fused
+    multiply-adds, then a 6-step butterfly adds the 64 lane sums, so the
+    squared norm is within gamma_n (n = chain + 6, gamma_n = n u / (1 - n u))
+    of the exact one (all terms are non-negative); the square root halves
+    that and adds one rounding."""
+    u = 2.0 ** -24
+    n = -(-H // 512) * 8 + 6
+    return 0.5 * n * u / (1 - n * u) + u
+
+
+@pytest.mark.timeout(300)
+def test_bridge_cme_norms_then_locate(orc):
+    """The MemoryBridge workload end to end: the bridge call returns the CME
+    norms |h_j| of its 49,152 input rows (64 contexts x 12 chunks x 64 CMEs),
+    localization ranks them per context.  Norms within their fp32 bound of
+    the oracle's fp64 norms; alpha and start bit-exact against the oracle's
+    chain (fp64 norms -> argmax -> chunk offset -> window start) wherever the
+    two largest norms of a context are further apart than that bound, and
+    otherwise equal to the oracle's decision on the kernel's own norms."""
+    w = wl.BRIDGE_WORKLOADS["bridge_gpt2l_llama3_batch64"]
+    B, N, m, chunk_tokens, ctx_len, W = 64, 768, 64, 256, 3072, 256
+    assert B * N == w.M
+    say(f"bridge -> locate: M={w.M} Hc={w.Hc}")
+    h = wl.bridge_h(w)
+    p = wl.bridge_params(w)
+    bf = lambda a: to_dev(np.ascontiguousarray(a))
+    hn = torch.empty((w.M,), dtype=torch.float32, device=DEV)
+    cmc.cmc_memory_bridge(bf(h), bf(p["w1"]), to_dev(p["b1"]), bf(p["w2"]), to_dev(p["b2"]), to_dev(p["gamma"]),
+                          to_dev(p["beta"]), w.nu, w.eps, h_norms_out=hn)
+    ctx = np.full(B, ctx_len, np.int32)
+    alpha, start = cmc.cmc_locate_window(hn.view(B, N), to_dev(ctx), W, m, chunk_tokens=chunk_tokens)
+    torch.cuda.synchronize()
+    got_n = to_host(hn).astype(np.float64).reshape(B, N)
+    ref_n = orc.row_norms(h).reshape(B, N)
+    rel = _norm_rel_bound(w.Hc)
+    assert (np.abs(got_n - ref_n) <= rel * ref_n).all(), f"worst rel err {np.max(np.abs(got_n / ref_n - 1)):.2e}"
+    ref_a, ref_s = orc.locate(ref_n, ctx, W, m, chunk_tokens=chunk_tokens)
+    own_a, own_s = orc.locate(got_n, ctx, W, m, chunk_tokens=chunk_tokens)
+    ga, gs = to_host(alpha), to_host(start)
+    top2 = -np.partition(-ref_n, 1, axis=1)[:, :2]
+    resolved = (top2[:, 0] - top2[:, 1]) > 2 * rel * top2[:, 0]
+    assert resolved.sum() >= B - 2, "workload norms too close to rank in fp32"
+    assert (ga[resolved] == ref_a[resolved]).all() and (gs[resolved] == ref_s[resolved]).all()
+    assert (ga == own_a).all() and (gs == own_s).all()
+    # the chosen chunks vary across contexts (the norms rank, they do not tie)
+    assert len(np.unique(ga)) > 4

@@ -87,6 +87,51 @@ def test_select_exact_ties(orc, N, k):
     _check_select(orc, keys, qv, k, "ties")
 
 
+@pytest.mark.parametrize("B,N,D,k,dup", [
+    (1, 7, 8, 3, 0), (3, 33, 16, 5, 0), (4, 4096, 64, 512, 6), (1, 32768, 8, 1024, 0), (2, 2047, 264, 1, 4),
+])
+def test_select_bf16_keys(orc, B, N, D, k, dup):
+    """bf16 selection keys (key_dtype = CMC_BF16) against the oracle on the
+    same bits.  Rounding the separated keys to bf16 merges close ones into
+    exact duplicates, which tie exactly on both sides (lower index wins)."""
+    keys, qv = _separated(B, N, D, seed=N + k + 1, dup_every=dup)
+    kb = _bf16(keys)
+    say(f"select bf16 keys: B={B} N={N} D={D} k={k}")
+    ref_idx, ref_s, _ = orc.select(kb, qv, k)
+    scores = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    idx = cmc.cmc_select_cmes(to_dev(kb), to_dev(qv), k, scores_out=scores)
+    torch.cuda.synchronize()
+    assert (to_host(idx) == ref_idx).all(), "index sets differ"
+    assert max_abs(to_host(scores), ref_s) < 1e-6
+
+
+def _accepted_bf16(w, orc, keys_bf16):
+    """Per sequence, the first question draw whose top-k gap on the bf16
+    keys clears the workload's rule."""
+    att = []
+    for b in range(w.B):
+        a = 0
+        while orc.select(keys_bf16[b:b + 1], wl.q_vec(w, b, a)[None], w.k)[2][0] < w.gap_min:
+            a += 1
+            assert a < 2000
+        att.append(a)
+    return att
+
+
+def test_select_bf16_keys_llama_layer_full_size(orc):
+    """The Llama-layer selection (N = 2048, D = 4096) with its keys rounded
+    to bf16, which halves the bytes the scoring pass reads."""
+    w = wl.get("llama3_8b_layer")
+    kb = _bf16(wl.sel_keys(w))
+    qv = wl.q_vecs(w, _accepted_bf16(w, orc, kb))
+    say("select bf16 keys: llama3_8b_layer")
+    ref_idx, _, gap = orc.select(kb, qv, w.k)
+    assert (gap >= w.gap_min).all()
+    idx = cmc.cmc_select_cmes(to_dev(kb), to_dev(qv), w.k)
+    torch.cuda.synchronize()
+    assert (to_host(idx) == ref_idx).all()
+
+
 def test_select_zero_rows_and_question(orc):
     keys, qv = _separated(2, 100, 8, seed=3)
     keys[0, 10] = 0.0
@@ -168,8 +213,20 @@ def _logit_bound_tol(q, keys_f64, scale, vmax, Dh):
     return 2.0 * dz * vmax + 1e-5
 
 
+def _same_bits(a, b) -> bool:
+    """Bitwise equality (NaN patterns included)."""
+    a, b = np.ascontiguousarray(a), np.ascontiguousarray(b)
+    u = {2: np.uint16, 4: np.uint32}[a.dtype.itemsize]
+    return a.shape == b.shape and a.dtype == b.dtype and bool((a.view(u) == b.view(u)).all())
+
+
+def _nan_like(x):
+    """A NaN of x's element type (bf16 bits are uint16)."""
+    return np.uint16(0x7FC0) if x.dtype == np.uint16 else np.float32("nan")
+
+
 def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_none=False, scale=None,
-                 kv_std=1.0, derived_tol=False, fused=False, t_new=1):
+                 kv_std=1.0, derived_tol=False, fused=False, t_new=1, unused_nan=False):
     rng = np.random.default_rng(seed)
     f = lambda *s: (rng.standard_normal(s) * kv_std).astype(np.float32)
     cv = _bf16 if dtype == "bf16" else (lambda x: x)
@@ -184,6 +241,9 @@ def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_n
         wk[:, :, :fill] = f(B, Hkv, fill, Dh)
         wv[:, :, :fill] = f(B, Hkv, fill, Dh)
     wk, wv = cv(wk), cv(wv)
+    if unused_nan:  # slots never filled hold NaN: they must not reach the output
+        wk[:, :, fill:] = _nan_like(wk)
+        wv[:, :, fill:] = _nan_like(wv)
     cnt = np.full((B,), fill, np.int32)
     scale = 1.0 / math.sqrt(Dh) if scale is None else scale
     d = dict(pk=to_dev(pk), pv=to_dev(pv), idx=None if idx is None else to_dev(idx),
@@ -211,7 +271,7 @@ def _decode_case(orc, B, Hq, Hkv, Dh, N, k, W, fill, dtype, seed, steps=3, idx_n
         torch.cuda.synchronize()
         assert not ws[:4 * (B + B * Hkv)].any(), "arrival counters must return to zero"
         if W:
-            assert (to_host(d["wk"]) == wk).all() and (to_host(d["wv"]) == wv).all(), "ring contents"
+            assert _same_bits(to_host(d["wk"]), wk) and _same_bits(to_host(d["wv"]), wv), "ring contents"
             assert (to_host(d["wc"]) == cnt).all(), "ring count"
         err = max_abs(to_host(out), ref)
         worst = max(worst, err)
@@ -296,6 +356,25 @@ def test_decode_random_configs(orc, seed):
     t_new = c["t_new"] if c["fused"] else 1
     _decode_case(orc, c["B"], c["Hq"], c["Hkv"], c["Dh"], c["N"], c["k"], c["W"], c["fill"], c["dtype"],
                  seed=2000 + seed, steps=2, idx_none=c["idx_none"], fused=c["fused"], t_new=t_new)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("B,Hkv,G,Dh,dtype,N,k,W,fill", [
+    (1, 8, 4, 128, "bf16", 300, 256, 512, 100),   # Llama-layer shape, split plan, ring a fifth full
+    (1, 8, 4, 128, "bf16", 300, 0, 512, 1),       # one filled slot
+    (2, 2, 1, 64, "bf16", 90, 40, 700, 333),      # G = 1, many splits
+    (32, 8, 4, 128, "bf16", 64, 32, 300, 45),     # 256 pairs: one 8-wave workgroup each (S = 1)
+    (3, 2, 2, 256, "bf16", 50, 20, 200, 17),      # wide head, single-buffered loop
+    (2, 2, 8, 128, "bf16", 50, 20, 200, 17),      # G = 8: VALU path
+    (2, 2, 4, 128, "f32", 50, 20, 200, 17),       # fp32: VALU path
+])
+def test_decode_unfilled_slots_hold_nan(orc, fused, B, Hkv, G, Dh, dtype, N, k, W, fill):
+    """Ring slots that were never filled may hold anything, NaN included:
+    the output must equal the oracle's (which never reads them) and stay
+    finite, with a ring that is not full and (where the plan splits) splits
+    that start past the filled slots."""
+    _decode_case(orc, B=B, Hq=G * Hkv, Hkv=Hkv, Dh=Dh, N=N, k=k, W=W, fill=fill, dtype=dtype,
+                 seed=B + W + fill + G, steps=3, fused=fused, unused_nan=True)
 
 
 def test_decode_empty_window_zero_output(orc):

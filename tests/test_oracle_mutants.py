@@ -23,8 +23,11 @@ MUTANTS = [
      "return (x->j < y->j) - (x->j > y->j);"),
     ("no_document_order", "qsort(out, (size_t)k, sizeof(int32_t), by_value);",
      "(void)by_value;"),
-    ("norm_of_query_in_row", "mm += (double)m[d] * (double)m[d];",
-     "mm += (double)q[d] * (double)q[d];"),
+    ("norm_of_query_in_row", "mm += m * m;", "mm += (double)q[d] * (double)q[d];"),
+    ("select_key_element_order", "const double m = load_elem(sel_keys, keys_bf16, row + d);",
+     "const double m = load_elem(sel_keys, keys_bf16, row + (d ^ 1));"),
+    ("row_norms_row_stride", "const double x = load_elem(rows, is_bf16, (size_t)r * D + d);",
+     "const double x = load_elem(rows, is_bf16, (size_t)r * (D / 2) + d);"),
     ("window_start_full_W", "long long s = alpha - W / 2;", "long long s = alpha - W;"),
     ("window_start_no_clamp_hi", "if (s > hi) s = hi;", "(void)hi;"),
     ("ring_slot_off_by_one", "int slot = (int)(((long long)c + t) % W);",
