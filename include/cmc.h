@@ -427,6 +427,33 @@ cmc_status cmc_decode_step_ragged(const float *q,
                                   float scale, float *out,
                                   void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * cmc_decode_step without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the arrival counters and split partials live in a
+ * fixed 4 MiB array inside the library (one per GPU, held until the process
+ * ends).  The call itself allocates nothing; the caller still passes every
+ * input and output.  Same arguments as cmc_decode_step minus the workspace,
+ * same kernels, results identical to cmc_decode_step.
+ *
+ * Limits (else CMC_ERR_UNSUPPORTED, nothing enqueued): B + B*Hkv <= 16384
+ * arrival counters, and the split partials of the launch plan within the
+ * rest of the array (about 4 MiB: e.g. the 8-pair Llama-layer step needs
+ * 0.23 MiB; plans with one workgroup per (sequence, kv head) pair need none).
+ * The first call on each device looks the array up and zeroes its counters
+ * with a small kernel on `stream`; make it outside graph capture.  Every call
+ * on one GPU shares that GPU's array: calls that may overlap in time (other
+ * streams, other threads, concurrent graph replays) race and must not be
+ * made.
+ */
+cmc_status cmc_decode_step_noalloc(const float *q,
+                                   const void *cme_k, const void *cme_v,
+                                   const int32_t *idx, int k,
+                                   void *win_k, void *win_v, int32_t *win_count, int W,
+                                   const void *new_k, const void *new_v, int T_new,
+                                   cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
+                                   float scale, float *out, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                             */
 /* ------------------------------------------------------------------------ */

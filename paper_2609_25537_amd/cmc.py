@@ -35,7 +35,7 @@ EXPORTED = [
     "cmc_window_start", "cmc_decode_workspace_bytes", "cmc_two_tier_decode", "cmc_decode_step",
     "cmc_two_tier_decode_ragged", "cmc_decode_step_ragged", "cmc_locate_window", "cmc_denoise_workspace_bytes",
     "cmc_denoise", "cmc_bridge_workspace_bytes", "cmc_memory_bridge", "cmc_status_string", "cmc_last_error",
-    "cmc_version",
+    "cmc_version", "cmc_decode_step_noalloc",
 ]
 
 
@@ -95,6 +95,9 @@ def lib() -> ctypes.CDLL:
         L.cmc_decode_step_ragged.argtypes = [P, P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
                                              ctypes.c_float, P, P, SZ, P]
         L.cmc_decode_step_ragged.restype = I
+        L.cmc_decode_step_noalloc.argtypes = [P, P, P, P, I, P, P, P, I, P, P, I, I, I, I, I, I, I,
+                                              ctypes.c_float, P, P]
+        L.cmc_decode_step_noalloc.restype = I
         L.cmc_status_string.argtypes = [I]
         L.cmc_status_string.restype = ctypes.c_char_p
         L.cmc_last_error.argtypes = []
@@ -416,9 +419,10 @@ def decode_workspace(B: int, Hq: int, Hkv: int, Dh: int, k: int, W: int, device)
                        device=device)
 
 
-def _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, workspace, W, k_len):
+def _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, workspace, W, k_len,
+                 noalloc=False):
     """Checks shared by the decode wrappers; returns the C call's sizes and
-    the (possibly allocated) out and workspace."""
+    the (possibly allocated) out and workspace (none with noalloc)."""
     import torch
     _need(q.dim() == 3 and q.is_contiguous() and q.dtype == torch.float32, "q must be contiguous fp32 [B][Hq][Dh]")
     B, Hq, Dh = q.shape
@@ -448,9 +452,11 @@ def _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v,
     if out is None:
         out = torch.empty((B, Hq, Dh), dtype=torch.float32, device=q.device)
     _need(out.shape == (B, Hq, Dh) and out.dtype == torch.float32 and out.is_contiguous(), "out [B][Hq][Dh] fp32")
-    if workspace is None:
-        workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = 0
+    if not noalloc:
+        if workspace is None:
+            workspace = decode_workspace(B, Hq, Hkv, Dh, k, W, q.device)
+        ws_bytes = workspace.numel() * workspace.element_size()
     win = ((_ptr(win_k), _ptr(win_v), _ptr(win_count)) if W > 0 else (None, None, None))
     new = ((_ptr(new_k), _ptr(new_v)) if W > 0 and new_k is not None else (None, None))
     return dict(B=B, Hq=Hq, Hkv=Hkv, Dh=Dh, N=N, W=int(W), T=T, win=win, new=new, out=out, workspace=workspace,
@@ -504,5 +510,19 @@ def cmc_decode_step_ragged(q, cme_k, cme_v, idx, k_len, k: int, win_k, win_v, wi
                                       *a["win"], a["W"], *a["new"], a["T"], a["dtype"], a["B"], a["Hq"], a["Hkv"],
                                       a["Dh"], a["N"], float(scale), _ptr(a["out"]), _ptr(a["workspace"]),
                                       a["ws_bytes"], _stream(stream))
+    _check(rc)
+    return a["out"]
+
+
+def cmc_decode_step_noalloc(q, cme_k, cme_v, idx, k: int, win_k, win_v, win_count, new_k, new_v, scale: float,
+                            out=None, W: Optional[int] = None, stream=None):
+    """cmc_decode_step without a workspace: the library's fixed scratch holds
+    the counters and split partials (no device allocation in the call; `out`
+    must then be passed by callers that cannot allocate)."""
+    a = _decode_args(q, cme_k, cme_v, idx, k, win_k, win_v, win_count, new_k, new_v, out, None, W, None,
+                     noalloc=True)
+    rc = lib().cmc_decode_step_noalloc(_ptr(q), _ptr(cme_k), _ptr(cme_v), _ptr(idx), int(k), *a["win"], a["W"],
+                                       *a["new"], a["T"], a["dtype"], a["B"], a["Hq"], a["Hkv"], a["Dh"], a["N"],
+                                       float(scale), _ptr(a["out"]), _stream(stream))
     _check(rc)
     return a["out"]

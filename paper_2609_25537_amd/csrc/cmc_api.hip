@@ -4,6 +4,7 @@
 // window.hip, enqueued on the caller's stream.
 #include <math.h>
 #include <algorithm>
+#include <mutex>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -394,12 +395,64 @@ size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W) 
 
 }  // extern "C"
 
+// ------------------------------------------------- no-allocation scratch
+//
+// cmc_decode_step_noalloc keeps its arrival counters and split partials in
+// this file-scope device array instead of a caller workspace.  Layout:
+// [arrival counters, kNoAllocCounterBytes | split partials].  The counter
+// region never holds anything else, so it is zero at the start of every
+// call: the array is zero when the code object is loaded, the first call on
+// a device zeroes the region once more (a fill kernel on its stream), and
+// every call re-arms the counters it used before it ends.  Each GPU holds
+// its own copy until the process ends; host code reaches it only through
+// the address hipGetSymbolAddress returns for the current device.
+namespace {
+constexpr size_t kNoAllocCounterBytes = size_t(64) << 10;  // up to 16384 counters: B + B*Hkv
+constexpr size_t kNoAllocBytes = size_t(4) << 20;
+constexpr int kNoAllocMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
 namespace {
 
+__global__ void zero_words_kernel(uint32_t *p, unsigned n) {
+    for (unsigned i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kNoAllocMaxDevices];
+
+// The current device's address of `scratch`, set up on the first call on
+// that device (symbol lookup, then the counters zeroed on `stream`).
+cmc_status noalloc_scratch(const char *fn, hipStream_t stream, char **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kNoAllocMaxDevices)
+        return fail(CMC_ERR_UNSUPPORTED, "%s: device %d beyond the %d supported", fn, dev, kNoAllocMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(CMC_ERR_HIP, "%s: hipGetSymbolAddress returned a null address", fn);
+        zero_words_kernel<<<16, 256, 0, stream>>>(static_cast<uint32_t *>(ptr), (unsigned)(kNoAllocCounterBytes / 4));
+        e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "zeroing the scratch counters");
+        g_scratch_ptr[dev] = static_cast<char *>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return CMC_OK;
+}
+
+// The decode calls.  With noalloc, `workspace` is ignored and the counters
+// and partials live in `scratch` (sizes beyond it are rejected).
 cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
                        const int32_t *k_len, int k, void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
                        const void *new_v, int T_new, cmc_dtype kv_dtype, int B, int Hq, int Hkv, int Dh, int N,
-                       float scale, float *out, void *workspace, size_t workspace_bytes, void *stream) {
+                       float scale, float *out, void *workspace, size_t workspace_bytes, void *stream,
+                       bool noalloc = false) {
     if (kv_dtype != CMC_F32 && kv_dtype != CMC_BF16)
         return fail(CMC_ERR_UNSUPPORTED, "%s: unknown kv_dtype %d", fn, (int)kv_dtype);
     if (B < 0 || Hq < 1 || Hkv < 1 || k < 0 || W < 0 || N < 0)
@@ -431,10 +484,26 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
         misaligned(new_k) || misaligned(new_v))
         return fail(CMC_ERR_UNSUPPORTED, "%s: every pointer must be 16-byte aligned", fn);
     const cmc::DecodePlan pl = cmc::plan_decode(B, Hq, Hkv, Dh, k, W);
-    if (!workspace || workspace_bytes < pl.total)
-        return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "%s: workspace of %zu bytes needed, %zu given", fn, pl.total,
-                    workspace ? workspace_bytes : (size_t)0);
-    char *ws = static_cast<char *>(workspace);
+    char *counters, *partials;
+    if (noalloc) {
+        const size_t nctr = ((size_t)B + (size_t)B * Hkv) * sizeof(unsigned);
+        if (nctr > kNoAllocCounterBytes || pl.ml_bytes + pl.acc_bytes > kNoAllocBytes - kNoAllocCounterBytes)
+            return fail(CMC_ERR_UNSUPPORTED,
+                        "%s: these sizes need %zu counter bytes (at most %zu) and %zu partial bytes (at most %zu) "
+                        "of the library's fixed scratch; use cmc_decode_step with a workspace",
+                        fn, nctr, kNoAllocCounterBytes, pl.ml_bytes + pl.acc_bytes,
+                        kNoAllocBytes - kNoAllocCounterBytes);
+        char *base = nullptr;
+        if (cmc_status st = noalloc_scratch(fn, static_cast<hipStream_t>(stream), &base)) return st;
+        counters = base;
+        partials = base + kNoAllocCounterBytes;
+    } else {
+        if (!workspace || workspace_bytes < pl.total)
+            return fail(CMC_ERR_WORKSPACE_TOO_SMALL, "%s: workspace of %zu bytes needed, %zu given", fn, pl.total,
+                        workspace ? workspace_bytes : (size_t)0);
+        counters = static_cast<char *>(workspace);
+        partials = counters + pl.counter_bytes;
+    }
     cmc::DecodeParams p{};
     p.q = q;
     p.cme_k = cme_k;
@@ -447,10 +516,10 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     p.new_k = T_new > 0 ? new_k : nullptr;
     p.new_v = T_new > 0 ? new_v : nullptr;
     p.out = out;
-    p.seq_counter = reinterpret_cast<unsigned *>(ws);
-    p.pair_counter = reinterpret_cast<unsigned *>(ws) + B;
-    p.part_ml = reinterpret_cast<float *>(ws + pl.counter_bytes);
-    p.part_acc = reinterpret_cast<float *>(ws + pl.counter_bytes + pl.ml_bytes);
+    p.seq_counter = reinterpret_cast<unsigned *>(counters);
+    p.pair_counter = reinterpret_cast<unsigned *>(counters) + B;
+    p.part_ml = reinterpret_cast<float *>(partials);
+    p.part_acc = reinterpret_cast<float *>(partials + pl.ml_bytes);
     p.k = k;
     p.W = W;
     p.B = B;
@@ -492,6 +561,17 @@ cmc_status cmc_decode_step(const float *q, const void *cme_k, const void *cme_v,
         return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step: need 1 <= T_new <= W (got T_new=%d W=%d)", T_new, W);
     return decode_impl("decode_step", q, cme_k, cme_v, idx, nullptr, k, win_k, win_v, win_count, W, new_k, new_v, T_new,
                        kv_dtype, B, Hq, Hkv, Dh, N, scale, out, workspace, workspace_bytes, stream);
+}
+
+cmc_status cmc_decode_step_noalloc(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,
+                                   int k, void *win_k, void *win_v, int32_t *win_count, int W, const void *new_k,
+                                   const void *new_v, int T_new, cmc_dtype kv_dtype, int B, int Hq, int Hkv,
+                                   int Dh, int N, float scale, float *out, void *stream) {
+    if (W > 0 && T_new < 1)
+        return fail(CMC_ERR_INVALID_ARGUMENT, "decode_step_noalloc: need 1 <= T_new <= W (got T_new=%d W=%d)",
+                    T_new, W);
+    return decode_impl("decode_step_noalloc", q, cme_k, cme_v, idx, nullptr, k, win_k, win_v, win_count, W, new_k,
+                       new_v, T_new, kv_dtype, B, Hq, Hkv, Dh, N, scale, out, nullptr, 0, stream, true);
 }
 
 cmc_status cmc_two_tier_decode_ragged(const float *q, const void *cme_k, const void *cme_v, const int32_t *idx,

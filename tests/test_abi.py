@@ -313,3 +313,28 @@ def test_gather_validation(kw, code):
 
 def test_gather_empty_ok():
     assert _gather(B=0) == cmc.CMC_OK and _gather(k=0) == cmc.CMC_OK
+
+
+def _noalloc(**kw):
+    a = dict(q=FAKE, ck=FAKE, cv=FAKE, idx=FAKE, k=4, wk=FAKE, wv=FAKE, wc=FAKE, W=8, nk=FAKE, nv=FAKE, T=1,
+             dt=cmc.CMC_BF16, B=1, Hq=8, Hkv=2, Dh=128, N=16, scale=0.1, out=FAKE, s=None)
+    a.update(kw)
+    return cmc.lib().cmc_decode_step_noalloc(*a.values())
+
+
+@pytest.mark.parametrize("kw", [
+    dict(B=4096, Hkv=8, Hq=32),                            # 36864 arrival counters > 16384
+    dict(B=2, Hkv=16, Hq=128, Dh=256, k=0, W=200000),      # split partials beyond the fixed array
+])
+def test_noalloc_rejects_sizes_beyond_its_scratch(kw):
+    """The no-allocation decode step refuses sizes its fixed scratch cannot
+    hold, before touching the GPU."""
+    assert _noalloc(**kw) == cmc.CMC_ERR_UNSUPPORTED
+    assert "scratch" in cmc.last_error()
+
+
+def test_noalloc_validates_like_decode_step():
+    assert _noalloc(T=0) == cmc.CMC_ERR_INVALID_ARGUMENT
+    assert _noalloc(Dh=96) == cmc.CMC_ERR_UNSUPPORTED
+    assert _noalloc(B=0) == cmc.CMC_OK
+
