@@ -424,6 +424,43 @@ def batched_leg(name: str, dev, reps: int = 512, P: int = 4):
             "tokens_per_s_all_layers": round(w.B / (L * t), 1)}
 
 
+def selection_leg(name: str, dev, reps: int = 5):
+    """Tier-1 selection (score pass + top-k, once per question) of a batched
+    workload with fp32 keys and with the same keys rounded to bf16
+    (key_dtype CMC_BF16): ms per call and the score pass's key bytes per ms.
+    Keys and questions are drawn on the device."""
+    import torch
+    from paper_2609_25537_amd import cmc
+    from paper_2609_25537_amd import workloads as wl
+    w = wl.get(name)
+    keys = wl.device_normal(w.seed, "sel_keys", (0,), (w.B, w.N, w.D), 1.0, dev, torch.float32)
+    qv = wl.device_normal(w.seed, "q_vec", (0,), (w.B, w.D), 1.0, dev, torch.float32)
+    idx = torch.empty((w.B, w.k), dtype=torch.int32, device=dev)
+    ws = torch.empty(max(1, cmc.cmc_select_workspace_bytes(w.B, w.N)), dtype=torch.uint8, device=dev)
+    res = {"workload": w.name, "B": w.B, "N": w.N, "D": w.D, "k": w.k}
+    for tag, kt in (("fp32_keys", keys), ("bf16_keys", None)):
+        if kt is None:
+            kt = keys.to(torch.bfloat16)
+            del keys
+        cmc.cmc_select_cmes(kt, qv, w.k, idx_out=idx, workspace=ws)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            cmc.cmc_select_cmes(kt, qv, w.k, idx_out=idx, workspace=ws)
+        b.record()
+        b.synchronize()
+        ms = a.elapsed_time(b) / reps
+        nbytes = kt.numel() * kt.element_size()
+        res[tag] = {"ms": round(ms, 4), "key_bytes": nbytes, "GBs": round(nbytes / ms / 1e6, 1),
+                    "frac_of_hbm_peak": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}
+        del kt
+    del qv, idx, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_stack(args, w, dev):
     """A decoder stack of w.layers layers sharing one index list: one pass is
     the selection plus w.steps decode steps, each running the two-tier decode
@@ -654,12 +691,13 @@ def main():
                 # cache-resident latency, not an HBM bandwidth claim
                 "cache_resident": nbytes * w.layers < LLC_BYTES}
 
-    batched = None
+    batched = selection = None
     if args.batched == "on" or (args.batched == "auto" and w.name == "llama3_8b_layer"):
         del inp, graph
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         batched = [batched_leg("llama_stack32", dev), batched_leg("mistral7b_batch64_x8", dev)]
+        selection = selection_leg("mistral7b_batch64", dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -692,6 +730,9 @@ def main():
         # the >= 70% HBM figures at the Llama/Mistral head geometry (Hq 32, Hkv 8, Dh 128): batched
         # launches whose bytes between reuses exceed the last-level cache
         line["batched"] = batched
+        # the once-per-question selection of the Mistral-shaped batch (4.29 GB of fp32 keys), and the
+        # same keys in bf16
+        line["batched_selection"] = selection
     txt = json.dumps(line)
     print(txt, flush=True)
     if args.out:
@@ -910,11 +951,12 @@ def main_bridge(args, w, dev):
     h = to_dev(wl.bridge_h(w), dev)
     d = {k: to_dev(v, dev) for k, v in p.items()}
     out = torch.empty((w.M, w.Hd), dtype=torch.float32, device=dev)
+    h_norms = torch.empty((w.M,), dtype=torch.float32, device=dev)  # the CME norms localization ranks
     ws = torch.empty(cmc.cmc_bridge_workspace_bytes(w.M, w.F), dtype=torch.uint8, device=dev)
 
     def call():
         cmc.cmc_memory_bridge(h, d["w1"], d["b1"], d["w2"], d["b2"], d["gamma"], d["beta"], w.nu, w.eps, out=out,
-                              workspace=ws)
+                              h_norms_out=h_norms, workspace=ws)
 
     reps = max(1, args.launch_reps // 50)
     g = capture(lambda: [call() for _ in range(reps)])
@@ -942,7 +984,8 @@ def main_bridge(args, w, dev):
         "config": {"workload": w.name, "M": w.M, "Hc": w.Hc, "F": w.F, "Hd": w.Hd, "nu": w.nu, "graph": True},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
-                     "kernel": "gemm_nt_kernel x2 + bridge_norm_kernel (one cmc_memory_bridge call)",
+                     "kernel": "cme_norm_kernel + gemm_nt_kernel x2 + bridge_norm_kernel (one cmc_memory_bridge "
+                               "call, CME norms included)",
                      "flops_per_launch": flops, "launch_us": round(t_call * 1e6, 3)},
         "cpu_baseline": cpu,
     }
