@@ -310,7 +310,7 @@ class Oracle:
         ..., n_b + q_b - 1 (q_b clamped into [0, idx_stride - k_b]), then -1
         up to idx_stride.  Returns (idx [B][idx_stride] int32, k_out [B] =
         k_b + q_b)."""
-        keys = np.ascontiguousarray(sel_keys, np.float32)
+        keys, _ = _keys(sel_keys)
         B, N, D = keys.shape
         stride = k if idx_stride is None else int(idx_stride)
         idx = np.full((B, stride), -1, np.int32)

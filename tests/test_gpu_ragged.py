@@ -54,6 +54,18 @@ def test_select_ragged_sizes(orc, B, N, D, k, stride, n_list, q_list):
     _check_select_ragged(orc, keys, qv, n_rows, k, q_rows, stride, "sizes")
 
 
+@pytest.mark.parametrize("B,N,D,k,stride,n_list,q_list", [
+    (4, 100, 8, 10, 16, [100, 37, 5, 0], [0, 3, 6, 16]),
+    (3, 4096, 64, 512, 560, [4096, 1000, 511], [48, 8, 20]),
+])
+def test_select_ragged_bf16_keys(orc, B, N, D, k, stride, n_list, q_list):
+    """bf16 selection keys through the ragged call (same bits on both sides;
+    rounding merges close keys into exact ties, resolved to the lower row)."""
+    keys, qv = _separated(B, N, D, seed=N + k + stride + 1)
+    _check_select_ragged(orc, wl.f32_to_bf16_bits(keys), qv, np.array(n_list, np.int32), k,
+                         np.array(q_list, np.int32), stride, "bf16 keys")
+
+
 def test_select_ragged_ties(orc):
     keys, qv = _separated(3, 1000, 8, seed=11, dup_every=4)
     _check_select_ragged(orc, keys, qv, np.array([1000, 401, 77], np.int32), 100,

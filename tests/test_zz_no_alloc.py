@@ -59,3 +59,51 @@ def test_noalloc_matches_workspace_path(orc):
     _both(orc, big, "first call, Llama-layer shape")
     _both(orc, small, "second call, smaller input")
     _both(orc, big, "third call, first shape again")
+
+
+def test_noalloc_under_graph_capture(orc):
+    """The callers it is for: three fused decode steps captured into a HIP
+    graph (after one set-up call outside capture), the graph replayed four
+    times with eager work in between; after every replay the outputs and the
+    ring equal the same three steps run eagerly through cmc_decode_step with
+    a workspace from the same state."""
+    c = _case(3, B=1, Hq=32, Hkv=8, Dh=128, N=2048, k=256, W=512, fill=300)  # split plan: partials in the array
+    rng = np.random.default_rng(33)
+    steps = 3
+    qs = [to_dev((rng.standard_normal(c["q"].shape) / 11.3).astype(np.float32)) for _ in range(steps)]
+    nks = [to_dev(wl.f32_to_bf16_bits((rng.standard_normal(c["nk"].shape) / 11.3).astype(np.float32)))
+           for _ in range(steps)]
+    nvs = [to_dev(wl.f32_to_bf16_bits((rng.standard_normal(c["nv"].shape) / 11.3).astype(np.float32)))
+           for _ in range(steps)]
+    pk, pv, idx = to_dev(c["pk"]), to_dev(c["pv"]), to_dev(c["idx"])
+    ring_g = [to_dev(c["wk"]), to_dev(c["wv"]), to_dev(c["cnt"])]
+    ring_e = [t.clone() for t in ring_g]
+    outs_g = [torch.empty((1, 32, 128), dtype=torch.float32, device=DEV) for _ in range(steps)]
+    outs_e = [torch.empty_like(o) for o in outs_g]
+    # set-up call outside capture (its result is discarded; the rings are re-copied below)
+    scratch_ring = [t.clone() for t in ring_g]
+    cmc.cmc_decode_step_noalloc(qs[0], pk, pv, idx, c["k"], *scratch_ring, nks[0], nvs[0], c["scale"],
+                                out=outs_g[0])
+    torch.cuda.synchronize()
+    say("noalloc graph: capturing")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for t in range(steps):
+            cmc.cmc_decode_step_noalloc(qs[t], pk, pv, idx, c["k"], *ring_g, nks[t], nvs[t], c["scale"],
+                                        out=outs_g[t])
+    torch.cuda.synchronize()
+    ws = cmc.decode_workspace(1, 32, 8, 128, c["k"], c["W"], DEV)
+    for r in range(4):
+        say(f"noalloc graph: replay {r}")
+        g.replay()
+        for t in range(steps):
+            cmc.cmc_decode_step(qs[t], pk, pv, idx, c["k"], *ring_e, nks[t], nvs[t], c["scale"], out=outs_e[t],
+                                workspace=ws)
+        torch.cuda.synchronize()
+        for t in range(steps):
+            assert torch.equal(outs_g[t], outs_e[t]), f"replay {r} step {t}: output"
+        for x, y in zip(ring_g, ring_e):
+            assert torch.equal(x, y), f"replay {r}: ring state"
+        a = torch.randn(256, 256, device=DEV)
+        (a @ a).sum().item()
+
