@@ -51,7 +51,16 @@
 extern "C" {
 #endif
 
-typedef enum cmc_status {
+/* Both enums are int-sized.  In C++ they are declared with int as their
+ * underlying type, so that any int a caller passes (an unknown dtype, say)
+ * is a valid value the library can reject, rather than undefined behaviour. */
+#ifdef __cplusplus
+#define CMC_ENUM_INT : int
+#else
+#define CMC_ENUM_INT
+#endif
+
+typedef enum cmc_status CMC_ENUM_INT {
     CMC_OK = 0,
     CMC_ERR_INVALID_ARGUMENT = 1,   /* shape/value out of the documented range   */
     CMC_ERR_UNSUPPORTED = 2,        /* valid but not implemented (dtype, Dh, G, alignment) */
@@ -59,7 +68,7 @@ typedef enum cmc_status {
     CMC_ERR_HIP = 4                 /* a HIP runtime call or launch failed        */
 } cmc_status;
 
-typedef enum cmc_dtype {
+typedef enum cmc_dtype CMC_ENUM_INT {
     CMC_F32 = 0,
     CMC_BF16 = 1
 } cmc_dtype;
