@@ -433,12 +433,28 @@ __global__ __launch_bounds__(256) void cme_norm_kernel(const uint16_t *h, int M,
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= M) return;  // wave-uniform; no barriers
     const uint4 *h4 = reinterpret_cast<const uint4 *>(h + (size_t)row * Hc);
+    // Lane l sums the squares of 16-byte chunks l, l + 64, ... in that order
+    // (one fma chain); up to kGroup chunks are requested before any is used,
+    // so a row of up to 4096 elements costs one memory round trip.
+    constexpr int kGroup = 8;
+    const int chunks = Hc / 8;
     float s = 0.f;
-    for (int c = lane; c < Hc / 8; c += kWave) {
-        float x[8];
-        Vec16<uint16_t>::widen(h4[c], x);
+    for (int c0 = 0; c0 < chunks; c0 += kGroup * kWave) {
+        uint4 v[kGroup];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s = fmaf(x[e], x[e], s);
+        for (int i = 0; i < kGroup; ++i) {
+            const int c = c0 + lane + i * kWave;
+            v[i] = c < chunks ? h4[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+            if (c0 + lane + i * kWave < chunks) {
+                float x[8];
+                Vec16<uint16_t>::widen(v[i], x);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) s = fmaf(x[e], x[e], s);
+            }
+        }
     }
     s = lane_reduce<OpSum, 1, kWave>(s);
     if (lane == 0) norms[row] = sqrtf(s);
