@@ -89,6 +89,7 @@ def test_select_exact_ties(orc, N, k):
 
 @pytest.mark.parametrize("B,N,D,k,dup", [
     (1, 7, 8, 3, 0), (3, 33, 16, 5, 0), (4, 4096, 64, 512, 6), (1, 32768, 8, 1024, 0), (2, 2047, 264, 1, 4),
+    (3, 30001, 64, 700, 5),  # >= 65536 rows: the large-batch launch (eight rows per wave), ragged last block
 ])
 def test_select_bf16_keys(orc, B, N, D, k, dup):
     """bf16 selection keys (key_dtype = CMC_BF16) against the oracle on the

@@ -57,6 +57,8 @@ def test_select_ragged_sizes(orc, B, N, D, k, stride, n_list, q_list):
 @pytest.mark.parametrize("B,N,D,k,stride,n_list,q_list", [
     (4, 100, 8, 10, 16, [100, 37, 5, 0], [0, 3, 6, 16]),
     (3, 4096, 64, 512, 560, [4096, 1000, 511], [48, 8, 20]),
+    # >= 65536 rows (the large-batch launch): counts ending inside a wave's rows
+    (3, 25003, 32, 400, 420, [25003, 12345, 7], [0, 20, 5]),
 ])
 def test_select_ragged_bf16_keys(orc, B, N, D, k, stride, n_list, q_list):
     """bf16 selection keys through the ragged call (same bits on both sides;
