@@ -64,6 +64,7 @@ def _separated(B, N, D, seed, dup_every=0):
 @pytest.mark.parametrize("B,N,D,k", [
     (1, 1, 4, 1), (1, 7, 8, 0), (1, 7, 8, 7), (3, 33, 12, 5), (2, 1000, 64, 999),
     (4, 4096, 16, 512), (1, 32768, 8, 1024), (2, 32768, 8, 32768), (5, 2047, 260, 1),
+    (65535, 6, 8, 2),  # the largest batch the host accepts (one grid row per sequence)
 ])
 def test_select_sizes(orc, B, N, D, k):
     keys, qv = _separated(B, N, D, seed=N + k)
@@ -89,7 +90,7 @@ def test_select_exact_ties(orc, N, k):
 
 @pytest.mark.parametrize("B,N,D,k,dup", [
     (1, 7, 8, 3, 0), (3, 33, 16, 5, 0), (4, 4096, 64, 512, 6), (1, 32768, 8, 1024, 0), (2, 2047, 264, 1, 4),
-    (3, 30001, 64, 700, 5),  # >= 65536 rows: the large-batch launch (eight rows per wave), ragged last block
+    (3, 30001, 64, 700, 5),  # >= 65536 rows: the large-batch launch (four rows per wave), ragged last block
 ])
 def test_select_bf16_keys(orc, B, N, D, k, dup):
     """bf16 selection keys (key_dtype = CMC_BF16) against the oracle on the
@@ -436,3 +437,13 @@ def test_tiny_workload_end_to_end(orc):
         torch.cuda.synchronize()
         assert max_abs(to_host(out), ref) <= 1e-5, t
     assert (to_host(d_wk) == wk).all() and (to_host(d_wc) == cnt).all()
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("B,Hq,Hkv,dtype", [(65535, 2, 1, "bf16"), (1, 65535, 65535, "f32")])
+def test_decode_grid_limits(orc, B, Hq, Hkv, dtype):
+    """The largest batch and the largest kv-head count the host accepts
+    (65535 each: one grid dimension per sequence / kv head), fused append
+    and decode, every output checked."""
+    _decode_case(orc, B=B, Hq=Hq, Hkv=Hkv, Dh=64, N=3, k=2, W=3, fill=2, dtype=dtype, seed=B + Hkv, steps=2,
+                 fused=True)
