@@ -392,9 +392,11 @@ cmc_status cmc_two_tier_decode(const float *q,
  * One whole decode step in a single launch: the ring append of
  * cmc_window_append (new_k/new_v [B][Hkv][T_new][Dh], 1 <= T_new <= W and
  * T_new <= 65535, else CMC_ERR_UNSUPPORTED) followed by cmc_two_tier_decode
- * over the updated cache.  Results (out, the
- * ring contents and win_count) are identical to calling the two in that
- * order.  With W == 0 there is no Tier-2 and new_k/new_v are ignored.
+ * over the updated cache.  The ring contents and win_count are identical
+ * to calling the two in that order, and out is the same attention over the
+ * same keys (the appended rows are taken in their own phase, so out may
+ * differ from the two calls' in the last bits, within the same accuracy).
+ * With W == 0 there is no Tier-2 and new_k/new_v are ignored.
  * Same arguments, limits and workspace as cmc_two_tier_decode otherwise.
  */
 cmc_status cmc_decode_step(const float *q,
