@@ -373,7 +373,10 @@ size_t cmc_decode_workspace_bytes(int B, int Hq, int Hkv, int Dh, int k, int W);
  *              zero-filled before first use (see cmc_decode_workspace_bytes)
  *
  * Limits: Hq % Hkv == 0 with Hq/Hkv in {1, 2, 4, 8}; Dh in {64, 128, 256};
- * 0 <= k <= N when idx == NULL; k + W >= 1; W >= 0.  Index values are not
+ * 0 <= k <= N when idx == NULL; k + W >= 1; W >= 0; B, Hkv <= 65535;
+ * k + W (+ T_new) <= INT_MAX; with bf16 K/V, N * Dh * 2 and W * Dh * 2 below
+ * 4 GiB (one (sequence, kv head)'s pool or ring); else CMC_ERR_UNSUPPORTED,
+ * nothing enqueued.  Index values are not
  * checked on the host; the device clamps them into [0, N-1], which keeps
  * memory access in bounds but makes the result meaningless.
  * Arithmetic: fp32 accumulation, fixed reduction order (run-to-run

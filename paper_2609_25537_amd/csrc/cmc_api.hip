@@ -2,6 +2,7 @@
 // launch planning and error reporting.  Everything here runs on the host;
 // every computation runs in the kernels of decode.hip, select.hip and
 // window.hip, enqueued on the caller's stream.
+#include <limits.h>
 #include <math.h>
 #include <algorithm>
 #include <mutex>
@@ -471,6 +472,14 @@ cmc_status decode_impl(const char *fn, const float *q, const void *cme_k, const 
     if (T_new > cmc::kMaxAppendRows)
         return fail(CMC_ERR_UNSUPPORTED, "%s: T_new=%d exceeds %d rows per call", fn, T_new, cmc::kMaxAppendRows);
     if (B > 65535 || Hkv > 65535) return fail(CMC_ERR_UNSUPPORTED, "%s: B and Hkv must be <= 65535", fn);
+    // The kernel indexes a sequence's key list (k + W + T_new rows) with
+    // 32-bit integers, and a bf16 (sequence, kv head) pool or ring with
+    // 32-bit byte offsets from its base.
+    if ((long long)k + W + T_new > INT_MAX)
+        return fail(CMC_ERR_UNSUPPORTED, "%s: k + W + T_new = %lld exceeds %d", fn, (long long)k + W + T_new, INT_MAX);
+    if (kv_dtype == CMC_BF16 && ((long long)N * Dh * 2 > 0xFFFFFFFFLL || (long long)W * Dh * 2 > 0xFFFFFFFFLL))
+        return fail(CMC_ERR_UNSUPPORTED, "%s: a (sequence, kv head)'s pool (N=%d) or ring (W=%d) of bf16 rows of Dh=%d "
+                    "must stay under 4 GiB", fn, N, W, Dh);
     if (W == 0) T_new = 0;  // no Tier-2: appending is a no-op
     if (B == 0) return ok();
     if (!q || !out) return fail(CMC_ERR_INVALID_ARGUMENT, "%s: q and out must be non-null", fn);

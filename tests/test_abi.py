@@ -201,6 +201,21 @@ def test_decode_step_ragged_needs_new_rows():
     assert _dec_r(step=True, T=0) == cmc.CMC_ERR_INVALID_ARGUMENT
 
 
+def test_decode_offset_limits():
+    """A bf16 (sequence, kv head) pool or ring of 4 GiB or more, and key
+    lists longer than INT_MAX rows, are refused before anything is enqueued
+    (the kernel addresses them with 32-bit offsets and indices); fp32 pools
+    of that size are addressed in 64 bits and pass this check."""
+    big = (1 << 32) // (128 * 2)  # rows of Dh = 128 bf16 in 4 GiB
+    assert _dec_r(N=big) == cmc.CMC_ERR_UNSUPPORTED and "4 GiB" in cmc.last_error()
+    assert _dec_r(W=big) == cmc.CMC_ERR_UNSUPPORTED and "4 GiB" in cmc.last_error()
+    assert _dec_r(step=True, W=big) == cmc.CMC_ERR_UNSUPPORTED
+    assert _dec_r(N=big - 1, wsb=64) == cmc.CMC_ERR_WORKSPACE_TOO_SMALL  # just under: passes this check
+    assert _dec_r(dt=cmc.CMC_F32, N=big, wsb=64) == cmc.CMC_ERR_WORKSPACE_TOO_SMALL
+    assert _dec_r(dt=cmc.CMC_F32, k=2**31 - 8, W=8, N=2**31 - 1) == cmc.CMC_ERR_UNSUPPORTED
+    assert "INT_MAX" in cmc.last_error() or "2147483647" in cmc.last_error()
+
+
 def test_decode_step_append_row_limit():
     """At most 65535 rows appended per call (the launch packs T_new into 16
     bits); beyond that the call is refused before anything is enqueued."""
