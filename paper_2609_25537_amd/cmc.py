@@ -126,10 +126,15 @@ def _check(rc: int) -> None:
 
 
 def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (None and raw integer addresses pass
+    through).  Host tensors are refused: the kernels would take their
+    addresses as device memory."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not t.is_cuda:
+        raise ValueError(f"cmc: tensor of shape {tuple(t.shape)} is on {t.device}; the library takes device tensors")
     return t.data_ptr()
 
 

@@ -353,3 +353,16 @@ def test_noalloc_validates_like_decode_step():
     assert _noalloc(Dh=96) == cmc.CMC_ERR_UNSUPPORTED
     assert _noalloc(B=0) == cmc.CMC_OK
 
+
+
+def test_binding_refuses_host_tensors():
+    """A host tensor never reaches the library as an address (the kernels
+    would read it as device memory); the check runs before any call."""
+    import torch
+    q = torch.zeros((1, 4, 64), dtype=torch.float32)
+    pool = torch.zeros((1, 4, 8, 64), dtype=torch.float32)
+    with pytest.raises(ValueError, match="device tensors"):
+        cmc._ptr(q)
+    with pytest.raises((ValueError, RuntimeError)):
+        cmc.cmc_two_tier_decode(q, pool, pool, None, 4, None, None, None, 0.125, W=0,
+                                out=torch.zeros((1, 4, 64)), workspace=torch.zeros(1024, dtype=torch.uint8))
