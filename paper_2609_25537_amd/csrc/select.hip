@@ -131,7 +131,7 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / kWave;
-constexpr int kPerThread = kSelectMaxN / kTopkThreads;  // 32
+constexpr int kMaxPerThread = kSelectMaxN / kTopkThreads;  // 32
 
 // Block-wide sum of an integer count (< 2^24, exact in fp32); every thread
 // gets the same total.  `slot` alternates between two LDS rows so one barrier
@@ -165,13 +165,18 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *s_wave) {
     return base + x - v;
 }
 
+// PER keys per thread (a power of two, PER * 1024 >= N): the per-thread
+// loops run over PER registers only, so a batch of N = 4096 rows does an
+// eighth of the compares of the largest instantiation.
+template <int PER>
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
+    constexpr int kPerThread = PER;
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
     const int N = p.N;
     const int nb = p.n_rows ? clamp_count(p.n_rows[b], N) : N;  // candidates: rows [0, nb)
     const int k = min(p.k, nb);
-    const int per = (N + kTopkThreads - 1) / kTopkThreads;  // <= kPerThread
+    const int per = (N + kTopkThreads - 1) / kTopkThreads;  // <= PER
     const int j0 = tid * per;
     const int cnt = max(0, min(per, nb - j0));
 
@@ -318,7 +323,14 @@ hipError_t launch_select(const SelectParams &p, hipStream_t stream) {
         e = hipGetLastError();
     }
     if (e != hipSuccess || (p.idx_stride == 0 && !p.k_out)) return e;
-    topk_kernel<<<p.B, kTopkThreads, 0, stream>>>(p);
+    const int per = (p.N + kTopkThreads - 1) / kTopkThreads;
+    if (per <= 1) topk_kernel<1><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else if (per <= 2) topk_kernel<2><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else if (per <= 4) topk_kernel<4><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else if (per <= 8) topk_kernel<8><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else if (per <= 16) topk_kernel<16><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else if (per <= kMaxPerThread) topk_kernel<kMaxPerThread><<<p.B, kTopkThreads, 0, stream>>>(p);
+    else return hipErrorInvalidValue;  // N > kSelectMaxN is rejected by the host checks
     return hipGetLastError();
 }
 
