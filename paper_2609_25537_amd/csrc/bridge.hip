@@ -62,6 +62,36 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return x * (x >= 0.f ? 1.f - half_erfc : half_erfc);
 }
 
+// Build-time tuning knob: 1 evaluates the cap's tanh as below, 0 with the
+// library tanhf.
+#ifndef CMC_BRIDGE_FAST_TANH
+#define CMC_BRIDGE_FAST_TANH 1
+#endif
+
+// tanh for the cap, within 4 units of 2^-24 absolute everywhere:
+//   |x| <  0.625: x + x^3 P(x^2), P a cubic fitted here by weighted least
+//                 squares to (tanh(x)/x - 1)/x^2 (1.35 units in fp32 Horner);
+//   |x| >= 0.625: sign(x) (1 - 2 / (e^(2|x|) + 1)) with the hardware 2^y and
+//                 reciprocal (3.4 units with a 1-ulp error in each; e = inf
+//                 past |x| ~ 44 gives exactly 1; NaN stays NaN).
+// About fourteen instructions against about thirty for the library tanhf,
+// which made the row kernel VALU-bound.
+__device__ __forceinline__ float tanh_cap(float x) {
+#if CMC_BRIDGE_FAST_TANH
+    const float ax = fabsf(x);
+    if (ax < 0.625f) {
+        const float s = x * x;
+        const float q = fmaf(fmaf(fmaf(0.01489475928246975f, s, -0.05170630291104317f), s, 0.1330212950706482f), s,
+                             -0.3333188593387604f);
+        return fmaf(x * s, q, x);
+    }
+    const float e = __builtin_amdgcn_exp2f(ax * 2.8853900817779268f);  // e^(2|x|)
+    return copysignf(fmaf(-2.f, __builtin_amdgcn_rcpf(e + 1.f), 1.f), x);
+#else
+    return tanhf(x);
+#endif
+}
+
 // Two fp32 values -> packed bf16 (low half first), round to nearest even
 // (one v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -353,10 +383,10 @@ __global__ __launch_bounds__(256) void bridge_norm_kernel(BridgeParams p) {
         const int c = lane + u * kWave;
         if (c < n4) {
             const float4 g = g4[c], b = b4[c];
-            v[u] = float4{p.nu * tanhf(fmaf(g.x * (v[u].x - mean), inv, b.x)),
-                          p.nu * tanhf(fmaf(g.y * (v[u].y - mean), inv, b.y)),
-                          p.nu * tanhf(fmaf(g.z * (v[u].z - mean), inv, b.z)),
-                          p.nu * tanhf(fmaf(g.w * (v[u].w - mean), inv, b.w))};
+            v[u] = float4{p.nu * tanh_cap(fmaf(g.x * (v[u].x - mean), inv, b.x)),
+                          p.nu * tanh_cap(fmaf(g.y * (v[u].y - mean), inv, b.y)),
+                          p.nu * tanh_cap(fmaf(g.z * (v[u].z - mean), inv, b.z)),
+                          p.nu * tanh_cap(fmaf(g.w * (v[u].w - mean), inv, b.w))};
             nn = fmaf(v[u].x, v[u].x, nn);
             nn = fmaf(v[u].y, v[u].y, nn);
             nn = fmaf(v[u].z, v[u].z, nn);
@@ -401,10 +431,10 @@ __global__ __launch_bounds__(256) void bridge_norm_wide_kernel(BridgeParams p) {
     const float inv = 1.f / sqrtf(var + p.eps);
     auto capped = [&](int c) {
         const float4 v = y4[c], g = g4[c], b = b4[c];
-        return float4{p.nu * tanhf(fmaf(g.x * (v.x - mean), inv, b.x)),
-                      p.nu * tanhf(fmaf(g.y * (v.y - mean), inv, b.y)),
-                      p.nu * tanhf(fmaf(g.z * (v.z - mean), inv, b.z)),
-                      p.nu * tanhf(fmaf(g.w * (v.w - mean), inv, b.w))};
+        return float4{p.nu * tanh_cap(fmaf(g.x * (v.x - mean), inv, b.x)),
+                      p.nu * tanh_cap(fmaf(g.y * (v.y - mean), inv, b.y)),
+                      p.nu * tanh_cap(fmaf(g.z * (v.z - mean), inv, b.z)),
+                      p.nu * tanh_cap(fmaf(g.w * (v.w - mean), inv, b.w))};
     };
     float nn = 0.f;
     for (int c = lane; c < n4; c += kWave) {
