@@ -9,8 +9,8 @@
 // norms are clamped to 1e-8, so a zero row scores 0.
 //
 // topk_kernel: one 1024-thread workgroup per sequence.  Scores become
-// order-preserving uint32 keys (kept in registers, 32 per thread, so N <=
-// 32768).  The k-th largest key T is found bit by bit from the top: T is the
+// order-preserving uint32 keys (kept in registers, ceil(N / 1024) per thread
+// rounded up to a power of two, at most 32, so N <= 32768).  The k-th largest key T is found bit by bit from the top: T is the
 // largest value with count(key >= T) >= k, one block-wide count per bit.
 // Then every key > T is taken, plus the first (k - count(key > T)) keys equal
 // to T in index order (ties go to the earlier document position).  Two
