@@ -81,3 +81,99 @@ def test_bridge_then_select(orc, B, N, Hc, F, Hd, k, nu):
     top = -np.sort(-ref_scores, axis=1)
     abs_gap = top[:, k - 1] - top[:, k]
     assert (np.abs(got_scores - ref_scores).max(axis=1) < 0.5 * abs_gap).all()
+
+
+def _stat_tol(H):
+    """fp32 bound on the Eq. 3 statistic (three H-term sums, |x.y| <= |x||y|)."""
+    u = 2.0 ** -24
+    return 3.0 * H * u / (1 - H * u) + 8 * u
+
+
+def _norm_rel_bound(H):
+    """Relative bound of the kernel's fp32 norm of an H-wide bf16 row (one fma
+    chain of ceil(H / 512) * 8 terms per lane, a 6-step butterfly, the root)."""
+    u = 2.0 ** -24
+    n = -(-H // 512) * 8 + 6
+    return 0.5 * n * u / (1 - n * u) + u
+
+
+def _linked_embeddings(seed, B, n, H, p_link):
+    """Token i continues token i - 1 (0.6 e + 0.8 z) with probability p_link,
+    else is fresh noise; bf16 bits."""
+    r = np.random.default_rng(seed)
+    z = r.standard_normal((B, n, H)).astype(np.float32)
+    link = r.random((B, n)) < p_link
+    e = np.empty_like(z)
+    e[:, 0] = z[:, 0]
+    for i in range(1, n):
+        e[:, i] = np.where(link[:, i, None], np.float32(0.6) * e[:, i - 1] + np.float32(0.8) * z[:, i], z[:, i])
+    return wl.f32_to_bf16_bits(e)
+
+
+def test_denoise_then_locate(orc):
+    """Denoising's chunk offsets (the position in C of each chunk's first
+    kept token) and the CME norms of those chunks' memory embeddings feed
+    CME-guided localization, all on the GPU; the oracle runs the same chain
+    on its fp64 statistic and norms.  The inputs are drawn until every Eq. 3
+    statistic lies further from tau than its fp32 bound, so both chains take
+    the same threshold decisions; kept sets and offsets must then be
+    bit-exact, and alpha / start too wherever a context's two largest norms
+    are further apart than their fp32 bound."""
+    B, n, H, g, tau, m, t, mc, W = 4, 1500, 256, 3, 0.05, 16, 64, 4, 128
+    n_tokens = np.array([1500, 1203, 777, 1399], np.int32)
+    tau32 = float(np.float32(tau))
+    tol = _stat_tol(H)
+    for seed in range(100):
+        emb = _linked_embeddings(seed, B, n, H, 0.3)
+        ref_stat = orc.denoise_scores(emb, g, n_tokens)
+        fin = np.isfinite(ref_stat)
+        if np.min(np.abs(ref_stat[fin] - tau32)) > tol:
+            break
+    else:
+        pytest.fail("no seed with every statistic resolved against tau")
+    ref = orc.denoise_select(ref_stat, tau32, m, n_tokens, t)
+    say(f"denoise -> locate: seed {seed}, kept {ref['kept_count'].tolist()}, chunks {ref['n_chunks'].tolist()}")
+
+    r = cmc.cmc_denoise(to_dev(emb), g=g, tau=tau, keep_min_every=m, n_tokens=to_dev(n_tokens), chunk_tokens=t)
+    torch.cuda.synchronize()
+    assert (to_host(r["kept_count"]) == ref["kept_count"]).all(), "kept counts differ"
+    assert (to_host(r["kept_idx"]) == ref["kept_idx"]).all(), "kept positions differ"
+    offsets = r["chunk_offset"]
+    assert (to_host(offsets) == ref["chunk_offset"]).all(), "chunk offsets differ"
+    assert (to_host(r["n_chunks"]) == ref["n_chunks"]).all()
+
+    # mc memory embeddings per chunk; their CME vectors' norms from the bridge
+    n_rows = (ref["n_chunks"] * mc).astype(np.int32)
+    N = int(offsets.shape[1]) * mc
+    Hc, F, Hd = 64, 128, 128
+    rng = np.random.default_rng(1000 + seed)
+    h32 = rng.standard_normal((B * N, Hc)).astype(np.float32)
+    h32 *= np.exp(rng.standard_normal((B * N, 1)) * 0.2).astype(np.float32)  # spread the norms
+    h = wl.f32_to_bf16_bits(h32)
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    bf = lambda a: to_dev(np.ascontiguousarray(a))
+    hn = torch.empty((B * N,), dtype=torch.float32, device=DEV)
+    cmc.cmc_memory_bridge(bf(h), bf(wl.f32_to_bf16_bits(f(F, Hc) / 8)), to_dev(f(F)), bf(wl.f32_to_bf16_bits(f(Hd, F) / 11)),
+                          to_dev(f(Hd)), to_dev(np.ones(Hd, np.float32)), to_dev(np.zeros(Hd, np.float32)), 1.0,
+                          h_norms_out=hn)
+    alpha, start = cmc.cmc_locate_window(hn.view(B, N), to_dev(n_tokens), W, mc, n_rows=to_dev(n_rows),
+                                         chunk_offset=offsets)
+    torch.cuda.synchronize()
+
+    got_n = to_host(hn).astype(np.float64).reshape(B, N)
+    ref_n = orc.row_norms(h).reshape(B, N)
+    rel = _norm_rel_bound(Hc)
+    assert (np.abs(got_n - ref_n) <= rel * ref_n).all()
+    ref_a, ref_s = orc.locate(ref_n, n_tokens, W, mc, n_rows=n_rows, chunk_offset=ref["chunk_offset"])
+    own_a, own_s = orc.locate(got_n, n_tokens, W, mc, n_rows=n_rows, chunk_offset=ref["chunk_offset"])
+    ga, gs = to_host(alpha), to_host(start)
+    resolved = np.zeros(B, bool)
+    for b in range(B):
+        top2 = -np.sort(-ref_n[b, :n_rows[b]])[:2]
+        resolved[b] = top2[0] - top2[1] > 2 * rel * top2[0]
+    assert resolved.any()
+    assert (ga[resolved] == ref_a[resolved]).all() and (gs[resolved] == ref_s[resolved]).all()
+    assert (ga == own_a).all() and (gs == own_s).all()
+    # alpha is a kept token's position: the first kept token of the chosen chunk
+    for b in range(B):
+        assert ga[b] in set(ref["kept_idx"][b, :ref["kept_count"][b]].tolist())
