@@ -236,41 +236,17 @@ struct RingCount {
     }
 };
 
-// Arrival on the sequence's counter once this wave's read of the ring count
-// has returned (the increments below depend on the value read, so they are
-// issued after it).  With `lds` set (an unsplit plan) the waves of the
-// workgroup first count themselves on a workgroup counter in LDS, and only
-// the last of them arrives on the sequence's counter: the arrival then
-// follows every count read of the workgroup, at the cost of one LDS atomic
-// per wave (a device-scope atomic from every wave would make each wave's
-// next load waits include that atomic's latency, since loads and atomics
-// return in order).  The returned value is read only when the count is
-// advanced, but the compiler waits for it where the branch ends, so callers
-// issue it next to loads they wait for anyway.  prev stays ~0u in lanes
-// that did not arrive.
-struct Arrival {
-    unsigned *ctrs;  // the sequence counters; the address is formed only in arrive(),
-    int b;           // so no wait for that kernel argument precedes the first loads
-    bool pending;    // wave-uniform
-    unsigned prev;
-    unsigned *lds;   // workgroup counter (zeroed before a barrier), or nullptr
-    unsigned nw;     // waves of the workgroup
-    __device__ __forceinline__ void arrive(int cnt_raw) {
-        if (pending) {
-            pending = false;
-            const unsigned one = (unsigned)(cnt_raw != INT_MIN);  // == 1, after the count load returned
-            const bool lane0 = (threadIdx.x & 63) == 0;
-            bool last = true;
-            if (lds) {
-                unsigned r = 0;
-                if (lane0) r = __hip_atomic_fetch_add(lds, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                last = __builtin_amdgcn_readfirstlane(r) == nw - 1;  // wave-uniform
-            }
-            if (last && lane0)
-                prev = __hip_atomic_fetch_add(ctrs + b, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
-};
+// One arrival on a counter (relaxed, agent scope) that returns the previous
+// value.  The address goes through a VGPR so that the compiler keeps it a
+// single returning atomic: its atomic optimizer would otherwise turn it into
+// a wave-wide scan that reads the result at once, and since loads and atomics
+// complete in order, that wait would also cover every load issued before.
+// As it is, the result is waited for only where it is used.
+__device__ __forceinline__ unsigned arrive_once(unsigned *ctrs, int i, unsigned one) {
+    int iv;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(iv) : "s"(i));
+    return __hip_atomic_fetch_add(ctrs + iv, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // --------------------------------------------------------------- MFMA loop
 //
@@ -406,7 +382,7 @@ template <int NW, int DH, int G, class Rows, bool RING_WRITE>
 __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh, int r0, int r1, Rows rows,
                                            const char *kbase, const char *vbase, char *ringK, char *ringV,
                                            QOperand<DH> &qo, RingCount &cnt, float *s_p,
-                                           WaveState<G, DH / 16> &st, Arrival &arr) {
+                                           WaveState<G, DH / 16> &st) {
     constexpr int SL = DH / 32, VD = DH / 16, RB = DH * 2;
     constexpr int VB = VD * 2;                 // bytes of V per lane per quarter: 8, 16 or 32
     constexpr int VW = VB >= 16 ? VB / 16 : 1; // 16-byte words (or one 8-byte word)
@@ -519,9 +495,9 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
     } while (0)
 
     // Once the wave's first K/V loads are in flight: fetch the ring count
-    // and q, split q (both round trips overlap the K/V loads'), arrive (an
-    // unsplit launch's workgroup completes its pair), then read the count
-    // into the masks and end the phase at the last filled ring slot.
+    // and q, split q (both round trips overlap the K/V loads'), then read the
+    // count into the masks and end the phase at the last filled ring slot
+    // (a phase without masks does not wait for the count).
 #define CMC_AFTER_FIRST_LOAD()                    \
     do {                                          \
         if (!qo.ready) {                          \
@@ -529,7 +505,6 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
             load_q_operand<DH, G>(p, b, kvh, qo.hi, qo.lo); \
             qo.ready = true;                      \
         }                                         \
-        arr.arrive(cnt.raw);                      \
         rows.resolve(cnt);                        \
         r1 = rows.limit(r1);                      \
     } while (0)
@@ -598,7 +573,7 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
 
 template <int NW, int DH, int G, bool IX>
 __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh, int kb, int c0, int c1,
-                                          RingCount &cnt, float *s_p, WaveState<G, DH / 16> &st, Arrival &arr) {
+                                          RingCount &cnt, float *s_p, WaveState<G, DH / 16> &st) {
     QOperand<DH> qo;
     qo.ready = false;
     const size_t head = (size_t)b * p.Hkv + kvh;
@@ -611,7 +586,7 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         const char *kb = static_cast<const char *>(p.cme_k) + head * (size_t)p.N * DH * 2;
         const char *vb = static_cast<const char *>(p.cme_v) + head * (size_t)p.N * DH * 2;
         mfma_phase<NW, DH, G, PoolRows<IX>, false>(p, b, kvh, c0, min(c1, pool_end), rows, kb, vb, nullptr, nullptr, qo,
-                                               cnt, s_p, st, arr);
+                                               cnt, s_p, st);
     }
     if (p.W > 0) {
         char *wk = static_cast<char *>(p.win_k) + head * (size_t)p.W * DH * 2;
@@ -619,14 +594,14 @@ __device__ __forceinline__ void mfma_loop(const DecodeParams &p, int b, int kvh,
         // the W ring slots in physical order, masked by the count
         const RingRows rr{pool_end, T_new, p.W};
         mfma_phase<NW, DH, G, RingRows, false>(p, b, kvh, max(c0, pool_end), min(c1, ring_end), rr, wk, wv, nullptr,
-                                               nullptr, qo, cnt, s_p, st, arr);
+                                               nullptr, qo, cnt, s_p, st);
         // rows appended in this call
         if (T_new > 0) {
             const NewRows nr{ring_end, p.W};
             const char *nk = static_cast<const char *>(p.new_k) + head * (size_t)T_new * DH * 2;
             const char *nv = static_cast<const char *>(p.new_v) + head * (size_t)T_new * DH * 2;
             mfma_phase<NW, DH, G, NewRows, true>(p, b, kvh, max(c0, ring_end), c1, nr, nk, nv, wk, wv, qo, cnt, s_p,
-                                                 st, arr);
+                                                 st);
         }
     }
     // Wave totals: l over the 16 keys of one lane row (rows hold copies),
@@ -836,40 +811,35 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
     const RowMap<T> rm = make_rowmap<T>(p, b, kvh, DH, kb, slot0, min(cnt0, p.W));
 
     // Ring count.  It may be advanced only after every wave of the
-    // sequence's workgroups has read it, so one arrival per (sequence, kv
-    // head) pair on the sequence's counter follows all of that pair's reads:
-    //   S == 1: each wave, once its own count load has returned (in its first
-    //     block, or after the loop if it had none), counts itself on the
-    //     workgroup's LDS counter; the last wave arrives for the pair;
-    //   S > 1: each split arrives on its pair counter after a barrier that
-    //     follows every count read of its workgroup; the merging workgroup
-    //     (the last split of the pair) then arrives for the pair.
+    // sequence's workgroups has read it.  Each wave stores the count it read
+    // into LDS before the barrier that ends its walk (a store of the loaded
+    // value, so the read has returned by then); after that barrier one
+    // arrival per (sequence, kv head) pair goes to the sequence's counter:
+    //   S == 1: thread 0 of the workgroup, right after the barrier;
+    //   S > 1: each split arrives on its pair counter after that barrier, and
+    //     the merging workgroup (the last split of the pair) then arrives for
+    //     the pair, overlapping its merge loads.
     // The last of the Hkv arrivals writes the advanced count and re-arms the
-    // counter, at its workgroup's end.  No data is published through the
-    // counter, so no fence is needed.
+    // counter, at its workgroup's end (the arrival's value is waited for only
+    // there).  No data is published through the counter, so no fence is
+    // needed.
     const bool bump = p.T_new > 0 && p.W > 0;
-    __shared__ unsigned s_reads;
-    if (bump && p.S == 1) {  // launch-uniform
-        if (threadIdx.x == 0) s_reads = 0u;
-        __syncthreads();
-    }
-    Arrival arr{p.seq_counter, b, bump && p.S == 1, ~0u, p.S == 1 ? &s_reads : nullptr, (unsigned)NW};
+    unsigned prev = ~0u;  // the sequence counter before this workgroup's arrival (one lane)
 
     WaveState<G, VEC> st;
     st.init();
     if constexpr (MF) {
         __shared__ float s_pw[NW][16 * G];
-        mfma_loop<NW, DH, G, IX>(p, b, kvh, kb, c0, c1, cnt, s_pw[threadIdx.x >> 6], st, arr);
+        mfma_loop<NW, DH, G, IX>(p, b, kvh, kb, c0, c1, cnt, s_pw[threadIdx.x >> 6], st);
     } else {
         constexpr int U = (sizeof(T) == 2 && DH >= 128) ? 4 : 2;
         valu_loop<NW, T, DH, G, U>(p, rm, b, kvh, c0, c1, st);
     }
     if (p.W > 0) cnt.load(p.win_count, b);  // a wave without K/V rows
-    arr.arrive(cnt.raw);                     // S == 1 and no K/V rows (or the VALU path)
     const int cnt_now = MF ? cnt.value() : cnt0;
 #define CMC_BUMP()                                                                         \
     do {                                                                                 \
-        if (bump && arr.prev == (unsigned)(p.Hkv - 1)) { /* one lane per sequence */   \
+        if (bump && prev == (unsigned)(p.Hkv - 1)) { /* one lane per sequence */       \
             p.win_count[b] = cnt_now + p.T_new;                                          \
             __hip_atomic_store(&p.seq_counter[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
         }                                                                                \
@@ -895,12 +865,16 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
             s_l[wave][g] = st.l[g];
         }
     }
+    __shared__ int s_cnt[NW];
+    if (bump && lane == 0) s_cnt[wave] = cnt.raw;  // stored once the wave's count read has returned
     __syncthreads();
 
     const size_t head = (size_t)b * p.Hkv + kvh;
     float *outp = p.out + ((size_t)b * p.Hq + (size_t)kvh * G) * DH;
     __shared__ int s_last;
     if (p.S == 1) {
+        // every wave's count read returned before the barrier above
+        if (bump && threadIdx.x == 0) prev = arrive_once(p.seq_counter, b, (unsigned)(s_cnt[NW - 1] != INT_MIN));
         for (int t = threadIdx.x; t < G * DH; t += kThreads) {
             const int g = t / DH, d = t % DH;
             float num, den;
@@ -954,8 +928,8 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
             s_ml[2 * t] = v.x;
             s_ml[2 * t + 1] = v.y;
         }
-        arr.pending = bump && wave == 0;
-        arr.arrive(cnt.raw);  // this workgroup completes the pair; overlaps the merge loads
+        // this workgroup completes the pair; the arrival overlaps the merge loads
+        if (bump && threadIdx.x == 0) prev = arrive_once(p.seq_counter, b, (unsigned)(s_cnt[NW - 1] != INT_MIN));
         __syncthreads();
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
