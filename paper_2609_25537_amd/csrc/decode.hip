@@ -220,7 +220,8 @@ struct WaveState {
 
 // The ring count, fetched by a wave with a vector load issued after its
 // first K/V loads (nothing waits for it before they are in flight) and read
-// where a mask, a ring slot or the arrival needs it.
+// where a mask or a ring slot needs it, and at the end of the walk (stored
+// into LDS before the arrival).
 struct RingCount {
     int raw;
     bool loaded;  // wave-uniform
