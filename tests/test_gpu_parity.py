@@ -65,6 +65,10 @@ def _separated(B, N, D, seed, dup_every=0):
     (1, 1, 4, 1), (1, 7, 8, 0), (1, 7, 8, 7), (3, 33, 12, 5), (2, 1000, 64, 999),
     (4, 4096, 16, 512), (1, 32768, 8, 1024), (2, 32768, 8, 32768), (5, 2047, 260, 1),
     (65535, 6, 8, 2),  # the largest batch the host accepts (one grid row per sequence)
+    # the top-k keeps ceil(N / 1024) keys per thread rounded up to a power of two:
+    # the first size of each instantiation (1, 2, 4, 8, 16, 32 keys per thread)
+    (2, 1024, 8, 100), (2, 1025, 8, 100), (2, 2049, 8, 300), (2, 4097, 16, 300), (2, 8193, 8, 2000),
+    (1, 16385, 8, 64),
 ])
 def test_select_sizes(orc, B, N, D, k):
     keys, qv = _separated(B, N, D, seed=N + k)
