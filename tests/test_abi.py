@@ -366,3 +366,28 @@ def test_binding_refuses_host_tensors():
     with pytest.raises((ValueError, RuntimeError)):
         cmc.cmc_two_tier_decode(q, pool, pool, None, 4, None, None, None, 0.125, W=0,
                                 out=torch.zeros((1, 4, 64)), workspace=torch.zeros(1024, dtype=torch.uint8))
+
+
+def test_last_error_is_per_thread():
+    """cmc_last_error() is thread-local: two threads failing validation with
+    different arguments, many times over and at the same time (ctypes calls
+    release the GIL), each read back their own message."""
+    import threading
+    L = cmc.lib()
+    L.cmc_last_error.restype = ctypes.c_char_p
+    bad = []
+
+    def worker(k, n_iter=2000):
+        for _ in range(n_iter):
+            rc = _sel(B=1, N=4, k=k)  # k > N: the message names this thread's k
+            msg = L.cmc_last_error().decode()
+            if rc != cmc.CMC_ERR_INVALID_ARGUMENT or f"k={k} " not in msg:
+                bad.append((k, rc, msg))
+                return
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in (5, 7, 9, 11)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not bad, bad[:3]
