@@ -303,7 +303,11 @@ def test_bridge_validation(kw, code):
 
 def test_bridge_empty_and_workspace():
     assert _bridge(M=0, h=None) == cmc.CMC_OK
-    assert cmc.cmc_bridge_workspace_bytes(10, 128) >= 10 * 128 * 2
+    assert cmc.cmc_bridge_workspace_bytes(10, 128) == 2560  # M * F bf16, rounded up to 256
+    need = 49152 * 4096 * 2
+    assert cmc.cmc_bridge_workspace_bytes(49152, 4096) == need
+    assert _bridge(M=49152, F=4096, Hd=4096, wsb=need - 1) == cmc.CMC_ERR_WORKSPACE_TOO_SMALL
+    assert f"{need} bytes needed" in cmc.last_error()
 
 
 def _gather(**kw):
