@@ -70,12 +70,15 @@ def test_denoise_neighbourhoods(orc, dtype, g):
 @pytest.mark.parametrize("n,H,n_tokens", [
     (1, 8, None), (15, 8, [15, 0]), (16, 16, [16, 1]), (17, 128, [17, 2]), (65, 40, [65, 64]),
     (1000, 1280, [1000, 999]), (9000, 16, [9000, 8193]), (200, 1288, [200, 53]),
+    (26, 64, [26, 25]), (39, 96, [39, 13]), (52, 160, [52, 51]), (66, 256, [66, 14]),
 ])
 def test_denoise_sizes(orc, dtype, n, H, n_tokens):
     """Tile edges (8 tokens per wave for fp32; 16 - g rows per wave for
-    bf16), row widths that are not whole 32-column steps (8, 40, 1288), the
-    last token, empty and one-token sequences, and sequences longer than one
-    round of the selection scan (8192 positions)."""
+    bf16, 13 at g = 3: sequences of exactly 2, 3 and 4 waves, and of 5 and
+    one token), row
+    widths that are not whole 32-column steps (8, 40, 1288), the last token,
+    empty and one-token sequences, and sequences longer than one round of
+    the selection scan (8192 positions)."""
     rng = np.random.default_rng(n + H)
     e = rng.standard_normal((2, n, H)).astype(np.float32)
     e[:, 1:] += 0.2 * e[:, :-1]
