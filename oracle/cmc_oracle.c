@@ -419,7 +419,9 @@ int oracle_denoise_select(const double *max_cos, const int32_t *n_tokens, int B,
 /* CME-guided Tier-2 localization (appendix on Tier-2 window           */
 /* localization: alpha is the token offset of the chunk whose CME has */
 /* the largest norm; the midpoint heuristic uses alpha = |C|/2).  Each */
-/* segment contributes m^(c) consecutive rows of M (Sec. 2.3).         */
+/* segment contributes m^(c) consecutive rows, in segment order (the   */
+/* concatenation of the segments' CMEs, Sec. 2.2, which the decoder-   */
+/* ready rows of Sec. 2.3 keep).                                       */
 /* ------------------------------------------------------------------ */
 
 /*
