@@ -94,6 +94,9 @@ def parse():
                          "cache) to the JSON line; auto: with the default workload")
     ap.add_argument("--baseline-steps", type=int, default=4,
                     help="stack workloads: timed decode steps of the uncompressed-cache baseline (0: skip it)")
+    ap.add_argument("--selection-only", action="store_true",
+                    help="time only the Tier-1 selection (score pass + top-k) of a uniform decode workload, with "
+                         "fp32 keys and with the same keys as bf16, --steps calls each; prints its JSON object")
     return ap.parse_args()
 
 
@@ -635,6 +638,13 @@ def main():
 
     cmc.lib()  # fail loudly before any work if the HIP library is missing
     dev = torch.device("cuda:0")
+    if args.selection_only:
+        w = wl.get(args.workload)
+        if w.ragged or w.layers != 1:
+            print("bench.py: --selection-only takes a uniform single-layer decode workload", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(selection_leg(w.name, dev, reps=max(1, args.steps))), flush=True)
+        return
     if args.workload in wl.DENOISE_WORKLOADS:
         return main_denoise(args, wl.DENOISE_WORKLOADS[args.workload], dev)
     if args.workload in wl.BRIDGE_WORKLOADS:
