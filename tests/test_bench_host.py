@@ -135,3 +135,14 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+@pytest.mark.parametrize("workload", ["ragged_batch64", "llama_stack32"])
+def test_selection_only_takes_uniform_single_layer_workloads(workload):
+    """--selection-only times the uniform selection of one layer's batch; a
+    ragged batch or a layer stack is refused before any GPU work."""
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--selection-only", "--workload", workload],
+                       capture_output=True, text=True, timeout=180, cwd=ROOT)
+    assert r.returncode == 2, r.stderr[-2000:]
+    assert "uniform single-layer" in r.stderr
+    assert r.stdout == ""
