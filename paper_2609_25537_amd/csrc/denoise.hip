@@ -309,6 +309,112 @@ __global__ __launch_bounds__(256) void denoise_gram_kernel(DenoiseParams p) {
     }
 }
 
+// denoise_gram_wg_kernel (bf16): the same statistic with the four waves of a
+// workgroup on 64 consecutive rows, 16 each (one batch of whole rows per
+// wave, as above), scoring 64 - g tokens: only the last g rows are re-read
+// by the next workgroup, so 64 / (64 - g) rows are streamed per token
+// instead of 16 / (16 - g).  The dot products that straddle two waves come
+// from one more MFMA per k-step, the wave's own fragment against the next
+// wave's first g rows, which that wave hands over through LDS (lanes with
+// row < g, 16 bytes per k-step).  The norms of those rows are read from the
+// next wave's Gram diagonal.  Every barrier sits in control flow that is
+// uniform over the workgroup (the loop over groups, the sequence-end test and
+// the k batches depend only on the block, the sequence and H).
+template <int G>
+__global__ __launch_bounds__(256) void denoise_gram_wg_kernel(DenoiseParams p) {
+    constexpr int KB = CMC_DENOISE_GRAM_BATCH;
+    constexpr int TT = 64 - G;  // tokens per workgroup; rows i0 .. i0 + 63
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, q4 = lane >> 4;
+    const int nb = p.n_tokens ? clamp_tokens(p.n_tokens[b], p.n) : p.n;
+    const char *base = static_cast<const char *>(p.emb) + (size_t)b * p.n * p.H * 2;
+    const size_t row_bytes = (size_t)p.H * 2;
+    const int KS = (p.H + 31) / 32;
+    __shared__ uint4 s_slot[4][KB][4][G];  // wave w's rows 0 .. g-1, per k-step and column quarter
+    __shared__ float s_c[4][16][17];       // each wave's Gram matrix
+    __shared__ float s_x[4][16][G];        // each wave's rows against the next wave's first g rows
+
+    for (int i0 = blockIdx.x * TT; i0 < p.n; i0 += gridDim.x * TT) {  // uniform
+        if (i0 >= nb) {  // uniform: positions past the sequence have no statistic
+            for (int t = threadIdx.x; t < TT; t += 256) {
+                const int i = i0 + t;
+                if (i < p.n) {
+                    const size_t o = (size_t)b * p.n + i;
+                    if (p.max_cos) p.max_cos[o] = -INFINITY;
+                    p.pass[o] = 0;
+                }
+            }
+            continue;
+        }
+        const int row = i0 + 16 * wave + r16;
+        const bool on = row < nb;
+        const char *rb = base + (size_t)min(row, nb - 1) * row_bytes;
+        const bool whole = i0 + 64 <= nb && p.H % 32 == 0;  // uniform: no masking needed
+        floatx4 c = {0.f, 0.f, 0.f, 0.f}, x = {0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < KS; k0 += KB) {  // uniform
+            uint4 v[KB];
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                const int col = min((k0 + j) * 32 + 8 * q4, p.H - 8);
+                v[j] = *reinterpret_cast<const uint4 *>(rb + (size_t)col * 2);
+            }
+            if (!whole) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j)
+                    if (!on || (k0 + j) * 32 + 8 * q4 >= p.H) v[j] = make_uint4(0, 0, 0, 0);
+            }
+            if (wave > 0 && r16 < G) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) s_slot[wave][j][q4][r16] = v[j];
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                if (k0 + j < KS) {  // uniform
+                    const bf16x8 f = __builtin_bit_cast(bf16x8, v[j]);
+                    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, f, c, 0, 0, 0);
+                    if (wave < 3) {  // wave-uniform
+                        const uint4 u = r16 < G ? s_slot[wave + 1][j][q4][r16] : make_uint4(0, 0, 0, 0);
+                        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, __builtin_bit_cast(bf16x8, u), x, 0, 0, 0);
+                    }
+                }
+            }
+            if (k0 + KB < KS) __syncthreads();  // uniform: the slots are read before the next batch writes them
+        }
+        // C fragment: lane l, element e -> row 4 (l / 16) + e, column l % 16.
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            s_c[wave][4 * q4 + e][r16] = c[e];
+            if (r16 < G) s_x[wave][4 * q4 + e][r16] = x[e];
+        }
+        __syncthreads();
+        const int t = 16 * wave + lane;  // token of the workgroup (lanes < 16)
+        const int i = i0 + t;
+        if (lane < 16 && t < TT) {
+            float best = -INFINITY;
+            if (i < nb) {
+                const float ni = fmaxf(sqrtf(s_c[wave][lane][lane]), 1e-8f);
+#pragma unroll
+                for (int d = 1; d <= G; ++d) {
+                    if (i + d < nb) {
+                        const int u = lane + d;  // u >= 16 only below wave 3 (t < TT)
+                        const float dot = u < 16 ? s_c[wave][lane][u] : s_x[wave][lane][u - 16];
+                        const float nn = u < 16 ? s_c[wave][u][u] : s_c[min(wave + 1, 3)][u - 16][u - 16];
+                        best = fmaxf(best, dot / (ni * fmaxf(sqrtf(nn), 1e-8f)));
+                    }
+                }
+            }
+            if (i < p.n) {
+                const size_t o = (size_t)b * p.n + i;
+                if (p.max_cos) p.max_cos[o] = best;
+                p.pass[o] = (uint8_t)(i < nb && best >= p.tau);
+            }
+        }
+        __syncthreads();  // the Gram matrices are read before the next group writes them
+    }
+}
+
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kPerThread = 8;
@@ -440,12 +546,25 @@ __global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoisePara
 #define CMC_DENOISE_MFMA 1
 #endif
 
+// Build-time tuning knob: the smallest g that runs denoise_gram_wg_kernel
+// (64 rows per workgroup); smaller g run denoise_gram_kernel (16 rows per
+// wave).  On 64 GPT2-Large-sized contexts, per call (us), 16-row waves /
+// 64-row workgroups: g = 1 64.2-64.5 / 66.4-67.0, g = 2 66.1-66.3 /
+// 67.1-67.4, g = 3 69.4-69.5 / 68.1, g = 4 79.2-79.5 / 69.2-69.4 -- the
+// workgroup kernel costs about the same for every g (its barriers and the
+// straddling MFMAs), the per-wave kernel grows with the halo.
+#ifndef CMC_DENOISE_WG_MIN_G
+#define CMC_DENOISE_WG_MIN_G 3
+#endif
+
 template <int G>
 hipError_t launch_gram(const DenoiseParams &p, hipStream_t stream) {
-    constexpr int per_wg = 4 * (16 - G);
+    constexpr bool kWg = G >= CMC_DENOISE_WG_MIN_G;
+    constexpr int per_wg = kWg ? 64 - G : 4 * (16 - G);
     int gx = (p.n + per_wg - 1) / per_wg;
     if (CMC_DENOISE_WG_PER_SEQ > 0 && gx > CMC_DENOISE_WG_PER_SEQ) gx = CMC_DENOISE_WG_PER_SEQ;
-    denoise_gram_kernel<G><<<dim3(gx, p.B), 256, 0, stream>>>(p);
+    if constexpr (kWg) denoise_gram_wg_kernel<G><<<dim3(gx, p.B), 256, 0, stream>>>(p);
+    else denoise_gram_kernel<G><<<dim3(gx, p.B), 256, 0, stream>>>(p);
     return hipGetLastError();
 }
 
