@@ -908,7 +908,11 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
         // The last split merges all S partials in fixed split order.  Its
         // first batch of acc partials (up to kMB splits per dim pair) and all
         // (m, l) pairs are requested together, so the merge costs one round
-        // trip when S <= kMB; the (m, l) pairs are staged in LDS.
+        // trip when S <= kMB; the (m, l) pairs are staged in LDS.  The
+        // batch's loads are issued unconditionally (splits past S - 1 reload
+        // split S - 1 and are never used): as atomic loads they cannot be
+        // speculated, and a branch around each cost about a dozen
+        // instructions between the arrival and the merge's data.
         constexpr int kPairs = (G * DH / 2 + kThreads - 1) / kThreads;  // dim pairs per thread
         constexpr int kMB = kPairs >= 4 ? 8 : 16;
         const float *ml = p.part_ml + head * p.S * G * 2;
@@ -918,11 +922,9 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
             const int t = threadIdx.x + pr * kThreads;
-            const int g = (2 * t) / DH, d = (2 * t) % DH;
+            const int g = (2 * min(t, G * DH / 2 - 1)) / DH, d = (2 * min(t, G * DH / 2 - 1)) % DH;
 #pragma unroll
-            for (int j = 0; j < kMB; ++j)
-                a[pr][j] = (t < G * DH / 2 && j < p.S) ? coherent_load2(&ac[(j * G + g) * DH + d])
-                                                       : make_float2(0.f, 0.f);
+            for (int j = 0; j < kMB; ++j) a[pr][j] = coherent_load2(&ac[(min(j, p.S - 1) * G + g) * DH + d]);
         }
         for (int t = threadIdx.x; t < p.S * G; t += kThreads) {
             const float2 v = coherent_load2(&ml[2 * t]);
@@ -968,7 +970,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
                     }
                 }
             }
-            const float inv = den > 0.f ? 1.f / den : 0.f;
+            const float inv = den > 0.f ? __builtin_amdgcn_rcpf(den) : 0.f;  // within 1 ulp
             *reinterpret_cast<float2 *>(&outp[g * DH + d]) = make_float2(n0 * inv, n1 * inv);
         }
         if (threadIdx.x == 0)

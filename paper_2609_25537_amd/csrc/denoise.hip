@@ -374,9 +374,24 @@ __global__ __launch_bounds__(256) void denoise_gram_wg_kernel(DenoiseParams p) {
                 if (k0 + j < KS) {  // uniform
                     const bf16x8 f = __builtin_bit_cast(bf16x8, v[j]);
                     c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, f, c, 0, 0, 0);
-                    if (wave < 3) {  // wave-uniform
-                        const uint4 u = r16 < G ? s_slot[wave + 1][j][q4][r16] : make_uint4(0, 0, 0, 0);
-                        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, __builtin_bit_cast(bf16x8, u), x, 0, 0, 0);
+                }
+            }
+            if (wave < 3) {  // wave-uniform
+                // the next wave's fragments XB k-steps at a time: one LDS round
+                // trip per XB straddling MFMAs
+                constexpr int XB = 8;
+#pragma unroll
+                for (int j0 = 0; j0 < KB; j0 += XB) {
+                    uint4 u[XB];
+#pragma unroll
+                    for (int jj = 0; jj < XB; ++jj)
+                        u[jj] = (j0 + jj < KB && r16 < G) ? s_slot[wave + 1][min(j0 + jj, KB - 1)][q4][r16 % G]
+                                                          : make_uint4(0, 0, 0, 0);
+#pragma unroll
+                    for (int jj = 0; jj < XB; ++jj) {
+                        if (j0 + jj < KB && k0 + j0 + jj < KS)  // uniform
+                            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v[j0 + jj]),
+                                                                         __builtin_bit_cast(bf16x8, u[jj]), x, 0, 0, 0);
                     }
                 }
             }

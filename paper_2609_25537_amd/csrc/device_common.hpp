@@ -54,12 +54,25 @@ __device__ __forceinline__ float dpp_mov(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
                                                                 0xF, 0xF, false));
 }
+// The same exchange for a sum: with 0 as the value a lane outside the row
+// would read (none does: every pattern used stays inside a 16-lane row), the
+// compiler folds the exchange into the add (one v_add_f32 with a DPP
+// operand per step instead of a move and an add).
+template <int CTRL>
+__device__ __forceinline__ float dpp_sum_operand(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                   0xF, 0xF, true));
+}
 
 struct OpSum {
     __device__ __forceinline__ static float f(float a, float b) { return a + b; }
+    template <int CTRL>
+    __device__ __forceinline__ static float partner(float v) { return dpp_sum_operand<CTRL>(v); }
 };
 struct OpMax {
     __device__ __forceinline__ static float f(float a, float b) { return fmaxf(a, b); }
+    template <int CTRL>
+    __device__ __forceinline__ static float partner(float v) { return dpp_mov<CTRL>(v); }
 };
 
 // f(v, v of lane ^ 16) and f(v, v of lane ^ 32).  Each swap returns the pair
@@ -83,15 +96,15 @@ __device__ __forceinline__ float combine_xor32(float v) {
 // lane_reduce<Op, 16, 64> across the four 16-lane rows, etc.
 template <typename Op, int LO, int HI>
 __device__ __forceinline__ float lane_reduce(float v) {
-    if constexpr (LO <= 1 && HI > 1) v = Op::f(v, dpp_mov<0xB1>(v));          // ^1
-    if constexpr (LO <= 2 && HI > 2) v = Op::f(v, dpp_mov<0x4E>(v));          // ^2
+    if constexpr (LO <= 1 && HI > 1) v = Op::f(v, Op::template partner<0xB1>(v));     // ^1
+    if constexpr (LO <= 2 && HI > 2) v = Op::f(v, Op::template partner<0x4E>(v));     // ^2
     if constexpr (LO <= 4 && HI > 4) {
-        if constexpr (LO <= 1) v = Op::f(v, dpp_mov<0x141>(v));                // ^7 (after ^1,^2)
+        if constexpr (LO <= 1) v = Op::f(v, Op::template partner<0x141>(v));           // ^7 (after ^1,^2)
         else v = Op::f(v, __shfl_xor(v, 4));
     }
     if constexpr (LO <= 8 && HI > 8) {
-        if constexpr (LO <= 1) v = Op::f(v, dpp_mov<0x140>(v));                // ^15 (after ^1,^2,^7)
-        else v = Op::f(v, dpp_mov<0x128>(v));                                  // ^8 (row rotate 8)
+        if constexpr (LO <= 1) v = Op::f(v, Op::template partner<0x140>(v));           // ^15 (after ^1,^2,^7)
+        else v = Op::f(v, Op::template partner<0x128>(v));                             // ^8 (row rotate 8)
     }
     if constexpr (LO <= 16 && HI > 16) v = combine_xor16<Op>(v);
     if constexpr (LO <= 32 && HI > 32) v = combine_xor32<Op>(v);
