@@ -564,12 +564,11 @@ __global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoisePara
 // Build-time tuning knob: the smallest g that runs denoise_gram_wg_kernel
 // (64 rows per workgroup); smaller g run denoise_gram_kernel (16 rows per
 // wave).  On 64 GPT2-Large-sized contexts, per call (us), 16-row waves /
-// 64-row workgroups: g = 1 64.2-64.5 / 66.4-67.0, g = 2 66.1-66.3 /
-// 67.1-67.4, g = 3 69.4-69.5 / 68.1, g = 4 79.2-79.5 / 69.2-69.4 -- the
-// workgroup kernel costs about the same for every g (its barriers and the
-// straddling MFMAs), the per-wave kernel grows with the halo.
+// 64-row workgroups: g = 1 64.4-64.5 / 64.4-64.5, g = 2 65.8-65.9 /
+// 64.9-65.0, g = 3 68.0-68.4 / 66.0-66.3, g = 4 68.7-69.3 (with 16-row
+// waves 79.1-79.5) / 67.1-67.7 -- the per-wave kernel grows with the halo.
 #ifndef CMC_DENOISE_WG_MIN_G
-#define CMC_DENOISE_WG_MIN_G 3
+#define CMC_DENOISE_WG_MIN_G 2
 #endif
 
 template <int G>
