@@ -438,14 +438,18 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
             c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo.hi[i], kbf, c, 0, 0, 0);                 \
             c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo.lo[i], kbf, c, 0, 0, 0);                 \
         }                                                                                            \
-        float pk[G];                                                                                 \
+        float pk[G], mbs[G];                                                                         \
+        /* the G heads' maxima first, in straight-line code, so their chains interleave */            \
+        _Pragma("unroll") for (int g = 0; g < G; ++g) mbs[g] = lane_reduce<OpMax, 1, 16>(kval ? c[g] : -INFINITY); \
         _Pragma("unroll") for (int g = 0; g < G; ++g) {                                              \
             const float sc = kval ? c[g] : -INFINITY;                                                \
-            const float mb = lane_reduce<OpMax, 1, 16>(sc);                                          \
+            const float mb = mbs[g];                                                                 \
             if (mb > st.m[g]) {                                                                      \
-                const float alpha = fast_exp2(st.m[g] - mb);                                         \
-                st.l[g] *= alpha;                                                                    \
-                _Pragma("unroll") for (int i = 0; i < VD; ++i) st.acc[g][i] *= alpha;                \
+                if (st.m[g] != -INFINITY) { /* before the first valid key l and acc are 0 */         \
+                    const float alpha = fast_exp2(st.m[g] - mb);                                     \
+                    st.l[g] *= alpha;                                                                \
+                    _Pragma("unroll") for (int i = 0; i < VD; ++i) st.acc[g][i] *= alpha;            \
+                }                                                                                    \
                 st.m[g] = mb;                                                                        \
             }                                                                                        \
             /* a masked key weighs 0 (also before any valid key: m is -inf) */                       \
@@ -740,7 +744,7 @@ __device__ __forceinline__ float combine_waves(const float (&sm)[NW][G], const f
     if (M != -INFINITY) {
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
-            const float f = exp2f(sm[w][g] - M);
+            const float f = fast_exp2(sm[w][g] - M);
             num = fmaf(f, sa[w][g][d], num);
             den = fmaf(f, sl[w][g], den);
         }
@@ -880,7 +884,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
             const int g = t / DH, d = t % DH;
             float num, den;
             combine_waves<NW, G, DH>(s_m, s_l, s_acc, g, d, num, den);
-            outp[t] = den > 0.f ? num / den : 0.f;
+            outp[t] = den > 0.f ? num * __builtin_amdgcn_rcpf(den) : 0.f;
         }
         CMC_BUMP();
     } else {
@@ -946,7 +950,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
 #pragma unroll
                 for (int j = 0; j < kMB; ++j) {
                     if (j < p.S) {
-                        const float f = exp2f(s_ml[(j * G + g) * 2] - M);
+                        const float f = fast_exp2(s_ml[(j * G + g) * 2] - M);
                         den = fmaf(f, s_ml[(j * G + g) * 2 + 1], den);
                         n0 = fmaf(f, a[pr][j].x, n0);
                         n1 = fmaf(f, a[pr][j].y, n1);
@@ -962,7 +966,7 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
                     for (int j = 0; j < kMB; ++j) {
                         if (q0 + j < p.S) {
                             const int q = q0 + j;
-                            const float f = exp2f(s_ml[(q * G + g) * 2] - M);
+                            const float f = fast_exp2(s_ml[(q * G + g) * 2] - M);
                             den = fmaf(f, s_ml[(q * G + g) * 2 + 1], den);
                             n0 = fmaf(f, x[j].x, n0);
                             n1 = fmaf(f, x[j].y, n1);
