@@ -943,18 +943,31 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
             const int t = threadIdx.x + pr * kThreads;
             if (t >= G * DH / 2) continue;
             const int g = (2 * t) / DH, d = (2 * t) % DH;
+            // The first batch's (m, l) pairs read together (splits past S - 1
+            // read split S - 1 again), and its terms masked by selects rather
+            // than branches: no LDS round trip waits for another.  The max
+            // is unchanged by the repeats, and the sums take the splits in
+            // order as before.
+            float mj[kMB], lj[kMB];
+#pragma unroll
+            for (int j = 0; j < kMB; ++j) {
+                const float2 v = *reinterpret_cast<const float2 *>(&s_ml[(min(j, p.S - 1) * G + g) * 2]);
+                mj[j] = v.x;
+                lj[j] = v.y;
+            }
             float M = -INFINITY;
-            for (int q = 0; q < p.S; ++q) M = fmaxf(M, s_ml[(q * G + g) * 2]);
+#pragma unroll
+            for (int j = 0; j < kMB; ++j) M = fmaxf(M, mj[j]);
+            for (int q = kMB; q < p.S; ++q) M = fmaxf(M, s_ml[(q * G + g) * 2]);
             float n0 = 0.f, n1 = 0.f, den = 0.f;
             if (M != -INFINITY) {
 #pragma unroll
                 for (int j = 0; j < kMB; ++j) {
-                    if (j < p.S) {
-                        const float f = fast_exp2(s_ml[(j * G + g) * 2] - M);
-                        den = fmaf(f, s_ml[(j * G + g) * 2 + 1], den);
-                        n0 = fmaf(f, a[pr][j].x, n0);
-                        n1 = fmaf(f, a[pr][j].y, n1);
-                    }
+                    const bool in = j < p.S;
+                    const float f = fast_exp2(mj[j] - M);
+                    den = in ? fmaf(f, lj[j], den) : den;
+                    n0 = in ? fmaf(f, a[pr][j].x, n0) : n0;
+                    n1 = in ? fmaf(f, a[pr][j].y, n1) : n1;
                 }
                 for (int q0 = kMB; q0 < p.S; q0 += kMB) {
                     float2 x[kMB];
