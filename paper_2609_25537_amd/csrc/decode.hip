@@ -736,18 +736,27 @@ template <int NW, int G, int DH>
 __device__ __forceinline__ float combine_waves(const float (&sm)[NW][G], const float (&sl)[NW][G],
                                                const float (&sa)[NW][G][DH], int g, int d, float &num,
                                                float &den) {
-    float M = sm[0][g];
+    // Every LDS read issued before the first wait, and no branch on M: with
+    // no valid key in any wave (M = -inf) every weight is exp2(-inf) = 0
+    // against finite accumulators (zeros), so num = den = 0.
+    float mw[NW], lw[NW], aw[NW];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) M = fmaxf(M, sm[w][g]);
+    for (int w = 0; w < NW; ++w) {
+        mw[w] = sm[w][g];
+        lw[w] = sl[w][g];
+        aw[w] = sa[w][g][d];
+    }
+    float M = mw[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, mw[w]);
+    const float Mc = M == -INFINITY ? 0.f : M;
     num = 0.f;
     den = 0.f;
-    if (M != -INFINITY) {
 #pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            const float f = fast_exp2(sm[w][g] - M);
-            num = fmaf(f, sa[w][g][d], num);
-            den = fmaf(f, sl[w][g], den);
-        }
+    for (int w = 0; w < NW; ++w) {
+        const float f = fast_exp2(mw[w] - Mc);
+        num = fmaf(f, aw[w], num);
+        den = fmaf(f, lw[w], den);
     }
     return M;
 }
@@ -922,6 +931,14 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
         const float *ml = p.part_ml + head * p.S * G * 2;
         const float *ac = p.part_acc + head * p.S * G * DH;
         float *s_ml = &s_acc[0][0][0];  // reuse: S*G*2 <= NW*G*DH floats (S <= 2*DH)
+        // The (m, l) pairs are requested first (loads complete in issue
+        // order, and the max and the weights need only them), and the barrier
+        // that publishes them in LDS waits for LDS alone: the acc partials
+        // may still be in flight while the weights are computed, and their
+        // first use waits for them.
+        const bool ml_first = threadIdx.x < p.S * G;  // the first kThreads pairs
+        float2 mlv = make_float2(0.f, 0.f);
+        if (ml_first) mlv = coherent_load2(&ml[2 * threadIdx.x]);
         float2 a[kPairs][kMB];
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
@@ -930,14 +947,21 @@ __global__ __launch_bounds__(NW * kWave) void decode_kernel(const void *cme_k, c
 #pragma unroll
             for (int j = 0; j < kMB; ++j) a[pr][j] = coherent_load2(&ac[(min(j, p.S - 1) * G + g) * DH + d]);
         }
-        for (int t = threadIdx.x; t < p.S * G; t += kThreads) {
+        if (ml_first) {
+            s_ml[2 * threadIdx.x] = mlv.x;
+            s_ml[2 * threadIdx.x + 1] = mlv.y;
+        }
+        for (int t = threadIdx.x + kThreads; t < p.S * G; t += kThreads) {
             const float2 v = coherent_load2(&ml[2 * t]);
             s_ml[2 * t] = v.x;
             s_ml[2 * t + 1] = v.y;
         }
         // this workgroup completes the pair; the arrival overlaps the merge loads
         if (bump && threadIdx.x == 0) prev = arrive_once(p.seq_counter, b, (unsigned)(s_cnt[NW - 1] != INT_MIN));
-        __syncthreads();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only: vmcnt and expcnt at their maxima
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int pr = 0; pr < kPairs; ++pr) {
             const int t = threadIdx.x + pr * kThreads;
