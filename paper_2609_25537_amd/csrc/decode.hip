@@ -440,7 +440,7 @@ __device__ __forceinline__ void mfma_phase(const DecodeParams &p, int b, int kvh
         }                                                                                            \
         float pk[G], mbs[G];                                                                         \
         /* the G heads' maxima first, in straight-line code, so their chains interleave */            \
-        _Pragma("unroll") for (int g = 0; g < G; ++g) mbs[g] = lane_reduce<OpMax, 1, 16>(kval ? c[g] : -INFINITY); \
+        _Pragma("unroll") for (int g = 0; g < G; ++g) mbs[g] = lane_max16(kval ? c[g] : -INFINITY);      \
         _Pragma("unroll") for (int g = 0; g < G; ++g) {                                              \
             const float sc = kval ? c[g] : -INFINITY;                                                \
             const float mb = mbs[g];                                                                 \

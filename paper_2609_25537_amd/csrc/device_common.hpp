@@ -75,6 +75,25 @@ struct OpMax {
     __device__ __forceinline__ static float partner(float v) { return dpp_mov<CTRL>(v); }
 };
 
+// The max over aligned 16-lane groups on order-preserving integer keys (a
+// float's bits with the magnitude bits flipped when the sign is set, so the
+// signed integer order is the float order, -0 below +0): the exchange folds
+// into v_max_i32 (one instruction per step), where fmaxf needs a move and
+// two NaN-quieting maxima besides.  Same result as lane_reduce<OpMax, 1, 16>
+// for inputs without NaN.
+__device__ __forceinline__ int f32_order_key(float x) {
+    const int b = __float_as_int(x);
+    return b ^ (int)((unsigned)(b >> 31) >> 1);
+}
+__device__ __forceinline__ float lane_max16(float v) {
+    int k = f32_order_key(v);
+    k = max(k, __builtin_amdgcn_update_dpp(0, k, 0xB1, 0xF, 0xF, true));   // ^1
+    k = max(k, __builtin_amdgcn_update_dpp(0, k, 0x4E, 0xF, 0xF, true));   // ^2
+    k = max(k, __builtin_amdgcn_update_dpp(0, k, 0x141, 0xF, 0xF, true));  // ^7
+    k = max(k, __builtin_amdgcn_update_dpp(0, k, 0x140, 0xF, 0xF, true));  // ^15
+    return __int_as_float(k ^ (int)((unsigned)(k >> 31) >> 1));
+}
+
 // f(v, v of lane ^ 16) and f(v, v of lane ^ 32).  Each swap returns the pair
 // {v, partner's v} in a lane-dependent order; the combine ops are
 // commutative, so the result is the same bits in either order.
