@@ -321,7 +321,7 @@ __global__ __launch_bounds__(256) void denoise_gram_kernel(DenoiseParams p) {
 // uniform over the workgroup (the loop over groups, the sequence-end test and
 // the k batches depend only on the block, the sequence and H).
 template <int G>
-__global__ __launch_bounds__(256) void denoise_gram_wg_kernel(DenoiseParams p) {
+__global__ __launch_bounds__(256, 2) void denoise_gram_wg_kernel(DenoiseParams p) {
     constexpr int KB = CMC_DENOISE_GRAM_BATCH;
     constexpr int TT = 64 - G;  // tokens per workgroup; rows i0 .. i0 + 63
     const int b = blockIdx.y;
@@ -369,32 +369,41 @@ __global__ __launch_bounds__(256) void denoise_gram_wg_kernel(DenoiseParams p) {
                 for (int j = 0; j < KB; ++j) s_slot[wave][j][q4][r16] = v[j];
             }
             __syncthreads();
-#pragma unroll
-            for (int j = 0; j < KB; ++j) {
-                if (k0 + j < KS) {  // uniform
-                    const bf16x8 f = __builtin_bit_cast(bf16x8, v[j]);
-                    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, f, c, 0, 0, 0);
-                }
-            }
-            if (wave < 3) {  // wave-uniform
-                // the next wave's fragments XB k-steps at a time: one LDS round
-                // trip per XB straddling MFMAs
-                constexpr int XB = 8;
-#pragma unroll
-                for (int j0 = 0; j0 < KB; j0 += XB) {
-                    uint4 u[XB];
-#pragma unroll
-                    for (int jj = 0; jj < XB; ++jj)
-                        u[jj] = (j0 + jj < KB && r16 < G) ? s_slot[wave + 1][min(j0 + jj, KB - 1)][q4][r16 % G]
-                                                          : make_uint4(0, 0, 0, 0);
-#pragma unroll
-                    for (int jj = 0; jj < XB; ++jj) {
-                        if (j0 + jj < KB && k0 + j0 + jj < KS)  // uniform
-                            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v[j0 + jj]),
-                                                                         __builtin_bit_cast(bf16x8, u[jj]), x, 0, 0, 0);
-                    }
-                }
-            }
+            // A whole batch (every batch when KB divides H / 32) runs without
+            // a branch per k-step, so the scheduler can overlap the straddling
+            // operands' LDS reads with the MFMAs; a partial last batch guards
+            // each k-step (uniform branches).
+#define CMC_DN_MMA(LIVE_)                                                                                      \
+    do {                                                                                                       \
+        _Pragma("unroll") for (int j = 0; j < KB; ++j) {                                                       \
+            if (LIVE_(j)) {                                                                                    \
+                const bf16x8 f = __builtin_bit_cast(bf16x8, v[j]);                                             \
+                c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, f, c, 0, 0, 0);                                 \
+            }                                                                                                  \
+        }                                                                                                      \
+        if (wave < 3) { /* wave-uniform */                                                                     \
+            /* the next wave's fragments XB k-steps at a time: one LDS round trip per XB straddling MFMAs */  \
+            constexpr int XB = 8;                                                                              \
+            _Pragma("unroll") for (int j0 = 0; j0 < KB; j0 += XB) {                                            \
+                uint4 u[XB];                                                                                   \
+                _Pragma("unroll") for (int jj = 0; jj < XB; ++jj)                                              \
+                    u[jj] = (j0 + jj < KB && r16 < G) ? s_slot[wave + 1][min(j0 + jj, KB - 1)][q4][r16 % G]    \
+                                                      : make_uint4(0, 0, 0, 0);                                \
+                _Pragma("unroll") for (int jj = 0; jj < XB; ++jj) {                                            \
+                    if (j0 + jj < KB && LIVE_(j0 + jj))                                                        \
+                        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v[j0 + jj]),    \
+                                                                     __builtin_bit_cast(bf16x8, u[jj]), x, 0, 0, 0); \
+                }                                                                                              \
+            }                                                                                                  \
+        }                                                                                                      \
+    } while (0)
+#define CMC_DN_ALL(j_) true
+#define CMC_DN_IN(j_) (k0 + (j_) < KS)
+            if (k0 + KB <= KS) CMC_DN_MMA(CMC_DN_ALL);  // uniform
+            else CMC_DN_MMA(CMC_DN_IN);
+#undef CMC_DN_ALL
+#undef CMC_DN_IN
+#undef CMC_DN_MMA
             if (k0 + KB < KS) __syncthreads();  // uniform: the slots are read before the next batch writes them
         }
         // C fragment: lane l, element e -> row 4 (l / 16) + e, column l % 16.
