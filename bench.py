@@ -888,8 +888,8 @@ def main_denoise(args, w, dev):
                    "retention": round(kept / tok, 4)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "denoise_gram_wg_kernel (bf16 embeddings, g >= 2; denoise_gram_kernel at g = 1, "
-                               "denoise_score_kernel for fp32) + denoise_select_kernel (one cmc_denoise call)",
+                     "kernel": "denoise_gram_wg_kernel (bf16 embeddings; denoise_score_kernel for fp32) "
+                               "+ denoise_select_kernel (one cmc_denoise call)",
                      "bytes_per_launch": nbytes, "launch_us": round(t_call * 1e6, 3)},
         "cpu_baseline": cpu,
     }

@@ -573,11 +573,11 @@ __global__ __launch_bounds__(kSelThreads) void denoise_select_kernel(DenoisePara
 // Build-time tuning knob: the smallest g that runs denoise_gram_wg_kernel
 // (64 rows per workgroup); smaller g run denoise_gram_kernel (16 rows per
 // wave).  On 64 GPT2-Large-sized contexts, per call (us), 16-row waves /
-// 64-row workgroups: g = 1 64.4-64.5 / 64.4-64.5, g = 2 65.8-65.9 /
-// 64.9-65.0, g = 3 68.0-68.4 / 66.0-66.3, g = 4 68.7-69.3 (with 16-row
-// waves 79.1-79.5) / 67.1-67.7 -- the per-wave kernel grows with the halo.
+// 64-row workgroups: g = 1 63.8-64.2 / 63.3-63.5, g = 2 65.8-65.9 /
+// 63.9, g = 3 68.0-68.4 / 65.1-65.2, g = 4 68.7-69.3 (with 16-row waves
+// 79.1-79.5) / 65.6-66.0 -- the per-wave kernel grows with the halo.
 #ifndef CMC_DENOISE_WG_MIN_G
-#define CMC_DENOISE_WG_MIN_G 2
+#define CMC_DENOISE_WG_MIN_G 1
 #endif
 
 template <int G>
