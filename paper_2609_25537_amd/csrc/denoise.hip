@@ -319,7 +319,9 @@ __global__ __launch_bounds__(256) void denoise_gram_kernel(DenoiseParams p) {
 // row < g, 16 bytes per k-step).  The norms of those rows are read from the
 // next wave's Gram diagonal.  Every barrier sits in control flow that is
 // uniform over the workgroup (the loop over groups, the sequence-end test and
-// the k batches depend only on the block, the sequence and H).
+// the k batches depend only on the block, the sequence and H).  Two
+// workgroups per CU (two waves per SIMD, at most 256 VGPRs each): the
+// branch-free batches would otherwise be scheduled into more registers.
 template <int G>
 __global__ __launch_bounds__(256, 2) void denoise_gram_wg_kernel(DenoiseParams p) {
     constexpr int KB = CMC_DENOISE_GRAM_BATCH;
